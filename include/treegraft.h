@@ -1,0 +1,236 @@
+/*
+ * treegraft.h - C ABI of libtreegraft.so, the MI355X (gfx950) hot path of
+ * tree-based speculative decoding with a shared, multi-drafter draft tree
+ * (TreeGraft: Adaptive Multi-Drafter Grafting for Tree-Based Speculative
+ * Decoding).
+ *
+ * Four calls:
+ *   tg_tree_verify_attention  target-side tree attention of a draft tree
+ *                             against a prefix KV cache (Alg. 3 mask; Sec. 3.1)
+ *   tg_tree_expand_topk       one standard expansion step (Sec. 3.1; Alg. 1)
+ *   tg_tree_rescore_graft     one middle-drafter step: expanded pool,
+ *                             rescoring, reselection, non-destructive graft
+ *                             (Sec. 3.2; Alg. 2, middle branch)
+ *   tg_tree_accept            greedy (temperature 0) acceptance of the longest
+ *                             draft path matching the target (Sec. 3.2,
+ *                             "Distribution preservation"; App. E)
+ *
+ * Conventions shared by every call
+ *   - Every pointer argument is DEVICE memory owned by the caller, except the
+ *     tg_tree struct itself, which is a host struct holding device pointers.
+ *     The library never allocates per call; scratch memory is the caller's
+ *     `workspace`, sized by the matching *_workspace() query.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream).  The returned tg_status reports host-side argument checks and
+ *     the kernel launch only.
+ *   - Data errors that only the device can see are OR-ed into `*d_err` (a
+ *     device uint32, optional: NULL disables reporting).  Each bit has a
+ *     documented safe fallback, so kernels always complete.  Read it after
+ *     synchronising the stream.
+ *   - Arrays are dense, row-major, with the shapes written next to each
+ *     argument.  Node ids are dense per tree and topological: a node's parent
+ *     id is smaller than its own.  The root is implicit: id -1, cumulative
+ *     score 0, depth 0.
+ *   - Scores are natural logs: an edge score p(u) of the paper is stored as
+ *     logp = log p(u), a path score s(v) = prod p(u) as cum = log s(v).
+ *     logp = fl(x - lse) and cum = fl(cum_parent + logp) are single IEEE fp32
+ *     operations (x = the token's fp32 logit, lse = the row's log-sum-exp).
+ *   - Rankings: a logits row's top-k tokens are ordered by (logit desc,
+ *     token asc); node rankings use (cum desc, depth asc, id asc), the key
+ *     Alg. 3 fixes for pruning.  -0.0 ranks equal to +0.0.
+ *   - The library holds no mutable global state and is reentrant.
+ */
+#ifndef TREEGRAFT_H
+#define TREEGRAFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TG_OK = 0,
+  TG_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, inconsistent shapes */
+  TG_ERR_UNSUPPORTED = 2,  /* valid but outside the supported limits below   */
+  TG_ERR_WORKSPACE = 3,    /* workspace NULL or smaller than the query says   */
+  TG_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed      */
+} tg_status;
+
+typedef enum { TG_F32 = 0, TG_BF16 = 1 } tg_dtype;
+
+/* Device error word bits and the fallback each one triggers. */
+#define TG_DERR_BAD_PARENT 1u  /* parent[i] >= i or < -1: read as -1            */
+#define TG_DERR_CAPACITY 2u    /* append would exceed tree cap: that tree is    *
+                                * left unchanged; accept: an acceptable node    *
+                                * deeper than max_depth was ignored             */
+#define TG_DERR_NONFINITE 4u   /* NaN or +inf logit: read as -inf               */
+#define TG_DERR_BAD_PREFIX 8u  /* prefix_len < 0 or prefix_len + N > S_max:     *
+                                * that sequence's outputs are written as zeros  */
+#define TG_DERR_BAD_NODE 16u   /* frontier id outside [-1, n_nodes), strong-    *
+                                * logits rows < n_nodes + 1, or a tree larger   *
+                                * than a kernel limit: that tree is unchanged   */
+
+#define TG_NO_NODE (-2)        /* padding of frontier outputs (-1 is the root) */
+
+/* Limits (TG_ERR_UNSUPPORTED outside them). */
+#define TG_MAX_TOPK 64         /* K of expand, M of rescore                     */
+#define TG_MAX_CAP 4096        /* tree capacity (nodes per tree, root excluded) */
+#define TG_MAX_EXPAND_CHILDREN 8192 /* F * K of one expand call                */
+#define TG_MAX_VERIFY_NODES 1024    /* N of one verify call                    */
+
+/*
+ * Caller-owned draft tree, structure of arrays, one row of `cap` slots per
+ * batch element (Sec. 3.1: each non-root node stores its token, its edge
+ * score and its path score; Sec. 3.2: the middle drafter's visited set P).
+ * Slots [0, n_nodes[b]) are live.  `visited` and `root_visited` hold P_k
+ * membership (1 = entered a middle-drafter pool before).
+ */
+typedef struct {
+  int32_t *parent;        /* [B, cap] parent id, -1 = root                   */
+  int32_t *token;         /* [B, cap] token id                               */
+  int32_t *depth;         /* [B, cap] depth (root 0); must equal the length  *
+                           * of the parent chain                             */
+  float *logp;            /* [B, cap] fp32 log edge score                    */
+  float *cum;             /* [B, cap] fp32 log path score                    */
+  uint8_t *visited;       /* [B, cap] 0/1                                    */
+  uint8_t *root_visited;  /* [B]      0/1                                    */
+  int32_t *n_nodes;       /* [B]      live node count, updated by appends    */
+  int32_t cap;            /* slots per batch element, <= TG_MAX_CAP          */
+} tg_tree;
+
+const char *tg_status_str(tg_status s);
+
+/* ------------------------------------------------------------------------ */
+/* Tree-verify attention (Alg. 3 mask; Sec. 3.1 root = verified prefix).     */
+/*
+ * For batch b, tree node i and query head h (KV head g = h / (Hq / Hkv)):
+ * node i attends to the prefix cache positions [0, L_b) and to the tree slots
+ * L_b + a for every a on its root-to-node path (its ancestors and itself), i.e.
+ * mask(i, j) = 1 iff j is the root (the prefix), an ancestor of i, or i.
+ *   out = softmax(sm_scale * q K^T) V over those keys.
+ *
+ * q          [B, N, Hq, D]       dtype
+ * k_cache    [B, Hkv, S_max, D]  dtype; prefix at [0, L_b), the N tree nodes'
+ * v_cache    [B, Hkv, S_max, D]  keys/values at [L_b, L_b + N)
+ * parent     [B, N] int32, parent[i] in [-1, i-1]; -1 = hangs under the prefix
+ * prefix_len [B] int32 (device), L_b >= 0 and L_b + N <= S_max
+ * out        [B, N, Hq, D]       dtype (fp32 accumulation inside)
+ * D in {64, 128}; Hq % Hkv == 0; 1 <= N <= TG_MAX_VERIFY_NODES.
+ * dtype TG_BF16 runs the MFMA kernel; TG_F32 runs an fp32 VALU kernel.
+ * Device errors: BAD_PARENT (that parent read as -1), BAD_PREFIX (zeros).
+ */
+size_t tg_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
+                                     int S_max, tg_dtype dtype);
+
+tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
+                                   const void *v_cache, const int32_t *parent,
+                                   const int32_t *prefix_len, void *out, int B,
+                                   int N, int Hq, int Hkv, int D, int S_max,
+                                   float sm_scale, tg_dtype dtype,
+                                   void *workspace, size_t ws_bytes,
+                                   uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* One expansion step (Sec. 3.1; Alg. 1).                                   */
+/*
+ * For tree b and each live frontier row f < F_b (F_b = n_frontier[b], or F
+ * when n_frontier is NULL), row logits[b, f, :] are the drafter's next-token
+ * logits at frontier node v = frontier[b, f] (-1 = root):
+ *   lse_f = log sum_t exp(x_t)                      (fp32, exported in row_lse)
+ *   top-K tokens y_j of the row, j = 0..K-1         (logit desc, token asc)
+ *   child (f, j): id n_b + f*K + j, parent v, token y_j, depth depth(v)+1,
+ *                 logp = fl(x_{y_j} - lse_f), cum = fl(cum(v) + logp),
+ *                 visited 0.
+ * All F_b*K children are attached (n_nodes[b] += F_b*K).  next_frontier[b]
+ * receives the ids of the best min(N, F_b*K) new children by (cum desc,
+ * depth asc, id asc), best first, padded with TG_NO_NODE; n_next[b] their
+ * count.  A row whose logits are all -inf has lse -inf and gives logp -inf.
+ *
+ * logits        [B, F, V] fp32
+ * frontier      [B, F] int32, ids in [-1, n_nodes[b])
+ * n_frontier    [B] int32 or NULL
+ * row_lse       [B, F] fp32 out (rows f >= F_b untouched)
+ * next_frontier [B, N] int32 out;  n_next [B] int32 out
+ * 1 <= K <= min(V, TG_MAX_TOPK); 1 <= N; F*K <= TG_MAX_EXPAND_CHILDREN.
+ * Device errors: NONFINITE; BAD_NODE or CAPACITY leave tree b unchanged
+ * (n_next[b] = 0, row_lse still written).
+ */
+size_t tg_expand_topk_workspace(int B, int F, int V, int K, int N);
+
+tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
+                              const int32_t *frontier,
+                              const int32_t *n_frontier, int B, int F, int V,
+                              int K, int N, float *row_lse,
+                              int32_t *next_frontier, int32_t *n_next,
+                              void *workspace, size_t ws_bytes,
+                              uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* One middle-drafter step (Sec. 3.2 candidate-pool equation; Alg. 2).      */
+/*
+ * strong_logits[b, r, :] are the middle drafter's next-token logits at the
+ * root (r = 0) and at node r-1 (r >= 1); rows of nodes the drafter ran on in
+ * an earlier step are its cached logits.  For tree b:
+ *   1. pool C = {v < n_b : !visited[v]}, plus the root while !root_visited.
+ *   2. for each non-root v in C: logp[v] = fl(x - lse) with x the logit of
+ *      token[v] in row parent[v]+1 and lse that row's log-sum-exp; then, in
+ *      parent-before-child order, cum[v] = fl(cum[parent] + logp[v]).
+ *   3. graft frontier F = the best min(W, |C|) of C by (cum desc, depth asc,
+ *      id asc) (root: id -1, cum 0, depth 0).
+ *   4. non-destructive graft: for frontier rank f and each of the top-M
+ *      tokens (rank j) of row F[f]+1, attach a NEW child with id
+ *      n_b + f*M + j, parent F[f], logp = fl(x - lse), cum = fl(cum(F[f]) +
+ *      logp), depth depth(F[f]) + 1, visited 0.  No existing node's parent,
+ *      token or depth is written.
+ *   5. P <- P u C: visited[0, n_b) = 1, root_visited = 1; n_b += |F|*M.
+ * row_lse[b, r] is written for the rows the step reads: v+1 and parent(v)+1
+ * for v in C (other rows untouched).  graft_frontier[b] = F (ids, -1 = root),
+ * padded with TG_NO_NODE; n_graft[b] = |F|.
+ *
+ * strong_logits  [B, R, V] fp32, R >= n_nodes[b] + 1 for every b
+ * row_lse        [B, R] fp32 out;  graft_frontier [B, W] int32 out;
+ * n_graft        [B] int32 out
+ * 1 <= M <= min(V, TG_MAX_TOPK); 1 <= W; cap <= TG_MAX_CAP; flags = 0.
+ * Device errors: NONFINITE; BAD_NODE (R too small) or CAPACITY
+ * (n_b + |F|*M > cap) leave tree b unchanged with n_graft[b] = 0.
+ */
+size_t tg_rescore_graft_workspace(int B, int R, int V, int W, int M, int cap);
+
+tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
+                                int B, int R, int V, int W, int M,
+                                uint32_t flags, float *row_lse,
+                                int32_t *graft_frontier, int32_t *n_graft,
+                                void *workspace, size_t ws_bytes,
+                                uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Greedy acceptance (temperature 0; Sec. 3.2; App. E).                     */
+/*
+ * greedy[b, 0] is the target's arg-max token after the prefix (the root),
+ * greedy[b, 1+i] its arg-max after node i.  A node is acceptable iff every
+ * node u on its root path has token[u] == greedy[b, parent[u]+1].  The
+ * accepted node is the deepest acceptable node of depth <= max_depth (ties
+ * to the smallest id); accept_len[b] = its depth (number of accepted draft
+ * tokens, 0 if none), accept_path[b] = its root path (node ids, root first,
+ * padded with -1), bonus[b] = greedy[b, accepted+1] (greedy[b, 0] if none).
+ *
+ * parent, token [B, cap] int32; n_nodes [B] int32 (<= cap, <= TG_MAX_CAP)
+ * greedy        [B, cap + 1] int32
+ * accept_len [B], accept_path [B, max_depth], bonus [B]  int32 out
+ * Device errors: BAD_PARENT (read as -1); CAPACITY (an acceptable node
+ * deeper than max_depth was ignored); BAD_NODE (n_nodes > cap: tree treated
+ * as empty).
+ */
+tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
+                         const int32_t *n_nodes, const int32_t *greedy, int B,
+                         int cap, int max_depth, int32_t *accept_len,
+                         int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
+                         void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREEGRAFT_H */

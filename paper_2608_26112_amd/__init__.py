@@ -1,0 +1,303 @@
+"""Python binding of libtreegraft.so: the MI355X tree-verify / tree-expand path.
+
+Argument marshalling only: every call forwards torch tensors' device pointers
+and the current HIP stream to the C ABI declared in include/treegraft.h; all
+computation runs in the library's HIP kernels.  There is no CPU fallback: a
+missing library or a non-GPU tensor is an error.
+
+Calls (same names as the C ABI without the ``tg_`` prefix):
+  verify_attention  tree attention over a prefix KV cache (Alg. 3 mask)
+  expand_topk       one expansion step (Sec. 3.1; Alg. 1)
+  rescore_graft     one middle-drafter step (Sec. 3.2; Alg. 2)
+  accept            greedy acceptance (temperature 0)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtreegraft.so")
+
+# status codes, dtypes, device error bits and limits of include/treegraft.h
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+F32, BF16 = 0, 1
+DERR_BAD_PARENT = 1
+DERR_CAPACITY = 2
+DERR_NONFINITE = 4
+DERR_BAD_PREFIX = 8
+DERR_BAD_NODE = 16
+NO_NODE = -2
+MAX_TOPK = 64
+MAX_CAP = 4096
+MAX_EXPAND_CHILDREN = 8192
+MAX_VERIFY_NODES = 1024
+
+EXPORTED = (
+    "tg_status_str",
+    "tg_verify_attention_workspace",
+    "tg_tree_verify_attention",
+    "tg_expand_topk_workspace",
+    "tg_tree_expand_topk",
+    "tg_rescore_graft_workspace",
+    "tg_tree_rescore_graft",
+    "tg_tree_accept",
+)
+
+
+class TgError(RuntimeError):
+    """A library call returned a status other than TG_OK."""
+
+    def __init__(self, call, status, message):
+        super().__init__(f"{call}: {message} (status {status})")
+        self.status = status
+
+
+class TgTree(ctypes.Structure):
+    _fields_ = [
+        ("parent", ctypes.c_void_p),
+        ("token", ctypes.c_void_p),
+        ("depth", ctypes.c_void_p),
+        ("logp", ctypes.c_void_p),
+        ("cum", ctypes.c_void_p),
+        ("visited", ctypes.c_void_p),
+        ("root_visited", ctypes.c_void_p),
+        ("n_nodes", ctypes.c_void_p),
+        ("cap", ctypes.c_int32),
+    ]
+
+
+_lib = None
+_vp, _i32, _sz, _u32, _f32 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t,
+                              ctypes.c_uint32, ctypes.c_float)
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libtreegraft.so (built by ``__graft_entry__.build()``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    lib.tg_status_str.restype = ctypes.c_char_p
+    lib.tg_status_str.argtypes = [_i32]
+    lib.tg_verify_attention_workspace.restype = _sz
+    lib.tg_verify_attention_workspace.argtypes = [_i32] * 6 + [_i32]
+    lib.tg_tree_verify_attention.restype = _i32
+    lib.tg_tree_verify_attention.argtypes = ([_vp] * 6 + [_i32] * 6 + [_f32, _i32, _vp, _sz,
+                                             _vp, _vp])
+    lib.tg_expand_topk_workspace.restype = _sz
+    lib.tg_expand_topk_workspace.argtypes = [_i32] * 5
+    lib.tg_tree_expand_topk.restype = _i32
+    lib.tg_tree_expand_topk.argtypes = ([ctypes.POINTER(TgTree), _vp, _vp, _vp] + [_i32] * 5 +
+                                        [_vp, _vp, _vp, _vp, _sz, _vp, _vp])
+    lib.tg_rescore_graft_workspace.restype = _sz
+    lib.tg_rescore_graft_workspace.argtypes = [_i32] * 6
+    lib.tg_tree_rescore_graft.restype = _i32
+    lib.tg_tree_rescore_graft.argtypes = ([ctypes.POINTER(TgTree), _vp] + [_i32] * 5 + [_u32] +
+                                          [_vp, _vp, _vp, _vp, _sz, _vp, _vp])
+    lib.tg_tree_accept.restype = _i32
+    lib.tg_tree_accept.argtypes = [_vp] * 4 + [_i32] * 3 + [_vp] * 5
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().tg_status_str(status).decode()
+
+
+def _check(call, status):
+    if status != OK:
+        raise TgError(call, status, status_str(status))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _dev(t, name, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    return t
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _workspace(nbytes, device, workspace):
+    if nbytes == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+class TreeState:
+    """Device-resident draft tree (the tg_tree SoA), one row of `cap` slots per
+    batch element.  Slots [0, n_nodes[b]) are live; ids are topological."""
+
+    FIELDS = ("parent", "token", "depth", "logp", "cum", "visited",
+              "root_visited", "n_nodes")
+
+    def __init__(self, B: int, cap: int, device="cuda"):
+        dev = torch.device(device)
+        self.B, self.cap = B, cap
+        self.parent = torch.full((B, cap), -1, dtype=torch.int32, device=dev)
+        self.token = torch.zeros((B, cap), dtype=torch.int32, device=dev)
+        self.depth = torch.zeros((B, cap), dtype=torch.int32, device=dev)
+        self.logp = torch.zeros((B, cap), dtype=torch.float32, device=dev)
+        self.cum = torch.zeros((B, cap), dtype=torch.float32, device=dev)
+        self.visited = torch.zeros((B, cap), dtype=torch.uint8, device=dev)
+        self.root_visited = torch.zeros((B,), dtype=torch.uint8, device=dev)
+        self.n_nodes = torch.zeros((B,), dtype=torch.int32, device=dev)
+
+    @classmethod
+    def from_host(cls, arrays: dict, cap: int, device="cuda") -> "TreeState":
+        """Upload host arrays (numpy or torch) with the FIELDS names."""
+        B = len(arrays["n_nodes"])
+        t = cls(B, cap, device)
+        for f in cls.FIELDS:
+            src = torch.as_tensor(arrays[f])
+            getattr(t, f).copy_(src.to(getattr(t, f).dtype))
+        return t
+
+    def to_host(self) -> dict:
+        return {f: getattr(self, f).cpu().numpy() for f in self.FIELDS}
+
+    def struct(self) -> TgTree:
+        return TgTree(*(getattr(self, f).data_ptr() for f in self.FIELDS), self.cap)
+
+
+# ----------------------------------------------------------------- calls
+
+def verify_attention_workspace(B, N, Hq, Hkv, D, S_max, dtype) -> int:
+    return load().tg_verify_attention_workspace(B, N, Hq, Hkv, D, S_max, dtype)
+
+
+def verify_attention(q, k_cache, v_cache, parent, prefix_len, sm_scale, out=None,
+                     workspace=None, d_err=None, stream=None):
+    """Tree-verify attention; q [B,N,Hq,D], caches [B,Hkv,S_max,D] (bf16 or fp32)."""
+    lib = load()
+    if q.dtype == torch.bfloat16:
+        dt = BF16
+    elif q.dtype == torch.float32:
+        dt = F32
+    else:
+        raise ValueError("q must be bfloat16 or float32")
+    for t, n in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, n, q.dtype)
+    _dev(parent, "parent", torch.int32)
+    _dev(prefix_len, "prefix_len", torch.int32)
+    B, N, Hq, D = q.shape
+    Hkv, S_max = k_cache.shape[1], k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, Hkv, S_max, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("k_cache/v_cache must be [B, Hkv, S_max, D]")
+    if tuple(parent.shape) != (B, N) or tuple(prefix_len.shape) != (B,):
+        raise ValueError("parent must be [B, N] and prefix_len [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", q.dtype)
+    nbytes = lib.tg_verify_attention_workspace(B, N, Hq, Hkv, D, S_max, dt)
+    ws, wsb = _workspace(nbytes, q.device, workspace)
+    if d_err is not None:
+        _dev(d_err, "d_err", torch.int32)
+    st = lib.tg_tree_verify_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(parent),
+                                      _ptr(prefix_len), _ptr(out), B, N, Hq, Hkv, D, S_max,
+                                      float(sm_scale), dt, _ptr(ws), wsb, _ptr(d_err),
+                                      _stream(stream))
+    _check("tg_tree_verify_attention", st)
+    return out
+
+
+def expand_topk_workspace(B, F, V, K, N) -> int:
+    return load().tg_expand_topk_workspace(B, F, V, K, N)
+
+
+def expand_topk(tree: TreeState, logits, frontier, n_frontier, K, N, row_lse=None,
+                next_frontier=None, n_next=None, workspace=None, d_err=None,
+                stream=None):
+    """One expansion step.  logits [B,F,V] fp32, frontier [B,F] int32,
+    n_frontier [B] int32 or None.  Returns (row_lse, next_frontier, n_next)."""
+    lib = load()
+    _dev(logits, "logits", torch.float32)
+    _dev(frontier, "frontier", torch.int32)
+    B, F, V = logits.shape
+    if tuple(frontier.shape) != (B, F):
+        raise ValueError("frontier must be [B, F]")
+    if n_frontier is not None:
+        _dev(n_frontier, "n_frontier", torch.int32)
+    dev = logits.device
+    row_lse = torch.empty((B, F), dtype=torch.float32, device=dev) if row_lse is None else row_lse
+    next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
+                     if next_frontier is None else next_frontier)
+    n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
+    ws, wsb = _workspace(lib.tg_expand_topk_workspace(B, F, V, K, N), dev, workspace)
+    ts = tree.struct()
+    st = lib.tg_tree_expand_topk(ctypes.byref(ts), _ptr(logits), _ptr(frontier),
+                                 _ptr(n_frontier), B, F, V, K, N, _ptr(row_lse),
+                                 _ptr(next_frontier), _ptr(n_next), _ptr(ws), wsb,
+                                 _ptr(d_err), _stream(stream))
+    _check("tg_tree_expand_topk", st)
+    return row_lse, next_frontier, n_next
+
+
+def rescore_graft_workspace(B, R, V, W, M, cap) -> int:
+    return load().tg_rescore_graft_workspace(B, R, V, W, M, cap)
+
+
+def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
+                  graft_frontier=None, n_graft=None, workspace=None, d_err=None,
+                  stream=None):
+    """One middle-drafter step.  strong_logits [B,R,V] fp32 (row 0 = root,
+    1+i = node i).  Returns (row_lse, graft_frontier, n_graft)."""
+    lib = load()
+    _dev(strong_logits, "strong_logits", torch.float32)
+    B, R, V = strong_logits.shape
+    dev = strong_logits.device
+    row_lse = (torch.full((B, R), float("nan"), dtype=torch.float32, device=dev)
+               if row_lse is None else row_lse)
+    graft_frontier = (torch.empty((B, W), dtype=torch.int32, device=dev)
+                      if graft_frontier is None else graft_frontier)
+    n_graft = torch.empty((B,), dtype=torch.int32, device=dev) if n_graft is None else n_graft
+    ws, wsb = _workspace(lib.tg_rescore_graft_workspace(B, R, V, W, M, tree.cap), dev,
+                         workspace)
+    ts = tree.struct()
+    st = lib.tg_tree_rescore_graft(ctypes.byref(ts), _ptr(strong_logits), B, R, V, W, M,
+                                   int(flags), _ptr(row_lse), _ptr(graft_frontier),
+                                   _ptr(n_graft), _ptr(ws), wsb, _ptr(d_err),
+                                   _stream(stream))
+    _check("tg_tree_rescore_graft", st)
+    return row_lse, graft_frontier, n_graft
+
+
+def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_path=None,
+           bonus=None, d_err=None, stream=None):
+    """Greedy acceptance.  parent/token [B,cap], n_nodes [B], greedy [B,cap+1].
+    Returns (accept_len [B], accept_path [B,max_depth], bonus [B])."""
+    lib = load()
+    for t, n in ((parent, "parent"), (token, "token"), (n_nodes, "n_nodes"),
+                 (greedy, "greedy")):
+        _dev(t, n, torch.int32)
+    B, cap = parent.shape
+    if tuple(greedy.shape) != (B, cap + 1):
+        raise ValueError("greedy must be [B, cap + 1]")
+    dev = parent.device
+    accept_len = torch.empty((B,), dtype=torch.int32, device=dev) if accept_len is None else accept_len
+    accept_path = (torch.empty((B, max_depth), dtype=torch.int32, device=dev)
+                   if accept_path is None else accept_path)
+    bonus = torch.empty((B,), dtype=torch.int32, device=dev) if bonus is None else bonus
+    st = lib.tg_tree_accept(_ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(greedy), B, cap,
+                            max_depth, _ptr(accept_len), _ptr(accept_path), _ptr(bonus),
+                            _ptr(d_err), _stream(stream))
+    _check("tg_tree_accept", st)
+    return accept_len, accept_path, bonus

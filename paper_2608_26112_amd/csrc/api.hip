@@ -1,0 +1,176 @@
+// libtreegraft C ABI: argument checks, workspace layout and kernel launches.
+// Every call is asynchronous on the caller's stream and allocates nothing.
+#include <hip/hip_runtime.h>
+
+#include "../../include/treegraft.h"
+#include "tg_kernels.h"
+
+namespace {
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workspace of the row-statistics pass: per (row slot, chunk) the partial
+// (max, sum-exp) pair and the chunk's top-K keys.
+struct RowWs {
+  size_t ms_off, keys_off, extra_off, bytes;
+};
+RowWs row_ws(long long slots, int V, int K, size_t extra) {
+  tg::RowPlan plan = tg::plan_rows(slots, V);
+  size_t ms = (size_t)slots * plan.ms_per_row;
+  size_t parts = (size_t)slots * plan.chunks;
+  RowWs w;
+  w.ms_off = 0;
+  w.keys_off = align_up(ms * sizeof(float2), 256);
+  w.extra_off = align_up(w.keys_off + parts * (size_t)K * sizeof(uint64_t), 256);
+  w.bytes = align_up(w.extra_off + extra, 256);
+  return w;
+}
+
+tg_status from_hip(hipError_t e) { return e == hipSuccess ? TG_OK : TG_ERR_HIP; }
+
+bool tree_ok(const tg_tree *t) {
+  return t && t->parent && t->token && t->depth && t->logp && t->cum &&
+         t->visited && t->root_visited && t->n_nodes && t->cap > 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tg_status_str(tg_status s) {
+  switch (s) {
+    case TG_OK: return "ok";
+    case TG_ERR_INVALID_ARG: return "invalid argument";
+    case TG_ERR_UNSUPPORTED: return "unsupported shape or option";
+    case TG_ERR_WORKSPACE: return "workspace missing or too small";
+    case TG_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+// ------------------------------------------------------------ verify attention
+size_t tg_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
+                                     int S_max, tg_dtype dtype) {
+  if (B <= 0 || N <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || S_max < N) return 0;
+  tg::AttnShape s{B, N, Hq, Hkv, D, S_max, 1.0f};
+  return tg::attn_workspace_bytes(s, dtype);
+}
+
+tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
+                                   const void *v_cache, const int32_t *parent,
+                                   const int32_t *prefix_len, void *out, int B,
+                                   int N, int Hq, int Hkv, int D, int S_max,
+                                   float sm_scale, tg_dtype dtype,
+                                   void *workspace, size_t ws_bytes,
+                                   uint32_t *d_err, void *stream) {
+  if (!q || !k_cache || !v_cache || !parent || !prefix_len || !out)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || N <= 0 || Hq <= 0 || Hkv <= 0 || S_max < N) return TG_ERR_INVALID_ARG;
+  if (Hq % Hkv) return TG_ERR_INVALID_ARG;
+  if (!(sm_scale == sm_scale)) return TG_ERR_INVALID_ARG;
+  if (D != 64 && D != 128) return TG_ERR_UNSUPPORTED;
+  if (N > TG_MAX_VERIFY_NODES) return TG_ERR_UNSUPPORTED;
+  if (dtype != TG_F32 && dtype != TG_BF16) return TG_ERR_INVALID_ARG;
+  tg::AttnShape s{B, N, Hq, Hkv, D, S_max, sm_scale};
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == TG_F32)
+    return from_hip(tg::launch_attn_f32(
+        s, static_cast<const float *>(q), static_cast<const float *>(k_cache),
+        static_cast<const float *>(v_cache), parent, prefix_len,
+        static_cast<float *>(out), d_err, st));
+  size_t need = tg::attn_workspace_bytes(s, dtype);
+  if (need && (!workspace || ws_bytes < need)) return TG_ERR_WORKSPACE;
+  return from_hip(tg::launch_attn_bf16(s, q, k_cache, v_cache, parent, prefix_len,
+                                       out, workspace, d_err, st));
+}
+
+// ------------------------------------------------------------------- expand
+size_t tg_expand_topk_workspace(int B, int F, int V, int K, int N) {
+  if (B <= 0 || F <= 0 || V <= 0 || K <= 0 || N <= 0) return 0;
+  return row_ws((long long)B * F, V, K, 0).bytes;
+}
+
+tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
+                              const int32_t *frontier,
+                              const int32_t *n_frontier, int B, int F, int V,
+                              int K, int N, float *row_lse,
+                              int32_t *next_frontier, int32_t *n_next,
+                              void *workspace, size_t ws_bytes,
+                              uint32_t *d_err, void *stream) {
+  if (!tree_ok(tree) || !logits || !frontier || !row_lse || !next_frontier || !n_next)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || F <= 0 || V <= 0 || K <= 0 || N <= 0) return TG_ERR_INVALID_ARG;
+  if (K > V) return TG_ERR_INVALID_ARG;
+  if (K > TG_MAX_TOPK || (long long)F * K > TG_MAX_EXPAND_CHILDREN ||
+      tree->cap > TG_MAX_CAP)
+    return TG_ERR_UNSUPPORTED;
+  RowWs w = row_ws((long long)B * F, V, K, 0);
+  if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
+  tg::RowPlan plan = tg::plan_rows((long long)B * F, V);
+  char *ws = static_cast<char *>(workspace);
+  float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
+  uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = tg::launch_row_partials(logits, B, F, V, K, plan, n_frontier,
+                                         nullptr, ms, keys, d_err, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(tg::launch_expand_tree(*tree, frontier, n_frontier, B, F, K, N,
+                                         plan, ms, keys, row_lse, next_frontier,
+                                         n_next, d_err, st));
+}
+
+// ------------------------------------------------------------ rescore + graft
+size_t tg_rescore_graft_workspace(int B, int R, int V, int W, int M, int cap) {
+  (void)W;
+  (void)cap;
+  if (B <= 0 || R <= 0 || V <= 0 || M <= 0) return 0;
+  return row_ws((long long)B * R, V, M, (size_t)B * R).bytes;
+}
+
+tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
+                                int B, int R, int V, int W, int M,
+                                uint32_t flags, float *row_lse,
+                                int32_t *graft_frontier, int32_t *n_graft,
+                                void *workspace, size_t ws_bytes,
+                                uint32_t *d_err, void *stream) {
+  if (!tree_ok(tree) || !strong_logits || !row_lse || !graft_frontier || !n_graft)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || R <= 0 || V <= 0 || W <= 0 || M <= 0) return TG_ERR_INVALID_ARG;
+  if (M > V) return TG_ERR_INVALID_ARG;
+  if (flags != 0) return TG_ERR_UNSUPPORTED;
+  if (M > TG_MAX_TOPK || tree->cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  RowWs w = row_ws((long long)B * R, V, M, (size_t)B * R);
+  if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
+  tg::RowPlan plan = tg::plan_rows((long long)B * R, V);
+  char *ws = static_cast<char *>(workspace);
+  float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
+  uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
+  uint8_t *needed = reinterpret_cast<uint8_t *>(ws + w.extra_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = tg::launch_rescore_pool(*tree, B, R, needed, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  e = tg::launch_row_partials(strong_logits, B, R, V, M, plan, nullptr, needed, ms,
+                              keys, d_err, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan,
+                                          needed, ms, keys, row_lse, graft_frontier,
+                                          n_graft, d_err, st));
+}
+
+// ------------------------------------------------------------------- accept
+tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
+                         const int32_t *n_nodes, const int32_t *greedy, int B,
+                         int cap, int max_depth, int32_t *accept_len,
+                         int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
+                         void *stream) {
+  if (!parent || !token || !n_nodes || !greedy || !accept_len || !bonus)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || cap <= 0 || max_depth < 0) return TG_ERR_INVALID_ARG;
+  if (max_depth > 0 && !accept_path) return TG_ERR_INVALID_ARG;
+  if (cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  return from_hip(tg::launch_accept(parent, token, n_nodes, greedy, B, cap, max_depth,
+                                    accept_len, accept_path, bonus, d_err,
+                                    reinterpret_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

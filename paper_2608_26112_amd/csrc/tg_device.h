@@ -1,0 +1,125 @@
+// Internal device helpers shared by the HIP kernels of libtreegraft (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/treegraft.h"
+
+namespace tg {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kWave = 64;
+
+__device__ __forceinline__ void report(uint32_t *d_err, uint32_t bits) {
+  if (d_err && bits) atomicOr(d_err, bits);
+}
+
+// ---------------------------------------------------------------- key order
+// A 32-bit unsigned image of an fp32 value that orders like the float
+// (-inf smallest); -0.0 is folded onto +0.0 first.
+__device__ __forceinline__ uint32_t float_order(float x) {
+  uint32_t b = __float_as_uint(x == 0.0f ? 0.0f : x);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float order_float(uint32_t o) {
+  uint32_t b = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
+  return __uint_as_float(b);
+}
+
+// Logits-row key: larger is better; (logit desc, token asc).  0 = empty slot
+// (every real key is larger: the order image of -inf is 0x007fffff).
+__device__ __forceinline__ uint64_t token_key(float x, uint32_t tok) {
+  return ((uint64_t)float_order(x) << 32) | (uint64_t)(0xffffffffu - tok);
+}
+__device__ __forceinline__ uint32_t key_token(uint64_t k) {
+  return 0xffffffffu - (uint32_t)k;
+}
+__device__ __forceinline__ float key_logit(uint64_t k) {
+  return order_float((uint32_t)(k >> 32));
+}
+
+// Node key: larger is better; (cum desc, depth asc, id asc).  The root is
+// id -1 (stored as id + 1 = 0).  Requires depth < 65536 and id < 65535.
+__device__ __forceinline__ uint64_t node_key(float cum, int depth, int id) {
+  uint32_t lo = 0xffffffffu - (((uint32_t)depth << 16) | (uint32_t)(id + 1));
+  return ((uint64_t)float_order(cum) << 32) | lo;
+}
+__device__ __forceinline__ int node_key_id(uint64_t k) {
+  return (int)((0xffffffffu - (uint32_t)k) & 0xffffu) - 1;
+}
+
+// NaN and +inf are read as -inf (flagged by the caller).
+__device__ __forceinline__ float clean_logit(float x, bool &bad) {
+  bool b = !(x < __builtin_inff());
+  bad |= b;
+  return b ? -__builtin_inff() : x;
+}
+
+// logp = fl(x - lse), -inf when the row has no finite logit.
+__device__ __forceinline__ float edge_logp(float x, float lse) {
+  return lse == -__builtin_inff() ? -__builtin_inff() : __fsub_rn(x, lse);
+}
+
+// ------------------------------------------------------------ wave helpers
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t w = __shfl_xor(v, o, kWave);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// Merge two (max, sum-of-exp relative to max) pairs in the log2 domain.
+__device__ __forceinline__ void merge_ms(float &m, float &s, float m2, float s2) {
+  float mn = fmaxf(m, m2);
+  if (mn == -__builtin_inff()) return;  // both empty
+  s = s * exp2f((m - mn) * kLog2e) + s2 * exp2f((m2 - mn) * kLog2e);
+  m = mn;
+}
+
+// Descending bitonic sort of n (power of two) 64-bit keys in LDS by the whole
+// block.  Callers synchronise before and the function synchronises after.
+__device__ inline void block_bitonic_desc(uint64_t *a, int n) {
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        int p = i ^ j;
+        if (p > i) {
+          uint64_t x = a[i], y = a[p];
+          bool desc = (i & k) == 0;
+          if (desc ? (x < y) : (x > y)) {
+            a[i] = y;
+            a[p] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__host__ __device__ constexpr int pow2_at_least(int n) {
+  int p = 1;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+}  // namespace tg

@@ -1,0 +1,80 @@
+// Internal launch interface between the C ABI (api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/treegraft.h"
+
+namespace tg {
+
+// ------------------------------------------------------------ logits rows
+// A logits row is cut into grains of kGrain elements; every grain yields one
+// (max, sum-exp) partial per wave of the row pass over a fixed element set,
+// so a row's log-sum-exp does not depend on the call's chunking.  A
+// workgroup handles `grains_per_chunk` consecutive grains (one chunk) and
+// emits the chunk's top-K; `chunks` chunks cover a row.
+constexpr int kGrain = 8192;
+struct RowPlan {
+  int chunks;
+  int grains_per_chunk;
+  int ms_per_row;  // (max, sum-exp) partials per row
+};
+RowPlan plan_rows(long long rows, int V);
+
+// Partial (max, sum-exp) and top-K keys of every live (row, chunk).
+//   rows are slots s = b * rows_per_batch + r of a [*, rows_per_batch, V] array;
+//   live iff r < n_live[b] (n_live may be NULL = all) when `needed` is NULL,
+//   else iff needed[s] != 0.
+hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
+                               int V, int K, RowPlan plan,
+                               const int32_t *n_live, const uint8_t *needed,
+                               float2 *part_ms, uint64_t *part_keys,
+                               uint32_t *d_err, hipStream_t stream);
+
+hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
+                              const int32_t *n_frontier, int B, int F, int K,
+                              int N, RowPlan plan, const float2 *part_ms,
+                              const uint64_t *part_keys, float *row_lse,
+                              int32_t *next_frontier, int32_t *n_next,
+                              uint32_t *d_err, hipStream_t stream);
+
+hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
+                               uint8_t *needed, hipStream_t stream);
+
+hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
+                               int R, int V, int W, int M, RowPlan plan,
+                               const uint8_t *needed, const float2 *part_ms,
+                               const uint64_t *part_keys, float *row_lse,
+                               int32_t *graft_frontier, int32_t *n_graft,
+                               uint32_t *d_err, hipStream_t stream);
+
+// ----------------------------------------------------------------- accept
+hipError_t launch_accept(const int32_t *parent, const int32_t *token,
+                         const int32_t *n_nodes, const int32_t *greedy, int B,
+                         int cap, int max_depth, int32_t *accept_len,
+                         int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
+                         hipStream_t stream);
+
+// -------------------------------------------------------------- attention
+struct AttnShape {
+  int B, N, Hq, Hkv, D, S_max;
+  float sm_scale;
+};
+// Number of prefix splits the bf16 kernel uses for this shape (1 = none).
+int attn_splits(const AttnShape &s);
+size_t attn_workspace_bytes(const AttnShape &s, tg_dtype dtype);
+
+hipError_t launch_attn_f32(const AttnShape &s, const float *q, const float *k,
+                           const float *v, const int32_t *parent,
+                           const int32_t *prefix_len, float *out,
+                           uint32_t *d_err, hipStream_t stream);
+
+hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
+                            const void *v, const int32_t *parent,
+                            const int32_t *prefix_len, void *out,
+                            void *workspace, uint32_t *d_err,
+                            hipStream_t stream);
+
+}  // namespace tg

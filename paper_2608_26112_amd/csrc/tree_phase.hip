@@ -1,0 +1,392 @@
+// Per-tree phases of the expansion step (Sec. 3.1; Alg. 1) and of the
+// middle-drafter step (Sec. 3.2; Alg. 2, middle branch).
+//
+// One workgroup owns one tree.  The vocabulary-wide work already happened in
+// row_partial_kernel; here the chunk partials of each needed row are merged
+// into its log-sum-exp and top-K list, then the tree is edited in place:
+// children appended (expand), pool rescored, graft positions reselected and
+// new children grafted without touching existing nodes (rescore_graft).
+// Node selection (Top_W) is a bitonic sort of 64-bit keys in LDS ordered by
+// (cum desc, depth asc, id asc).
+#include "tg_device.h"
+#include "tg_kernels.h"
+
+namespace tg {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+
+// Merge the partials of one row with one wave: the row's `n_ms` (max,
+// sum-exp) partials (lane l folds partials l, l + 64, ... in order, then a
+// fixed shuffle tree) and its `chunks` top-K lists.  Returns the row's
+// log-sum-exp (every lane).  When `mykey` is non-null, lane j < K receives
+// the row's j-th best key (0 for lanes >= K).
+__device__ float merge_row_wave(const float2 *__restrict__ ms, int n_ms,
+                                const uint64_t *__restrict__ keys, int chunks,
+                                int K, uint64_t *mykey) {
+  const int lane = threadIdx.x & (kWave - 1);
+  float m = -__builtin_inff(), s = 0.0f;
+  for (int i = lane; i < n_ms; i += kWave) {
+    float2 p = ms[i];
+    merge_ms(m, s, p.x, p.y);
+  }
+  float M = wave_max_f32(m);
+  float sc = (m == -__builtin_inff()) ? 0.0f : s * exp2f((m - M) * kLog2e);
+  float S = wave_sum_f32(sc);
+  float lse = (M == -__builtin_inff()) ? -__builtin_inff() : M + logf(S);
+  if (mykey) {
+    int idx = 0;
+    uint64_t head = lane < chunks ? keys[(size_t)lane * K] : 0;
+    uint64_t mine = 0;
+    for (int j = 0; j < K; ++j) {
+      uint64_t best = wave_max_u64(head);
+      if (head == best && best != 0) {
+        ++idx;
+        head = idx < K ? keys[(size_t)lane * K + idx] : 0;
+      }
+      if (lane == j) mine = best;
+    }
+    *mykey = mine;
+  }
+  return lse;
+}
+
+__device__ __forceinline__ int sane_parent(int p, int v, bool &bad) {
+  bool b = p < -1 || p >= v;
+  bad |= b;
+  return b ? -1 : p;
+}
+
+// --------------------------------------------------------------- expand
+__global__ __launch_bounds__(kThreads) void expand_tree_kernel(
+    tg_tree tree, const int32_t *__restrict__ frontier,
+    const int32_t *__restrict__ n_frontier, int F, int K, int N, int chunks,
+    int n_ms, const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
+    float *__restrict__ row_lse, int32_t *__restrict__ next_frontier,
+    int32_t *__restrict__ n_next, uint32_t *d_err) {
+  extern __shared__ uint64_t smem[];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), w = tid / kWave;
+  const int cap = tree.cap;
+  int Fb = n_frontier ? n_frontier[b] : F;
+  Fb = Fb < 0 ? 0 : (Fb > F ? F : Fb);
+  const int nb = tree.n_nodes[b];
+  const int total = Fb * K;
+  const int P2 = pow2_at_least(total > 0 ? total : 1);
+  uint64_t *topk = smem;                 // [F*K]
+  uint64_t *skey = smem + (size_t)F * K; // [P2]
+  float *lse_s = reinterpret_cast<float *>(skey + P2);  // [F]
+
+  bool bad = nb < 0 || nb > cap;
+  for (int f = tid; f < Fb; f += kThreads) {
+    int v = frontier[(size_t)b * F + f];
+    bad |= v < -1 || v >= nb;
+  }
+  bad = __syncthreads_or(bad);
+
+  for (int f = w; f < Fb; f += kWaves) {
+    size_t slot = (size_t)b * F + f;
+    uint64_t mine;
+    float lse = merge_row_wave(part_ms + slot * n_ms, n_ms,
+                               part_keys + slot * chunks * K, chunks, K, &mine);
+    if (lane < K) topk[(size_t)f * K + lane] = mine;
+    if (lane == 0) {
+      row_lse[slot] = lse;
+      lse_s[f] = lse;
+    }
+  }
+  __syncthreads();
+
+  const bool full = !bad && (nb + total > cap);
+  if (bad || full) {
+    if (tid == 0) {
+      report(d_err, bad ? TG_DERR_BAD_NODE : TG_DERR_CAPACITY);
+      n_next[b] = 0;
+    }
+    for (int j = tid; j < N; j += kThreads) next_frontier[(size_t)b * N + j] = TG_NO_NODE;
+    return;
+  }
+
+  const size_t base = (size_t)b * cap;
+  for (int c = tid; c < P2; c += kThreads) {
+    if (c >= total) {
+      skey[c] = 0;
+      continue;
+    }
+    const int f = c / K;
+    const uint64_t key = topk[c];
+    const int v = frontier[(size_t)b * F + f];
+    const float cv = v < 0 ? 0.0f : tree.cum[base + v];
+    const int dv = v < 0 ? 0 : tree.depth[base + v];
+    const float lp = edge_logp(key_logit(key), lse_s[f]);
+    const float cum = __fadd_rn(cv, lp);
+    const int id = nb + c;
+    tree.parent[base + id] = v;
+    tree.token[base + id] = (int)key_token(key);
+    tree.depth[base + id] = dv + 1;
+    tree.logp[base + id] = lp;
+    tree.cum[base + id] = cum;
+    tree.visited[base + id] = 0;
+    skey[c] = node_key(cum, dv + 1, id);
+  }
+  __syncthreads();
+  block_bitonic_desc(skey, P2);
+  const int nn = min(N, total);
+  for (int j = tid; j < N; j += kThreads)
+    next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
+  if (tid == 0) {
+    n_next[b] = nn;
+    tree.n_nodes[b] = nb + total;
+  }
+}
+
+// ------------------------------------------------------- middle-step pool
+// needed[b, r] = 1 iff logits row r is read by this middle step: the row of
+// each pool node (its children) and the row of each pool node's parent (its
+// edge score).  Rows of trees that cannot be processed are all 0.
+__global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
+    tg_tree tree, int R, uint8_t *__restrict__ needed) {
+  __shared__ uint8_t flag[TG_MAX_CAP + 1];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int nb = tree.n_nodes[b];
+  const bool ok = nb >= 0 && nb <= tree.cap && nb + 1 <= R;
+  const int rows = ok ? nb + 1 : 0;
+  for (int r = tid; r < rows; r += kThreads) flag[r] = 0;
+  __syncthreads();
+  const size_t base = (size_t)b * tree.cap;
+  if (ok) {
+    if (tid == 0 && !tree.root_visited[b]) flag[0] = 1;
+    bool dummy = false;
+    for (int v = tid; v < nb; v += kThreads) {
+      if (!tree.visited[base + v]) {
+        flag[v + 1] = 1;
+        flag[sane_parent(tree.parent[base + v], v, dummy) + 1] = 1;
+      }
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < R; r += kThreads)
+    needed[(size_t)b * R + r] = r < rows ? flag[r] : 0;
+}
+
+// ------------------------------------------------ rescore + reselect + graft
+__global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
+    tg_tree tree, const float *__restrict__ strong, int R, int V, int W, int M,
+    int chunks, int n_ms, const uint8_t *__restrict__ needed,
+    const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
+    float *__restrict__ row_lse, int32_t *__restrict__ graft_frontier,
+    int32_t *__restrict__ n_graft, uint32_t *d_err) {
+  extern __shared__ uint64_t smem[];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), w = tid / kWave;
+  const int cap = tree.cap;
+  const int nb = tree.n_nodes[b];
+  const size_t base = (size_t)b * cap;
+
+  const bool bad_tree = nb < 0 || nb > cap || nb + 1 > R;
+  if (bad_tree) {
+    if (tid == 0) {
+      report(d_err, TG_DERR_BAD_NODE);
+      n_graft[b] = 0;
+    }
+    for (int f = tid; f < W; f += kThreads) graft_frontier[(size_t)b * W + f] = TG_NO_NODE;
+    return;
+  }
+  const int P2 = pow2_at_least(nb + 1);
+  uint64_t *skey = smem;                                   // [P2]
+  float *lse_s = reinterpret_cast<float *>(skey + P2);     // [nb + 1]
+  float *cum_s = lse_s + (nb + 1);                         // [nb]
+  float *lp_s = cum_s + nb;                                // [nb]
+  int *par_s = reinterpret_cast<int *>(lp_s + nb);         // [nb]
+  uint8_t *inC = reinterpret_cast<uint8_t *>(par_s + nb);  // [nb]
+  uint8_t *done = inC + nb;                                // [nb]
+
+  // ---- pool C and parents
+  bool badp = false;
+  int cnt = 0;
+  for (int v = tid; v < nb; v += kThreads) {
+    uint8_t in = tree.visited[base + v] ? 0 : 1;
+    inC[v] = in;
+    done[v] = in ? 0 : 1;
+    cum_s[v] = tree.cum[base + v];
+    par_s[v] = sane_parent(tree.parent[base + v], v, badp);
+    cnt += in;
+  }
+  const int root_in = tree.root_visited[b] ? 0 : 1;
+  if (badp) report(d_err, TG_DERR_BAD_PARENT);
+  __shared__ int red[kWaves];
+  int wsum = wave_sum_i32(cnt);
+  if (lane == 0) red[w] = wsum;
+  __syncthreads();
+  int poolC = root_in;
+  for (int i = 0; i < kWaves; ++i) poolC += red[i];
+
+  // ---- log-sum-exp of every needed row (exported)
+  const uint8_t *need = needed + (size_t)b * R;
+  for (int r = w; r <= nb; r += kWaves) {
+    if (!need[r]) continue;
+    size_t slot = (size_t)b * R + r;
+    float lse = merge_row_wave(part_ms + slot * n_ms, n_ms, nullptr, chunks, M, nullptr);
+    if (lane == 0) {
+      lse_s[r] = lse;
+      row_lse[slot] = lse;
+    }
+  }
+  __syncthreads();
+
+  const int nF = min(W, poolC);
+  if (nb + nF * M > cap) {
+    if (tid == 0) {
+      report(d_err, TG_DERR_CAPACITY);
+      n_graft[b] = 0;
+    }
+    for (int f = tid; f < W; f += kThreads) graft_frontier[(size_t)b * W + f] = TG_NO_NODE;
+    return;
+  }
+
+  // ---- rescoring: logp[v] = fl(x[pa(v)+1][tok v] - lse[pa(v)+1])
+  bool badtok = false, nonfin = false;
+  for (int v = tid; v < nb; v += kThreads) {
+    if (!inC[v]) continue;
+    const int p = par_s[v];
+    const int tok = tree.token[base + v];
+    float x = -__builtin_inff();
+    if (tok >= 0 && tok < V)
+      x = clean_logit(strong[((size_t)b * R + (p + 1)) * V + tok], nonfin);
+    else
+      badtok = true;
+    const float lp = edge_logp(x, lse_s[p + 1]);
+    lp_s[v] = lp;
+    tree.logp[base + v] = lp;
+  }
+  if (badtok) report(d_err, TG_DERR_BAD_NODE);
+  if (nonfin) report(d_err, TG_DERR_NONFINITE);
+  __syncthreads();
+
+  // ---- cum recompute, parents before children: rounds of "every pool node
+  // whose parent is final takes cum[parent] + logp" (one round per level)
+  for (;;) {
+    // phase 1: decide who is ready from the previous round's state
+    uint32_t ready = 0;  // bit i <-> node tid + i * kThreads
+    int pending = 0;
+    for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
+      if (!inC[v] || done[v]) continue;
+      const int p = par_s[v];
+      if (p < 0 || done[p]) ready |= 1u << i;
+      else pending = 1;
+    }
+    __syncthreads();
+    for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
+      if (!(ready >> i & 1u)) continue;
+      const int p = par_s[v];
+      cum_s[v] = __fadd_rn(p < 0 ? 0.0f : cum_s[p], lp_s[v]);
+      done[v] = 1;
+    }
+    if (!__syncthreads_or(pending)) break;
+  }
+
+  // ---- reselection: Top_W(C) by (cum desc, depth asc, id asc)
+  for (int i = tid; i < P2; i += kThreads) {
+    uint64_t k = 0;
+    if (i < nb) {
+      if (inC[i]) k = node_key(cum_s[i], tree.depth[base + i], i);
+    } else if (i == nb && root_in) {
+      k = node_key(0.0f, 0, -1);
+    }
+    skey[i] = k;
+  }
+  __syncthreads();
+  block_bitonic_desc(skey, P2);
+
+  // ---- non-destructive graft: new children only, ids nb + f*M + j
+  for (int f = w; f < nF; f += kWaves) {
+    const int v = node_key_id(skey[f]);
+    const int row = v + 1;
+    const size_t slot = (size_t)b * R + row;
+    uint64_t key;
+    merge_row_wave(part_ms + slot * n_ms, n_ms, part_keys + slot * chunks * M,
+                   chunks, M, &key);
+    const float cv = v < 0 ? 0.0f : cum_s[v];
+    const int dv = v < 0 ? 0 : tree.depth[base + v];
+    const float lse = lse_s[row];
+    if (lane < M) {
+      const int j = lane;
+      const float lp = edge_logp(key_logit(key), lse);
+      const int id = nb + f * M + j;
+      tree.parent[base + id] = v;
+      tree.token[base + id] = (int)key_token(key);
+      tree.depth[base + id] = dv + 1;
+      tree.logp[base + id] = lp;
+      tree.cum[base + id] = __fadd_rn(cv, lp);
+      tree.visited[base + id] = 0;
+    }
+  }
+  for (int f = tid; f < W; f += kThreads)
+    graft_frontier[(size_t)b * W + f] = f < nF ? node_key_id(skey[f]) : TG_NO_NODE;
+  // ---- P <- P u C; write back rescored path scores
+  for (int v = tid; v < nb; v += kThreads) {
+    if (inC[v]) tree.cum[base + v] = cum_s[v];
+    tree.visited[base + v] = 1;
+  }
+  if (tid == 0) {
+    tree.root_visited[b] = 1;
+    tree.n_nodes[b] = nb + nF * M;
+    n_graft[b] = nF;
+  }
+}
+
+}  // namespace
+
+static size_t expand_lds(int F, int K) {
+  int total = F * K;
+  return (size_t)F * K * 8 + (size_t)pow2_at_least(total > 0 ? total : 1) * 8 +
+         (size_t)F * 4;
+}
+
+hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
+                              const int32_t *n_frontier, int B, int F, int K,
+                              int N, RowPlan plan, const float2 *part_ms,
+                              const uint64_t *part_keys, float *row_lse,
+                              int32_t *next_frontier, int32_t *n_next,
+                              uint32_t *d_err, hipStream_t stream) {
+  size_t lds = expand_lds(F, K);
+  hipError_t e = hipFuncSetAttribute((const void *)expand_tree_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
+                     tree, frontier, n_frontier, F, K, N, plan.chunks, plan.ms_per_row, part_ms,
+                     part_keys, row_lse, next_frontier, n_next, d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
+                               uint8_t *needed, hipStream_t stream) {
+  hipLaunchKernelGGL(rescore_pool_kernel, dim3(B), dim3(kThreads), 0, stream,
+                     tree, R, needed);
+  return hipGetLastError();
+}
+
+hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
+                               int R, int V, int W, int M, RowPlan plan,
+                               const uint8_t *needed, const float2 *part_ms,
+                               const uint64_t *part_keys, float *row_lse,
+                               int32_t *graft_frontier, int32_t *n_graft,
+                               uint32_t *d_err, hipStream_t stream) {
+  // worst case over any live node count up to cap
+  int n = tree.cap;
+  size_t lds = (size_t)pow2_at_least(n + 1) * 8 + (size_t)(n + 1) * 4 +
+               (size_t)n * (4 + 4 + 4 + 1 + 1);
+  hipError_t e = hipFuncSetAttribute((const void *)rescore_tree_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
+                     tree, strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms,
+                     part_keys, row_lse, graft_frontier, n_graft, d_err);
+  return hipGetLastError();
+}
+
+}  // namespace tg
