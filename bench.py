@@ -1,0 +1,381 @@
+#!/usr/bin/env python3
+"""Benchmark of the tree-verify / tree-expand hot path on one MI355X.
+
+One step = one TreeGraft decoding turn's data-parallel work on the
+Llama-3-8B-shaped workload (batch 1, vocabulary 128256, frontier W = 10,
+m = 8 children per node, 32/8 heads, head_dim 128, prefix 2048, bf16):
+
+  reset          the shared tree becomes the lone root (T_1 = {r}, P_1 = {})
+  k=1  middle    tg_tree_rescore_graft  pool {root}: graft its top-8 children
+  k=2  small     tg_tree_expand_topk    expand Top_W of the grafted children
+  k=3  middle    tg_tree_rescore_graft  pool = 72 unvisited nodes, rescore,
+                                        reselect 10 graft points, +80 nodes
+  k=4  small     tg_tree_expand_topk    expand Top_W of those 80
+  k=5  middle    tg_tree_rescore_graft  pool = 160 nodes, rescore, +80 nodes
+  verify         tg_tree_verify_attention  one target layer over a 64-node
+                                        verify tree (root + 63 draft nodes)
+  accept         tg_tree_accept         greedy acceptance on the draft tree
+
+The schedule [1,0,1,0,1] is the paper's fixed ablation schedule (Sec. 5.3).
+Drafter and target logits, Q/K/V and tokens are seeded synthetic data of the
+workload's shapes and distributions (logits N(0,3) fp32; Q/K/V N(0,1)/sqrt(128)
+bf16).  Inputs rotate over several resident copies (> the 256 MB MALL) so no
+timed read is served from the last-level cache.
+
+The timed region replays one captured HIP graph per input copy (the whole
+step, so host launch overhead is not measured).  A second, eager pass over the
+same steps records every kernel's device time with the library's trace events
+(dispatch-level start/stop events on the launch stream); the dominant kernel's
+roofline comes from those.  The CPU baseline times the oracle (tests' CPU
+reference) on the same inputs.
+
+Prints ONE JSON line.  N > 1 GPUs is not supported by this build.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tree-verify attention TB/s & TFLOP/s (% roofline); draft-tree nodes/sec"
+PEAK_HBM = 8.0e12        # B/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15       # flop/s, dense bf16 MFMA
+
+# workload (Llama-3-8B-shaped turn)
+V, W_FR, M_CH = 128256, 10, 8
+SCHEDULE = (1, 0, 1, 0, 1)
+B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64
+CAP = 512
+R_ROWS = 313             # strong-logits rows (root + up to 312 nodes)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--copies", type=int, default=4, help="resident input copies")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------- inputs
+
+def make_inputs(c, dev):
+    """Input copy c (seed 1002 + 100 * c): the workload's tensors on the GPU."""
+    import torch
+    import workloads as W
+    g = W.rng([1002, c])
+    strong = torch.empty((B, R_ROWS, V), dtype=torch.float32, device=dev)
+    for r0 in range(0, R_ROWS, 32):        # chunks keep host memory small
+        r1 = min(R_ROWS, r0 + 32)
+        strong[0, r0:r1] = torch.from_numpy(W.normal(g, (r1 - r0, V), 3.0)).to(dev)
+    weak = [torch.from_numpy(W.normal(g, (B, W_FR, V), 3.0)).to(dev) for _ in range(2)]
+    s = np.float32(1.0 / np.sqrt(128.0))
+    S = L + N_VER
+    q = torch.from_numpy(W.normal(g, (B, N_VER, HQ, D)) * s).to(dev).bfloat16()
+    k = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
+    v = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
+    return dict(strong=strong, weak=weak, q=q, k=k, v=v)
+
+
+def make_trees(dev):
+    """Verify tree (root + 63 draft nodes shaped like a pruned top-8 /
+    frontier-10 expansion of depth 6) and the accept inputs on its draft nodes:
+    sibling-distinct tokens, target greedy agreeing with the first child with
+    p = 0.7 per level."""
+    import torch
+    import workloads as W
+    g = W.rng(1002)
+    draft = W.expansion_shaped_tree(g, N_VER - 1, 6, 8, W_FR)
+    vpar = W.verify_layout_with_root(draft)
+    tok = W.distinct_sibling_tokens(g, draft, V)
+    greedy = W.greedy_match_first_child(g, draft, tok, V, 0.7)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    return dict(vparent=t(vpar[None]), plen=t([L]), dparent=t(draft[None]),
+                dtoken=t(tok[None]), dn=t([N_VER - 1]), greedy=t(greedy[None]),
+                host=dict(draft=draft, vpar=vpar, tok=tok, greedy=greedy))
+
+
+class Step:
+    """All buffers of one step on one input copy, so it can be captured."""
+
+    def __init__(self, tg, inp, trees, dev):
+        import torch
+        self.tg, self.inp, self.tr = tg, inp, trees
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.tree = tg.TreeState(B, CAP, dev)
+        self.ws_r = torch.empty(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
+                                dtype=torch.uint8, device=dev)
+        self.ws_e = torch.empty(tg.expand_topk_workspace(B, W_FR, V, M_CH, W_FR),
+                                dtype=torch.uint8, device=dev)
+        nv = tg.verify_attention_workspace(B, N_VER, HQ, HKV, D, L + N_VER, tg.BF16)
+        self.ws_v = torch.empty(max(nv, 1), dtype=torch.uint8, device=dev)
+        self.r_lse = [torch.empty((B, R_ROWS), dtype=torch.float32, device=dev) for _ in range(3)]
+        self.gf = [torch.empty((B, W_FR), **i32) for _ in range(3)]
+        self.ng = [torch.empty((B,), **i32) for _ in range(3)]
+        self.e_lse = [torch.empty((B, W_FR), dtype=torch.float32, device=dev) for _ in range(2)]
+        self.fr = [torch.empty((B, W_FR), **i32) for _ in range(5)]
+        self.nn = [torch.empty((B,), **i32) for _ in range(5)]
+        self.out = torch.empty_like(inp["q"])
+        self.A = torch.empty((B,), **i32)
+        self.path = torch.empty((B, 6), **i32)
+        self.bonus = torch.empty((B,), **i32)
+
+    def run(self):
+        tg, x, t = self.tg, self.inp, self.tree
+        tg.tree_reset(t)
+        mid, small = 0, 0
+        for k, a in enumerate(SCHEDULE):
+            if a == 1:       # middle-drafter step
+                tg.rescore_graft(t, x["strong"], W_FR, M_CH, row_lse=self.r_lse[mid],
+                                 graft_frontier=self.gf[mid], n_graft=self.ng[mid], N=W_FR,
+                                 next_frontier=self.fr[k], n_next=self.nn[k],
+                                 workspace=self.ws_r)
+                mid += 1
+            else:            # small-drafter step over the previous step's new nodes
+                tg.expand_topk(t, x["weak"][small], self.fr[k - 1], self.nn[k - 1], M_CH, W_FR,
+                               row_lse=self.e_lse[small], next_frontier=self.fr[k],
+                               n_next=self.nn[k], workspace=self.ws_e)
+                small += 1
+        tg.verify_attention(x["q"], x["k"], x["v"], self.tr["vparent"], self.tr["plen"],
+                            D ** -0.5, out=self.out, workspace=self.ws_v)
+        tg.accept(self.tr["dparent"], self.tr["dtoken"], self.tr["dn"], self.tr["greedy"], 6,
+                  accept_len=self.A, accept_path=self.path, bonus=self.bonus)
+
+
+# ------------------------------------------------------------ accounting
+
+def rows_read_per_step():
+    """Logits rows one step reads (structural: independent of the values).
+    k=1 pool {root}: row 0.  k=2: the 8 frontier rows.  k=3 pool = 72
+    unvisited nodes: their 72 rows + the root row (parent of 8 of them).
+    k=4: 10 rows.  k=5 pool = 160 nodes: their rows + the rows of the 10
+    graft points of k=3 (parents of 80 of them, already visited)."""
+    rescore = [1, 73, 170]
+    expand = [8, 10]
+    return rescore, expand
+
+
+def path_len_sum(vpar):
+    """Sum over nodes of the number of tree keys a node attends to (its
+    ancestors and itself)."""
+    tot = 0
+    for i in range(len(vpar)):
+        u = i
+        while u != -1:
+            tot += 1
+            u = int(vpar[u])
+    return tot
+
+
+def verify_work(vpar):
+    """Algorithmic bytes and flops of one verify call (each K/V element read
+    once, Q read, O written; flops over ancestor-or-self keys only)."""
+    kv = 2 * B * HKV * (L + N_VER) * D * 2
+    qo = 2 * B * N_VER * HQ * D * 2
+    keys = N_VER * L + path_len_sum(vpar)
+    flops = 4 * D * HQ * B * keys
+    return kv + qo + vpar.nbytes, flops
+
+
+# -------------------------------------------------------------- cpu leg
+
+def cpu_baseline(inp, trees, budget_s):
+    """The oracle (the tests' CPU reference, untuned) running the same turn on
+    input copy 0 until about `budget_s` seconds have been spent."""
+    from oracle import attention as OA
+    from oracle import tree as OT
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = 1
+    strong = inp["strong"].cpu().numpy()
+    weak = [w.cpu().numpy() for w in inp["weak"]]
+    q = inp["q"].float().cpu().numpy()
+    k = inp["k"].float().cpu().numpy()
+    v = inp["v"].float().cpu().numpy()
+    h = trees["host"]
+    turns, t0 = 0, time.perf_counter()
+    while True:
+        t = OT.Tree.empty(B, CAP)
+        fr = nn = None
+        small = 0
+        for a in SCHEDULE:
+            if a == 1:
+                t, _, _, _, _, fr, nn = OT.rescore_graft(t, strong, W_FR, M_CH, N=W_FR)
+            else:
+                t, _, fr, nn, _ = OT.expand(t, weak[small], fr, nn, M_CH, W_FR)
+                small += 1
+        OA.tree_verify_attention_fast(q, k, v, h["vpar"][None], [L], D ** -0.5)
+        OT.accept(h["draft"][None], h["tok"][None], np.array([N_VER - 1]), h["greedy"][None], 6)
+        turns += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            return turns, el, blas
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; multi-GPU sharding of the "
+              "tree-verify path is described in DESIGN.md but not implemented", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2608_26112_amd as tg
+    tg.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    trees = make_trees(dev)
+    inputs = [make_inputs(c, dev) for c in range(args.copies)]
+    steps = [Step(tg, inputs[c], trees, dev) for c in range(args.copies)]
+    torch.cuda.synchronize()
+
+    # correctness guard: the turn produces the structurally expected tree
+    steps[0].run()
+    torch.cuda.synchronize()
+    n_nodes = int(steps[0].tree.n_nodes[0].item())
+    assert n_nodes == 8 + 64 + 80 + 80 + 80, n_nodes
+
+    # ---- graph capture: one graph per input copy
+    graphs = []
+    timing = "eager launches"
+    if not args.no_graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for st in steps:
+                st.run()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        try:
+            for st in steps:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    st.run()
+                graphs.append(g)
+            torch.cuda.synchronize()
+            timing = "one captured HIP graph per step"
+        except Exception as exc:  # report and time eager launches instead
+            print(f"bench.py: graph capture failed ({exc}); timing eager launches",
+                  file=sys.stderr)
+            graphs = []
+        # replaying a graph must reproduce the eager turn
+        if graphs:
+            graphs[0].replay()
+            torch.cuda.synchronize()
+            assert int(steps[0].tree.n_nodes[0].item()) == n_nodes
+
+    def run_steps(n, graph=True):
+        for i in range(n):
+            if graph and graphs:
+                graphs[i % len(graphs)].replay()
+            else:
+                steps[i % len(steps)].run()
+
+    # ---- warmup + timed region (graph replay)
+    run_steps(args.warmup, graph=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run_steps(args.steps, graph=True)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # ---- eager pass with per-kernel trace events (same steps)
+    run_steps(args.warmup, graph=False)
+    torch.cuda.synchronize()
+    tg.trace_begin(64 * (args.steps + 1))
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2.record()
+    run_steps(args.steps, graph=False)
+    e3.record()
+    torch.cuda.synchronize()
+    recs = tg.trace_end()
+    ms_eager = e2.elapsed_time(e3) / args.steps
+    kern = {}
+    for name, ms in recs:
+        d = kern.setdefault(name, [0, 0.0])
+        d[0] += 1
+        d[1] += ms
+    kernels = {k: {"launches_per_step": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0],
+                   "us_per_step": 1e3 * v[1] / args.steps} for k, v in kern.items()}
+
+    # ---- accounting
+    rows_r, rows_e = rows_read_per_step()
+    row_bytes = V * 4
+    vpar = trees["host"]["vpar"]
+    v_bytes, v_flops = verify_work(vpar)
+    step_bytes = (sum(rows_r) + sum(rows_e)) * row_bytes + v_bytes
+    nodes = 8 + 64 + 80 + 80 + 80            # created per turn
+    rescored = 72 + 160                       # non-root pool nodes rescored
+    value = step_bytes / (ms_step * 1e-3) / 1e12
+
+    # dominant kernel (largest device time per step) and its roofline
+    dom = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    if dom == "row_partial":
+        dom_bytes = (sum(rows_r) + sum(rows_e)) * row_bytes
+        launches = kern[dom][0]
+        achieved = dom_bytes * args.steps / (kern[dom][1] * 1e-3)
+        roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM, "traffic": None,
+                "bytes_per_launch": dom_bytes * args.steps / launches,
+                "avg_launch_us": 1e3 * kern[dom][1] / launches}
+    else:
+        t_us = kernels[dom]["us_per_step"]
+        roof = {"bound": "hbm", "kernel": dom, "achieved": None, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s", "frac": None, "traffic": None, "avg_launch_us": t_us}
+    attn_us = sum(kernels[k]["us_per_step"] for k in ("attn_mfma", "attn_combine") if k in kernels)
+    verify = {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
+              "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
+              "frac_hbm": v_bytes / (attn_us * 1e-6) / PEAK_HBM,
+              "frac_mfma": v_flops / (attn_us * 1e-6) / PEAK_BF16,
+              "bytes": v_bytes, "flops": v_flops}
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "TB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp32+bf16", "data": "synthetic",
+        "config": {"workload": "TreeGraft turn (schedule 1,0,1,0,1) + Llama-3-8B-shaped "
+                               "verify layer", "batch": B, "vocab": V, "frontier_W": W_FR,
+                   "children_m": M_CH, "q_heads": HQ, "kv_heads": HKV, "head_dim": D,
+                   "prefix": L, "verify_nodes": N_VER, "input_copies": args.copies,
+                   "timing": timing},
+        "roofline": roof,
+        "draft_nodes_per_s": (nodes + rescored) / (ms_step * 1e-3),
+        "verify_attention": verify,
+        "step_bytes": step_bytes,
+        "eager_ms_per_step": ms_eager,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        turns, el, blas = cpu_baseline(inputs[0], trees, args.cpu_seconds)
+        out["cpu_baseline"] = {"value": step_bytes * turns / el / 1e12, "unit": "TB/s",
+                               "cores": blas, "kind": "oracle",
+                               "sample": f"{turns} full turns of the same workload on input "
+                                         f"copy 0 in {el:.1f} s (tree steps single-threaded "
+                                         f"NumPy; attention matmuls on {blas} BLAS threads)"}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -102,6 +102,14 @@ typedef struct {
 
 const char *tg_status_str(tg_status s);
 
+/*
+ * Start a new drafting turn: every tree becomes the lone root (n_nodes = 0,
+ * root unvisited; Alg. 1/2 initialise T_1 = {r} and P_1 = empty).  Slots are
+ * not cleared.  A kernel, not a memset, so the call can sit in a captured
+ * HIP graph.
+ */
+tg_status tg_tree_reset(const tg_tree *tree, int B, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Tree-verify attention (Alg. 3 mask; Sec. 3.1 root = verified prefix).     */
 /*
@@ -188,13 +196,21 @@ tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
  * row_lse[b, r] is written for the rows the step reads: v+1 and parent(v)+1
  * for v in C (other rows untouched).  graft_frontier[b] = F (ids, -1 = root),
  * padded with TG_NO_NODE; n_graft[b] = |F|.
+ * The grafted children are N_{k+1}, the pool of a following small step (Sec.
+ * 3.2, small steps use C = N_k).  When next_frontier is non-NULL it receives
+ * their best min(N, |F|*M) ids by (cum desc, depth asc, id asc), padded with
+ * TG_NO_NODE, and n_next[b] their count: the frontier to hand to
+ * tg_tree_expand_topk for that small step.
  *
  * strong_logits  [B, R, V] fp32, R >= n_nodes[b] + 1 for every b
  * row_lse        [B, R] fp32 out;  graft_frontier [B, W] int32 out;
  * n_graft        [B] int32 out
+ * next_frontier  [B, N] int32 out or NULL;  n_next [B] int32 out (NULL iff
+ *                next_frontier is NULL);  N >= 1 when next_frontier is used
  * 1 <= M <= min(V, TG_MAX_TOPK); 1 <= W; cap <= TG_MAX_CAP; flags = 0.
  * Device errors: NONFINITE; BAD_NODE (R too small) or CAPACITY
- * (n_b + |F|*M > cap) leave tree b unchanged with n_graft[b] = 0.
+ * (n_b + |F|*M > cap) leave tree b unchanged with n_graft[b] = 0 and
+ * n_next[b] = 0.
  */
 size_t tg_rescore_graft_workspace(int B, int R, int V, int W, int M, int cap);
 
@@ -202,6 +218,7 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 int B, int R, int V, int W, int M,
                                 uint32_t flags, float *row_lse,
                                 int32_t *graft_frontier, int32_t *n_graft,
+                                int32_t *next_frontier, int32_t *n_next, int N,
                                 void *workspace, size_t ws_bytes,
                                 uint32_t *d_err, void *stream);
 
@@ -228,6 +245,27 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
                          int cap, int max_depth, int32_t *accept_len,
                          int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
                          void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel timing (benchmarks and profiling; not part of the hot path).      */
+/*
+ * tg_trace_begin(capacity) creates `capacity` HIP event pairs and turns
+ * tracing on: from then on every kernel the library launches is dispatched
+ * with its own start/stop events (hipExtLaunchKernelGGL), so each record is
+ * the device time of one kernel on the stream it ran on.  Launches beyond
+ * `capacity` are not recorded.  tg_trace_end waits for the recorded events,
+ * writes at most max_records records in launch order (kernel names are
+ * static strings owned by the library), frees the events and turns tracing
+ * off.  Tracing state is process-global and not thread-safe; while it is
+ * off (the default) no event is created or recorded.
+ */
+typedef struct {
+  const char *kernel;
+  float ms;
+} tg_trace_record;
+
+tg_status tg_trace_begin(int capacity);
+tg_status tg_trace_end(tg_trace_record *out, int max_records, int *n_records);
 
 #ifdef __cplusplus
 }

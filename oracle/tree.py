@@ -202,7 +202,7 @@ def needed_rows(tree: Tree, b: int):
 
 
 def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
-                  lse_override=None):
+                  lse_override=None, N: int = 0):
     """One middle-drafter step of Alg. 2, applied to a copy.
 
     strong: [B, R, V] fp32; row 0 = the middle drafter's logits at the root,
@@ -216,8 +216,12 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
       4. For each v in F (rank f) and each of its row's top-M tokens (rank j):
          attach a new child, id n_b + f*M + j, never touching existing nodes.
       5. P <- P u C: every pre-existing node and the root become visited.
-    Returns (tree', row_lse [B, R], graft_frontier [B, W], n_graft [B], err);
-    row_lse holds NaN for rows that were not needed.
+    The grafted children are N_{k+1}, the pool of a following small step
+    (Sec. 3.2: a small step's pool is the previous step's new nodes); with
+    N > 0 their Top_N by (cum desc, depth asc, id asc) is also returned.
+    Returns (tree', row_lse [B, R], graft_frontier [B, W], n_graft [B], err)
+    and, when N > 0, also (next_frontier [B, N], n_next [B]).  row_lse holds
+    NaN for rows that were not needed.
     """
     B, R, V = strong.shape
     t = tree.copy()
@@ -225,6 +229,8 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
     lse_out = np.full((B, R), np.nan, np.float32)
     fr_out = np.full((B, W), NO_NODE, np.int32)
     n_graft = np.zeros(B, np.int32)
+    nxt = np.full((B, max(N, 1)), NO_NODE, np.int32)
+    n_next = np.zeros(B, np.int32)
     for b in range(B):
         nb = int(t.n_nodes[b])
         if nb + 1 > R:
@@ -257,6 +263,7 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
                       node_key(t.cum[b, v], t.depth[b, v], v) for v in C)
         Fsel = [k[2] for k in cand[:nF]]
         # 4. non-destructive grafting
+        kids = []
         for f, v in enumerate(Fsel):
             toks, vals = row_topk(strong[b, v + 1], M)
             lse = lse_out[b, v + 1]
@@ -271,12 +278,19 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
                 t.logp[b, nid] = lp
                 t.cum[b, nid] = F32(cum_v + lp)
                 t.visited[b, nid] = 0
+                kids.append(node_key(t.cum[b, nid], d_v + 1, nid))
+        kids.sort()
+        sel = [k[2] for k in kids[:N]]
+        nxt[b, :len(sel)] = sel
+        n_next[b] = len(sel)
         # 5. visited update
         t.visited[b, :nb] = 1
         t.root_visited[b] = 1
         t.n_nodes[b] = nb + nF * M
         fr_out[b, :nF] = Fsel
         n_graft[b] = nF
+    if N > 0:
+        return t, lse_out, fr_out, n_graft, err, nxt, n_next
     return t, lse_out, fr_out, n_graft, err
 
 

@@ -37,6 +37,9 @@ MAX_VERIFY_NODES = 1024
 
 EXPORTED = (
     "tg_status_str",
+    "tg_tree_reset",
+    "tg_trace_begin",
+    "tg_trace_end",
     "tg_verify_attention_workspace",
     "tg_tree_verify_attention",
     "tg_expand_topk_workspace",
@@ -53,6 +56,10 @@ class TgError(RuntimeError):
     def __init__(self, call, status, message):
         super().__init__(f"{call}: {message} (status {status})")
         self.status = status
+
+
+class TgTraceRecord(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char_p), ("ms", ctypes.c_float)]
 
 
 class TgTree(ctypes.Structure):
@@ -98,9 +105,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_rescore_graft_workspace.argtypes = [_i32] * 6
     lib.tg_tree_rescore_graft.restype = _i32
     lib.tg_tree_rescore_graft.argtypes = ([ctypes.POINTER(TgTree), _vp] + [_i32] * 5 + [_u32] +
-                                          [_vp, _vp, _vp, _vp, _sz, _vp, _vp])
+                                          [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp])
     lib.tg_tree_accept.restype = _i32
     lib.tg_tree_accept.argtypes = [_vp] * 4 + [_i32] * 3 + [_vp] * 5
+    lib.tg_tree_reset.restype = _i32
+    lib.tg_tree_reset.argtypes = [ctypes.POINTER(TgTree), _i32, _vp]
+    lib.tg_trace_begin.restype = _i32
+    lib.tg_trace_begin.argtypes = [_i32]
+    lib.tg_trace_end.restype = _i32
+    lib.tg_trace_end.argtypes = [ctypes.POINTER(TgTraceRecord), _i32, ctypes.POINTER(_i32)]
     _lib = lib
     return lib
 
@@ -256,10 +269,11 @@ def rescore_graft_workspace(B, R, V, W, M, cap) -> int:
 
 
 def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
-                  graft_frontier=None, n_graft=None, workspace=None, d_err=None,
-                  stream=None):
+                  graft_frontier=None, n_graft=None, N=0, next_frontier=None, n_next=None,
+                  workspace=None, d_err=None, stream=None):
     """One middle-drafter step.  strong_logits [B,R,V] fp32 (row 0 = root,
-    1+i = node i).  Returns (row_lse, graft_frontier, n_graft)."""
+    1+i = node i).  Returns (row_lse, graft_frontier, n_graft), plus
+    (next_frontier, n_next) -- the best N grafted children -- when N > 0."""
     lib = load()
     _dev(strong_logits, "strong_logits", torch.float32)
     B, R, V = strong_logits.shape
@@ -269,14 +283,21 @@ def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
     graft_frontier = (torch.empty((B, W), dtype=torch.int32, device=dev)
                       if graft_frontier is None else graft_frontier)
     n_graft = torch.empty((B,), dtype=torch.int32, device=dev) if n_graft is None else n_graft
+    if N > 0:
+        next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
+                         if next_frontier is None else next_frontier)
+        n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
     ws, wsb = _workspace(lib.tg_rescore_graft_workspace(B, R, V, W, M, tree.cap), dev,
                          workspace)
     ts = tree.struct()
     st = lib.tg_tree_rescore_graft(ctypes.byref(ts), _ptr(strong_logits), B, R, V, W, M,
                                    int(flags), _ptr(row_lse), _ptr(graft_frontier),
-                                   _ptr(n_graft), _ptr(ws), wsb, _ptr(d_err),
-                                   _stream(stream))
+                                   _ptr(n_graft), _ptr(next_frontier if N > 0 else None),
+                                   _ptr(n_next if N > 0 else None), int(N), _ptr(ws), wsb,
+                                   _ptr(d_err), _stream(stream))
     _check("tg_tree_rescore_graft", st)
+    if N > 0:
+        return row_lse, graft_frontier, n_graft, next_frontier, n_next
     return row_lse, graft_frontier, n_graft
 
 
@@ -301,3 +322,24 @@ def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_pa
                             _ptr(d_err), _stream(stream))
     _check("tg_tree_accept", st)
     return accept_len, accept_path, bonus
+
+
+def tree_reset(tree: TreeState, stream=None):
+    """Empty every tree (n_nodes = 0, root unvisited) with a device kernel."""
+    lib = load()
+    ts = tree.struct()
+    _check("tg_tree_reset", lib.tg_tree_reset(ctypes.byref(ts), tree.B, _stream(stream)))
+
+
+def trace_begin(capacity: int = 4096):
+    """Turn on per-kernel device timing (see tg_trace_begin)."""
+    _check("tg_trace_begin", load().tg_trace_begin(int(capacity)))
+
+
+def trace_end(max_records: int = 1 << 16):
+    """Turn tracing off; returns [(kernel name, milliseconds)] in launch order."""
+    lib = load()
+    recs = (TgTraceRecord * max_records)()
+    n = ctypes.c_int(0)
+    _check("tg_trace_end", lib.tg_trace_end(recs, max_records, ctypes.byref(n)))
+    return [(recs[i].kernel.decode(), float(recs[i].ms)) for i in range(n.value)]

@@ -115,7 +115,7 @@ hipError_t launch_accept(const int32_t *parent, const int32_t *token,
                          int cap, int max_depth, int32_t *accept_len,
                          int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
                          hipStream_t stream) {
-  hipLaunchKernelGGL(accept_kernel, dim3(B), dim3(kThreads), 0, stream, parent,
+  launch("accept", accept_kernel, dim3(B), dim3(kThreads), 0, stream, parent,
                      token, n_nodes, greedy, cap, max_depth, accept_len,
                      accept_path, bonus, d_err);
   return hipGetLastError();

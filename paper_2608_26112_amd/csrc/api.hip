@@ -48,6 +48,11 @@ const char *tg_status_str(tg_status s) {
   return "unknown status";
 }
 
+tg_status tg_tree_reset(const tg_tree *tree, int B, void *stream) {
+  if (!tree_ok(tree) || B <= 0) return TG_ERR_INVALID_ARG;
+  return from_hip(tg::launch_tree_reset(*tree, B, reinterpret_cast<hipStream_t>(stream)));
+}
+
 // ------------------------------------------------------------ verify attention
 size_t tg_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
                                      int S_max, tg_dtype dtype) {
@@ -131,10 +136,13 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 int B, int R, int V, int W, int M,
                                 uint32_t flags, float *row_lse,
                                 int32_t *graft_frontier, int32_t *n_graft,
+                                int32_t *next_frontier, int32_t *n_next, int N,
                                 void *workspace, size_t ws_bytes,
                                 uint32_t *d_err, void *stream) {
   if (!tree_ok(tree) || !strong_logits || !row_lse || !graft_frontier || !n_graft)
     return TG_ERR_INVALID_ARG;
+  if ((next_frontier == nullptr) != (n_next == nullptr)) return TG_ERR_INVALID_ARG;
+  if (next_frontier && N <= 0) return TG_ERR_INVALID_ARG;
   if (B <= 0 || R <= 0 || V <= 0 || W <= 0 || M <= 0) return TG_ERR_INVALID_ARG;
   if (M > V) return TG_ERR_INVALID_ARG;
   if (flags != 0) return TG_ERR_UNSUPPORTED;
@@ -154,7 +162,8 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   if (e != hipSuccess) return TG_ERR_HIP;
   return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan,
                                           needed, ms, keys, row_lse, graft_frontier,
-                                          n_graft, d_err, st));
+                                          n_graft, next_frontier, n_next,
+                                          next_frontier ? N : 0, d_err, st));
 }
 
 // ------------------------------------------------------------------- accept

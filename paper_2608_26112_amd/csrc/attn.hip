@@ -456,10 +456,10 @@ hipError_t launch_attn_f32(const AttnShape &s, const float *q, const float *k,
   const long long rows = (long long)s.B * s.N * s.Hq;
   dim3 grid((unsigned)((rows + 3) / 4)), blk(kThreads);
   if (s.D == 64)
-    hipLaunchKernelGGL(attn_f32_kernel<64>, grid, blk, 0, stream, q, k, v, parent,
+    launch("attn_f32", attn_f32_kernel<64>, grid, blk, 0, stream, q, k, v, parent,
                        prefix_len, out, s.B, s.N, s.Hq, s.Hkv, s.S_max, s.sm_scale, d_err);
   else
-    hipLaunchKernelGGL(attn_f32_kernel<128>, grid, blk, 0, stream, q, k, v, parent,
+    launch("attn_f32", attn_f32_kernel<128>, grid, blk, 0, stream, q, k, v, parent,
                        prefix_len, out, s.B, s.N, s.Hq, s.Hkv, s.S_max, s.sm_scale, d_err);
   return hipGetLastError();
 }
@@ -482,21 +482,21 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   auto vb = reinterpret_cast<const __bf16 *>(v);
   auto ob = reinterpret_cast<__bf16 *>(out);
   if (s.D == 64)
-    hipLaunchKernelGGL(attn_mfma_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0,
+    launch("attn_mfma", attn_mfma_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0,
                        stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse,
                        s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2, tiles, sp, d_err);
   else
-    hipLaunchKernelGGL(attn_mfma_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0,
+    launch("attn_mfma", attn_mfma_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0,
                        stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse,
                        s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2, tiles, sp, d_err);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || sp <= 1) return e;
   const unsigned cgrid = (unsigned)((rows + 3) / 4);
   if (s.D == 64)
-    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(cgrid), dim3(kThreads), 0, stream,
+    launch("attn_combine", attn_combine_kernel<64>, dim3(cgrid), dim3(kThreads), 0, stream,
                        part_o, part_lse, prefix_len, ob, s.B, s.N, s.Hq, s.S_max, sp);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(cgrid), dim3(kThreads), 0, stream,
+    launch("attn_combine", attn_combine_kernel<128>, dim3(cgrid), dim3(kThreads), 0, stream,
                        part_o, part_lse, prefix_len, ob, s.B, s.N, s.Hq, s.S_max, sp);
   return hipGetLastError();
 }

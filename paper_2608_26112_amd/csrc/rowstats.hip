@@ -251,7 +251,7 @@ hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   dim3 g((unsigned)grid), blk(kThreads);
 #define TG_ROWS(KC)                                                          \
-  hipLaunchKernelGGL((row_partial_kernel<KC>), g, blk, 0, stream, logits,     \
+  launch("row_partial", (row_partial_kernel<KC>), g, blk, 0, stream, logits,     \
                      rows_per_batch, V, K, plan.chunks, plan.grains_per_chunk,      \
                      n_live, needed, part_ms, part_keys, d_err)
   if (K <= 4)

@@ -7,7 +7,24 @@
 
 #include "../../include/treegraft.h"
 
+#include <hip/hip_ext.h>
+
 namespace tg {
+
+// ------------------------------------------------------------ launching
+// Takes a start/stop event pair when tracing is on (trace.hip).
+bool trace_slot(const char *name, hipEvent_t *start, hipEvent_t *stop);
+
+// Callers check hipGetLastError() afterwards.
+template <typename F, typename... Args>
+void launch(const char *name, F kernel, dim3 grid, dim3 block, size_t shmem,
+            hipStream_t stream, Args... args) {
+  hipEvent_t a, b;
+  if (trace_slot(name, &a, &b))
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shmem, stream, a, b, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, args...);
+}
 
 // ------------------------------------------------------------ logits rows
 // A logits row is cut into grains of kGrain elements; every grain yields one
@@ -40,6 +57,8 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
                               int32_t *next_frontier, int32_t *n_next,
                               uint32_t *d_err, hipStream_t stream);
 
+hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream);
+
 hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
                                uint8_t *needed, hipStream_t stream);
 
@@ -48,6 +67,7 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                const uint8_t *needed, const float2 *part_ms,
                                const uint64_t *part_keys, float *row_lse,
                                int32_t *graft_frontier, int32_t *n_graft,
+                               int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t *d_err, hipStream_t stream);
 
 // ----------------------------------------------------------------- accept

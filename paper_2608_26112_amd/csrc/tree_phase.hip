@@ -177,7 +177,8 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     int chunks, int n_ms, const uint8_t *__restrict__ needed,
     const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
     float *__restrict__ row_lse, int32_t *__restrict__ graft_frontier,
-    int32_t *__restrict__ n_graft, uint32_t *d_err) {
+    int32_t *__restrict__ n_graft, int32_t *__restrict__ next_frontier,
+    int32_t *__restrict__ n_next, int N, uint32_t *d_err) {
   extern __shared__ uint64_t smem[];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & (kWave - 1), w = tid / kWave;
@@ -185,23 +186,29 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   const int nb = tree.n_nodes[b];
   const size_t base = (size_t)b * cap;
 
-  const bool bad_tree = nb < 0 || nb > cap || nb + 1 > R;
-  if (bad_tree) {
+  auto fail = [&](uint32_t bit) {
     if (tid == 0) {
-      report(d_err, TG_DERR_BAD_NODE);
+      report(d_err, bit);
       n_graft[b] = 0;
+      if (N > 0) n_next[b] = 0;
     }
     for (int f = tid; f < W; f += kThreads) graft_frontier[(size_t)b * W + f] = TG_NO_NODE;
+    for (int j = tid; j < N; j += kThreads) next_frontier[(size_t)b * N + j] = TG_NO_NODE;
+  };
+  if (nb < 0 || nb > cap || nb + 1 > R) {
+    fail(TG_DERR_BAD_NODE);
     return;
   }
+  // LDS layout sized by cap (as allocated by the launcher), used up to nb
+  const int P2cap = pow2_at_least(cap + 1);
   const int P2 = pow2_at_least(nb + 1);
-  uint64_t *skey = smem;                                   // [P2]
-  float *lse_s = reinterpret_cast<float *>(skey + P2);     // [nb + 1]
-  float *cum_s = lse_s + (nb + 1);                         // [nb]
-  float *lp_s = cum_s + nb;                                // [nb]
-  int *par_s = reinterpret_cast<int *>(lp_s + nb);         // [nb]
-  uint8_t *inC = reinterpret_cast<uint8_t *>(par_s + nb);  // [nb]
-  uint8_t *done = inC + nb;                                // [nb]
+  uint64_t *skey = smem;                                   // [P2cap]
+  float *lse_s = reinterpret_cast<float *>(skey + P2cap);  // [cap + 1]
+  float *cum_s = lse_s + (cap + 1);                        // [cap]
+  float *lp_s = cum_s + cap;                               // [cap]
+  int *par_s = reinterpret_cast<int *>(lp_s + cap);        // [cap]
+  uint8_t *inC = reinterpret_cast<uint8_t *>(par_s + cap); // [cap]
+  uint8_t *done = inC + cap;                               // [cap]
 
   // ---- pool C and parents
   bool badp = false;
@@ -238,11 +245,7 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
 
   const int nF = min(W, poolC);
   if (nb + nF * M > cap) {
-    if (tid == 0) {
-      report(d_err, TG_DERR_CAPACITY);
-      n_graft[b] = 0;
-    }
-    for (int f = tid; f < W; f += kThreads) graft_frontier[(size_t)b * W + f] = TG_NO_NODE;
+    fail(TG_DERR_CAPACITY);
     return;
   }
 
@@ -335,9 +338,43 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     tree.n_nodes[b] = nb + nF * M;
     n_graft[b] = nF;
   }
+  // ---- Top_N of the grafted children (the next small step's frontier)
+  if (N > 0) {
+    __syncthreads();  // children written above are visible to the block
+    const int total = nF * M;
+    const int P2c = pow2_at_least(total > 0 ? total : 1);
+    for (int c = tid; c < P2c; c += kThreads) {
+      uint64_t k = 0;
+      if (c < total) {
+        const int id = nb + c;
+        k = node_key(tree.cum[base + id], tree.depth[base + id], id);
+      }
+      skey[c] = k;
+    }
+    __syncthreads();
+    block_bitonic_desc(skey, P2c);
+    const int nn = min(N, total);
+    for (int j = tid; j < N; j += kThreads)
+      next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
+    if (tid == 0) n_next[b] = nn;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void tree_reset_kernel(tg_tree tree, int B) {
+  const int b = blockIdx.x * kThreads + threadIdx.x;
+  if (b < B) {
+    tree.n_nodes[b] = 0;
+    tree.root_visited[b] = 0;
+  }
 }
 
 }  // namespace
+
+hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream) {
+  launch("tree_reset", tree_reset_kernel, dim3((B + kThreads - 1) / kThreads),
+         dim3(kThreads), 0, stream, tree, B);
+  return hipGetLastError();
+}
 
 static size_t expand_lds(int F, int K) {
   int total = F * K;
@@ -356,7 +393,7 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
+  launch("expand_tree", expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
                      tree, frontier, n_frontier, F, K, N, plan.chunks, plan.ms_per_row, part_ms,
                      part_keys, row_lse, next_frontier, n_next, d_err);
   return hipGetLastError();
@@ -364,7 +401,7 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
 
 hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
                                uint8_t *needed, hipStream_t stream) {
-  hipLaunchKernelGGL(rescore_pool_kernel, dim3(B), dim3(kThreads), 0, stream,
+  launch("rescore_pool", rescore_pool_kernel, dim3(B), dim3(kThreads), 0, stream,
                      tree, R, needed);
   return hipGetLastError();
 }
@@ -374,18 +411,20 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                const uint8_t *needed, const float2 *part_ms,
                                const uint64_t *part_keys, float *row_lse,
                                int32_t *graft_frontier, int32_t *n_graft,
+                               int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t *d_err, hipStream_t stream) {
   // worst case over any live node count up to cap
-  int n = tree.cap;
+  const int n = tree.cap;
   size_t lds = (size_t)pow2_at_least(n + 1) * 8 + (size_t)(n + 1) * 4 +
                (size_t)n * (4 + 4 + 4 + 1 + 1);
   hipError_t e = hipFuncSetAttribute((const void *)rescore_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
+  launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
                      tree, strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms,
-                     part_keys, row_lse, graft_frontier, n_graft, d_err);
+                     part_keys, row_lse, graft_frontier, n_graft, next_frontier,
+                     n_next, N, d_err);
   return hipGetLastError();
 }
 

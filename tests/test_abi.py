@@ -137,6 +137,7 @@ def _rescore(lib, tree=None, **kw):
     t = _tree() if tree is None else tree
     return lib.tg_tree_rescore_graft(ctypes.byref(t), a["strong"], a["B"], a["R"], a["V"],
                                      a["W"], a["M"], a["flags"], a["lse"], a["gf"], a["ng"],
+                                     a.get("nx", NULL), a.get("nn", NULL), a.get("N", 0),
                                      a["ws"], a["wsb"], NULL, NULL)
 
 
@@ -146,6 +147,8 @@ def test_rescore_host_checks(lib):
     assert _rescore(lib, W=0) == tg.ERR_INVALID_ARG
     assert _rescore(lib, M=2000) == tg.ERR_INVALID_ARG
     assert _rescore(lib, flags=1) == tg.ERR_UNSUPPORTED
+    assert _rescore(lib, nx=P) == tg.ERR_INVALID_ARG              # n_next missing
+    assert _rescore(lib, nx=P, nn=P, N=0) == tg.ERR_INVALID_ARG   # N must be >= 1
     assert _rescore(lib, M=100, V=5000) == tg.ERR_UNSUPPORTED
     assert _rescore(lib, ws=NULL) == tg.ERR_WORKSPACE
     need = lib.tg_rescore_graft_workspace(1, 17, 1000, 8, 4, 64)
@@ -165,6 +168,15 @@ def test_accept_host_checks(lib):
     assert acc(md=-1) == tg.ERR_INVALID_ARG
     assert acc(path=NULL) == tg.ERR_INVALID_ARG
     assert acc(cap=5000) == tg.ERR_UNSUPPORTED
+
+
+def test_reset_and_trace_host_checks(lib):
+    import paper_2608_26112_amd as tg
+    assert lib.tg_tree_reset(ctypes.byref(_tree(n_nodes=1)), 1, NULL) == tg.ERR_INVALID_ARG
+    assert lib.tg_tree_reset(ctypes.byref(_tree()), 0, NULL) == tg.ERR_INVALID_ARG
+    assert lib.tg_trace_begin(0) == tg.ERR_INVALID_ARG
+    n = ctypes.c_int(7)
+    assert lib.tg_trace_end(None, 0, ctypes.byref(n)) == tg.ERR_INVALID_ARG  # not tracing
 
 
 def test_python_binding_rejects_cpu_tensors():

@@ -257,17 +257,18 @@ def test_twodrafter_expand(tg, twodrafter):
 
 # ----------------------------------------------------------- rescore + graft
 
-def run_rescore(tg, tree_h, strong, Wsel, M, check_free=True):
+def run_rescore(tg, tree_h, strong, Wsel, M, check_free=True, N=7):
     ts = C.tree_to_dev(tg, tree_h)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
-    lse, gf, ng = tg.rescore_graft(ts, _d(strong), Wsel, M, d_err=err)
+    lse, gf, ng, nx, nn = tg.rescore_graft(ts, _d(strong), Wsel, M, N=N, d_err=err)
     torch.cuda.synchronize()
     lse_g, gf_g, ng_g = lse.cpu().numpy(), gf.cpu().numpy(), ng.cpu().numpy()
     got = C.tree_from_dev(ts)
-    want, lse_o, gf_o, ng_o, err_o = OT.rescore_graft(tree_h, strong, Wsel, M,
-                                                      lse_override=np.nan_to_num(lse_g, nan=0.0))
+    want, lse_o, gf_o, ng_o, err_o, nx_o, nn_o = OT.rescore_graft(
+        tree_h, strong, Wsel, M, lse_override=np.nan_to_num(lse_g, nan=0.0), N=N)
     C.assert_tree_equal(got, want, "rescore")
     assert np.array_equal(gf_g, gf_o) and np.array_equal(ng_g, ng_o)
+    assert np.array_equal(nx.cpu().numpy(), nx_o) and np.array_equal(nn.cpu().numpy(), nn_o)
     assert int(err.item()) == err_o
     # rows written exactly where the oracle reads them
     assert np.array_equal(np.isnan(lse_g), np.isnan(lse_o))
@@ -304,7 +305,7 @@ def test_rescore_graft_golden(tg):
     for call in gd["calls"]:
         e = call["expect"]
         n0 = int(t.n_nodes[0])
-        t, lse, gf, ng, err = run_rescore(tg, t, rows, call["W"], call["M"])
+        t, lse, gf, ng, err = run_rescore(tg, t, rows, call["W"], call["M"], N=call["N"])
         assert err == 0
         assert list(gf[0, :ng[0]]) == e["graft_frontier"]
         assert list(t.token[0, n0:int(t.n_nodes[0])]) == e["new_token"]

@@ -244,8 +244,11 @@ def test_rescore_graft_golden():
         e = call["expect"]
         n0 = int(t.n_nodes[0])
         old = (t.parent[0, :n0].copy(), t.token[0, :n0].copy(), t.depth[0, :n0].copy())
-        t, lse, fr, ng, err = T.rescore_graft(t, rows, call["W"], call["M"])
+        t, lse, fr, ng, err, nx, nn = T.rescore_graft(t, rows, call["W"], call["M"],
+                                                      N=call["N"])
         assert err == 0
+        assert list(nx[0, :nn[0]]) == e["next_frontier"]
+        assert all(v == T.NO_NODE for v in nx[0, nn[0]:])
         np.testing.assert_allclose(np.exp(t.cum[0, :n0].astype(np.float64)),
                                    e["prob_existing"], rtol=3e-6)
         assert int(ng[0]) == e["n_graft"]
@@ -325,7 +328,8 @@ def test_rescore_graft_invariants(seed):
     strong = W.normal(g, (B, R, V), 3.0)
     Wsel, M = int(g.integers(1, 8)), int(g.integers(1, 4))
     before = tree.copy()
-    t2, lse, fr, ng, err = T.rescore_graft(tree, strong, Wsel, M)
+    Nn = int(g.integers(1, 20))
+    t2, lse, fr, ng, err, nx, nn = T.rescore_graft(tree, strong, Wsel, M, N=Nn)
     assert err == 0
     for b in range(B):
         n = int(before.n_nodes[b])
@@ -362,6 +366,11 @@ def test_rescore_graft_invariants(seed):
             p = -1 if v < 0 else int(before.parent[b, v])
             if v >= 0 and p in set(C_all):
                 assert p in Fs
+        # next frontier: best Nn grafted children, by pairwise counting
+        kids = list(range(n, int(t2.n_nodes[b])))
+        kk = {v: (float(t2.cum[b, v]), int(t2.depth[b, v]), v) for v in kids}
+        krank = {v: sum(_beats(kk[u], kk[v]) for u in kids) for v in kids}
+        assert list(nx[b, :nn[b]]) == sorted(kids, key=lambda v: krank[v])[:Nn]
         # grafted children: rank-j token of the frontier node's own row
         for f, v in enumerate(want):
             toks = _topk_bruteforce(strong[b, v + 1], M)
