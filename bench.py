@@ -67,6 +67,9 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--workload", default="turn",
+                    choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b"],
+                    help="turn (default) or tree-verify attention alone at one shape")
     return ap.parse_args()
 
 
@@ -227,6 +230,96 @@ def cpu_baseline(inp, trees, budget_s):
             return turns, el, blas
 
 
+# ------------------------------------------------------- attention alone
+
+ATTN_SHAPES = {
+    # name: (B, Hq, Hkv, D, prefix, nodes, levels, qkv scale)
+    "attn-llama8b": (1, 32, 8, 128, 2048, 64, None, 1.0 / np.sqrt(128.0)),
+    "attn-longctx": (4, 32, 8, 128, 8192, 128, 10, 1.0),
+    "attn-llama70b": (8, 64, 8, 128, 32768, 256, 12, 1.0),
+}
+
+
+def attention_bench(args, tg, torch, dev):
+    """tg_tree_verify_attention alone at one workload shape; inputs rotate over
+    enough copies to exceed 512 MB so no timed read hits the MALL."""
+    import workloads as W
+    Bq, Hq, Hkv, Dh, Lp, Nn, levels, scale = ATTN_SHAPES[args.workload]
+    g = W.rng(2000)
+    if levels is None:
+        par = np.stack([W.verify_layout_with_root(W.expansion_shaped_tree(g, Nn - 1, 6, 8, 10))
+                        for _ in range(Bq)])
+    else:
+        par = np.stack([W.level_tree(g, Nn, levels, 8) for _ in range(Bq)])
+    S = Lp + Nn
+    per_copy = 2 * Bq * Hkv * S * Dh * 2
+    copies = max(1, min(8, -(-(512 << 20) // per_copy)))
+    bufs = []
+    for c in range(copies):
+        gc = W.rng([2000, c])
+        q = torch.empty((Bq, Nn, Hq, Dh), dtype=torch.bfloat16, device=dev)
+        k = torch.empty((Bq, Hkv, S, Dh), dtype=torch.bfloat16, device=dev)
+        v = torch.empty((Bq, Hkv, S, Dh), dtype=torch.bfloat16, device=dev)
+        for b in range(Bq):
+            q[b] = torch.from_numpy(W.normal(gc, (Nn, Hq, Dh)) * np.float32(scale)).to(dev)
+            k[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
+            v[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
+        bufs.append((q, k, v, torch.empty_like(q)))
+    parent = torch.from_numpy(par.astype(np.int32)).to(dev)
+    plen = torch.full((Bq,), Lp, dtype=torch.int32, device=dev)
+    nws = tg.verify_attention_workspace(Bq, Nn, Hq, Hkv, Dh, S, tg.BF16)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+
+    def call(i):
+        q, k, v, o = bufs[i % copies]
+        tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    tg.trace_begin(4 * (args.steps + 1))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    recs = tg.trace_end()
+    ms = e0.elapsed_time(e1) / args.steps
+    kern = {}
+    for name, t in recs:
+        d = kern.setdefault(name, [0, 0.0])
+        d[0] += 1
+        d[1] += t
+    main_us = 1e3 * kern["attn_mfma"][1] / kern["attn_mfma"][0]
+    keys = sum(Nn * Lp + path_len_sum(par[b]) for b in range(Bq))
+    flops = 4 * Dh * Hq * keys
+    nbytes = 2 * Bq * Hkv * S * Dh * 2 + 2 * Bq * Nn * Hq * Dh * 2 + par.nbytes
+    ridge = PEAK_BF16 / PEAK_HBM
+    bound = "mfma" if flops / nbytes > ridge else "hbm"
+    call_s = ms * 1e-3
+    if bound == "mfma":
+        ach, peak, unit = flops / (main_us * 1e-6) / 1e12, PEAK_BF16 / 1e12, "TFLOP/s"
+    else:
+        ach, peak, unit = nbytes / (main_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s"
+    out = {
+        "metric": METRIC, "value": (flops if bound == "mfma" else nbytes) / call_s / 1e12,
+        "unit": "TFLOP/s" if bound == "mfma" else "TB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "batch": Bq, "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": Dh, "prefix": Lp, "tree_nodes": Nn, "input_copies": copies},
+        "roofline": {"bound": bound, "kernel": "attn_mfma", "achieved": ach, "peak": peak,
+                     "unit": unit, "frac": ach / peak, "traffic": None,
+                     "avg_launch_us": main_us},
+        "TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
+        "bytes": nbytes, "flops": flops,
+        "kernels": {k: {"launches_per_call": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0]}
+                    for k, v in kern.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -242,6 +335,9 @@ def main():
     tg.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.workload != "turn":
+        attention_bench(args, tg, torch, dev)
+        return
 
     trees = make_trees(dev)
     inputs = [make_inputs(c, dev) for c in range(args.copies)]

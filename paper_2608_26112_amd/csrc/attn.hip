@@ -20,6 +20,8 @@
 //
 // attn_f32_kernel (fp32): one wave per (batch, node, head) row, VALU dot
 // products, online softmax, fp32 throughout.
+#include <algorithm>
+
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -35,13 +37,33 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per tile
-constexpr int kMaxNodeWords = TG_MAX_VERIFY_NODES / 32;
 
 __device__ __forceinline__ bool bad_prefix(int L, int N, int S_max) {
   return L < 0 || L + N > S_max;
 }
 
 // ------------------------------------------------------------ bf16 / MFMA
+// LDS row pitches (bf16 elements): K rows are read 16 bytes per lane with one
+// key per lane, V rows with the transposed 8-byte read in 4-row x 16-column
+// blocks; the paddings put the rows a lane group touches on distinct banks.
+template <int D> struct AttnLds {
+  static constexpr int KP = D + 8;    // K row pitch
+  static constexpr int VP = D + 32;   // V row pitch
+  static constexpr int KBUF = BN * KP;
+  static constexpr int VBUF = BN * VP;
+  static constexpr int STAGE = KBUF + VBUF;
+  static constexpr size_t bytes(int anc_words) {
+    return (size_t)2 * STAGE * 2 + (size_t)anc_words * 4;
+  }
+};
+
+__device__ __forceinline__ bf16x4 lds_read_tr4(const __bf16 *p) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4 *)(p));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
@@ -50,14 +72,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     float *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
     int Hq, int Hkv, int S_max, float scale2, int n_tiles, int n_splits,
     uint32_t *d_err) {
+  using Lds = AttnLds<D>;
   constexpr int KS = D / 16;  // k-steps of the QK^T product
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
-  constexpr int KPAD = D + 8;
-  constexpr int VPAD = BN + 8;
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KPAD];
-  __shared__ __attribute__((aligned(16))) __bf16 Vt[D * VPAD];
-  __shared__ int par_s[TG_MAX_VERIFY_NODES];
-  __shared__ uint32_t anc_s[BM * kMaxNodeWords];
+  constexpr int CPR = D / 8;  // 16-byte chunks per K/V row
+  constexpr int LOADS = BN * CPR / kThreads;
+  extern __shared__ __attribute__((aligned(16))) __bf16 lds[];
+  uint32_t *anc_s = reinterpret_cast<uint32_t *>(lds + 2 * Lds::STAGE);
+  int *par_s = reinterpret_cast<int *>(lds);  // prologue only (aliases stage 0)
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
@@ -92,7 +114,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     return;
   }
 
-  // ---- parents and ancestor-or-self bitsets of this tile's nodes
+  // ---- parents and ancestor-or-self bitsets of this tile's nodes (a1)
   const int node_lo = row0 / G;
   const int node_hi = min(N, (row0 + BM - 1) / G + 1);
   const int nloc = node_hi - node_lo;
@@ -113,7 +135,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     uint32_t *row = anc_s + tid * NW;
     for (int u = node_lo + tid; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
   }
-  __syncthreads();
+  __syncthreads();  // bitsets ready; par_s (stage 0) free again
 
   // ---- this lane's query row, Q fragment in registers
   const int qrow = row0 + w * 32 + r32;
@@ -125,12 +147,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   {
     const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if (qvalid)
-        qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
-      else
-        qf[s] = bf16x8{};
-    }
+    for (int s = 0; s < KS; ++s)
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
   }
 
   // ---- key ranges: this split's share of the prefix, then (last split) tree
@@ -140,7 +158,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   const int p_end = min(L, p_beg + chunk);
   const bool do_tree = split == n_splits - 1;
   const int n_ptiles = (p_end - p_beg + BN - 1) / BN;
-  const int n_ttiles = do_tree ? (N + BN - 1) / BN : 0;
+  const int n_tiles_all = n_ptiles + (do_tree ? (N + BN - 1) / BN : 0);
 
   const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
   const __bf16 *kb = kc + kv_base;
@@ -149,40 +167,59 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   f32x16 o[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x16{};
-  float m = -__builtin_inff();  // running max, log2 domain
+  float m = -__builtin_inff();  // running max, scaled log2 units
   float l = 0.0f;               // this lane's share of the running sum
 
-  constexpr int CPR = D / 8;                 // 16-byte chunks per row
-  constexpr int LOADS = BN * CPR / kThreads; // per thread per matrix
-
-  for (int t = 0; t < n_ptiles + n_ttiles; ++t) {
-    const bool tree_tile = t >= n_ptiles;
-    const int k0 = tree_tile ? L + (t - n_ptiles) * BN : p_beg + t * BN;
-    const int k_lim = tree_tile ? L + N : p_end;
-
-    // ---- stage K (row-major) and V (transposed) tiles in LDS
+  bf16x8 kreg[LOADS], vreg[LOADS];
+  auto tile_k0 = [&](int t) { return t >= n_ptiles ? L + (t - n_ptiles) * BN : p_beg + t * BN; };
+  auto tile_lim = [&](int t) { return t >= n_ptiles ? L + N : p_end; };
+  auto fetch = [&](int t) {
+    const int k0 = tile_k0(t), lim = tile_lim(t);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int c = tid + i * kThreads;
+      const int row = k0 + c / CPR;
+      const int cc = c % CPR;
+      if (row < lim) {
+        kreg[i] = *reinterpret_cast<const bf16x8 *>(kb + (size_t)row * D + cc * 8);
+        vreg[i] = *reinterpret_cast<const bf16x8 *>(vb + (size_t)row * D + cc * 8);
+      } else {
+        kreg[i] = bf16x8{};
+        vreg[i] = bf16x8{};
+      }
+    }
+  };
+  auto stash = [&](__bf16 *st) {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int c = tid + i * kThreads;
       const int kr = c / CPR, cc = c % CPR;
-      const int row = k0 + kr;
-      bf16x8 kv8 = bf16x8{}, vv8 = bf16x8{};
-      if (row < k_lim) {
-        kv8 = *reinterpret_cast<const bf16x8 *>(kb + (size_t)row * D + cc * 8);
-        vv8 = *reinterpret_cast<const bf16x8 *>(vb + (size_t)row * D + cc * 8);
-      }
-      *reinterpret_cast<bf16x8 *>(Ks + kr * KPAD + cc * 8) = kv8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(cc * 8 + e) * VPAD + kr] = vv8[e];
+      *reinterpret_cast<bf16x8 *>(st + kr * Lds::KP + cc * 8) = kreg[i];
+      *reinterpret_cast<bf16x8 *>(st + Lds::KBUF + kr * Lds::VP + cc * 8) = vreg[i];
     }
-    __syncthreads();
+  };
+
+  if (n_tiles_all > 0) {
+    fetch(0);
+    stash(lds);
+  }
+  __syncthreads();
+
+  for (int t = 0; t < n_tiles_all; ++t) {
+    const __bf16 *Kt = lds + (t & 1) * Lds::STAGE;
+    const __bf16 *Vt = Kt + Lds::KBUF;
+    const bool has_next = t + 1 < n_tiles_all;
+    if (has_next) fetch(t + 1);  // global loads stay in flight during compute
+    const bool tree_tile = t >= n_ptiles;
+    const int k0 = tile_k0(t);
+    const int k_lim = tile_lim(t);
 
     // ---- S^T = K Q^T for two 32-key blocks
     f32x16 acc[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       acc[blk] = f32x16{};
-      const __bf16 *kp = Ks + (blk * 32 + r32) * KPAD + 8 * h;
+      const __bf16 *kp = Kt + (blk * 32 + r32) * Lds::KP + 8 * h;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         bf16x8 a = *reinterpret_cast<const bf16x8 *>(kp + 16 * s);
@@ -190,49 +227,62 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
       }
     }
 
-    // ---- mask + online softmax (lane owns query r32, keys below)
-    uint32_t tw[2] = {0xffffffffu, 0xffffffffu};
-    if (tree_tile) {
-      const int j0 = k0 - L;  // multiple of 64
-      tw[0] = my_anc[(j0 >> 5)];
-      tw[1] = ((j0 >> 5) + 1) < NW ? my_anc[(j0 >> 5) + 1] : 0u;
-    }
-    float mx = -__builtin_inff();
+    // ---- mask (partial prefix tile or tree tile only)
+    if (tree_tile || k0 + BN > k_lim) {
+      uint32_t tw0 = 0xffffffffu, tw1 = 0xffffffffu;
+      if (tree_tile) {
+        const int wj = (k0 - L) >> 5;  // k0 - L is a multiple of 64
+        tw0 = my_anc[wj];
+        tw1 = wj + 1 < NW ? my_anc[wj + 1] : 0u;
+      }
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
+      for (int blk = 0; blk < 2; ++blk) {
+        const uint32_t tw = blk ? tw1 : tw0;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kk = blk * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        bool valid = (k0 + kk) < k_lim;
-        if (tree_tile) valid = valid && ((tw[blk] >> (kk & 31)) & 1u);
-        float sv = valid ? acc[blk][r] * scale2 : -__builtin_inff();
-        acc[blk][r] = sv;
-        mx = fmaxf(mx, sv);
+        for (int r = 0; r < 16; ++r) {
+          const int kk = blk * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          const bool valid = (k0 + kk) < k_lim && ((tw >> (kk & 31)) & 1u);
+          acc[blk][r] = valid ? acc[blk][r] : -__builtin_inff();
+        }
       }
     }
+
+    // ---- online softmax: one cross-lane max per tile, lazy O rescale
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(acc[blk][r], acc[blk][r + 1]));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m, mx);
-    // Rows whose keys are all masked so far keep m = -inf; they use 0 as the
-    // reference so every p is exactly 0.  No branch: the MFMAs below run with
-    // the whole wave active.
-    const float m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+    const float m_new = fmaxf(m, mx * scale2);
+    if (__any(m_new > m)) {
+      // some row's max grew: rescale that row's running sum and output
+      const float alpha = __builtin_amdgcn_exp2f(m - (m_new == -__builtin_inff() ? 0.0f : m_new));
+      l *= alpha;
+#pragma unroll
+      for (int i = 0; i < DB; ++i) o[i] *= alpha;
+      m = m_new;
+    }
+    // rows whose keys are all masked so far keep m = -inf and use 0 as the
+    // reference, so every p is exactly 0
+    const float m_use = m == -__builtin_inff() ? 0.0f : m;
     float ps = 0.0f;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float p = __builtin_amdgcn_exp2f(acc[blk][r] - m_use);
+        const float p = __builtin_amdgcn_exp2f(fmaf(acc[blk][r], scale2, -m_use));
         acc[blk][r] = p;
         ps += p;
       }
     }
-    l = l * alpha + ps;
-#pragma unroll
-    for (int i = 0; i < DB; ++i) o[i] *= alpha;
-    m = m_new;
+    l += ps;
 
-    // ---- O^T += V^T P^T, four 16-key steps
+    // ---- O^T += V^T P^T, four 16-key steps; V^T fragments by transposed
+    // reads of the row-major V tile (lane group: 4 keys x 16 d)
+    const int grp = lane >> 4, gl = lane & 15;
+    const int vrow = 4 * (grp >> 1) + (gl >> 2);           // key within the 8-key half
+    const int vcol = 16 * (grp & 1) + 4 * (gl & 3);        // d within the 32-wide block
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
@@ -240,17 +290,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
         bf16x8 pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)acc[blk][8 * u + e];
-        const int kb0 = blk * 32 + 16 * u + 4 * h;
+        const __bf16 *vp = Vt + (blk * 32 + 16 * u + vrow) * Lds::VP + vcol;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const __bf16 *vp = Vt + (db * 32 + r32) * VPAD + kb0;
-          bf16x4 lo = *reinterpret_cast<const bf16x4 *>(vp);
-          bf16x4 hi = *reinterpret_cast<const bf16x4 *>(vp + 8);
-          bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x4 lo = lds_read_tr4(vp + db * 32);
+          const bf16x4 hi = lds_read_tr4(vp + 8 * Lds::VP + db * 32);
+          const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[db], 0, 0, 0);
         }
       }
     }
+    if (has_next) stash(lds + ((t + 1) & 1) * Lds::STAGE);
     __syncthreads();
   }
 
@@ -481,15 +531,28 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   auto kb = reinterpret_cast<const __bf16 *>(k);
   auto vb = reinterpret_cast<const __bf16 *>(v);
   auto ob = reinterpret_cast<__bf16 *>(out);
-  if (s.D == 64)
-    launch("attn_mfma", attn_mfma_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0,
-                       stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse,
-                       s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2, tiles, sp, d_err);
-  else
-    launch("attn_mfma", attn_mfma_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0,
-                       stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse,
-                       s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2, tiles, sp, d_err);
-  hipError_t e = hipGetLastError();
+  // bitset words of the nodes one 128-row tile can hold
+  const int nodes_per_tile = std::min(s.N, (BM + G - 1) / G + 1);
+  const int anc_words = nodes_per_tile * ((s.N + 31) / 32);
+  hipError_t e;
+  if (s.D == 64) {
+    const size_t lds = AttnLds<64>::bytes(anc_words);
+    e = hipFuncSetAttribute((const void *)attn_mfma_kernel<64>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    launch("attn_mfma", attn_mfma_kernel<64>, dim3((unsigned)grid), dim3(kThreads), lds,
+           stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq,
+           s.Hkv, s.S_max, scale2, tiles, sp, d_err);
+  } else {
+    const size_t lds = AttnLds<128>::bytes(anc_words);
+    e = hipFuncSetAttribute((const void *)attn_mfma_kernel<128>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    launch("attn_mfma", attn_mfma_kernel<128>, dim3((unsigned)grid), dim3(kThreads), lds,
+           stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq,
+           s.Hkv, s.S_max, scale2, tiles, sp, d_err);
+  }
+  e = hipGetLastError();
   if (e != hipSuccess || sp <= 1) return e;
   const unsigned cgrid = (unsigned)((rows + 3) / 4);
   if (s.D == 64)
