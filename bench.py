@@ -67,6 +67,9 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="profiling aid: run one device copy of this many MiB first, so a "
+                         "counter pass can scale FETCH_SIZE/WRITE_SIZE by a known size")
     ap.add_argument("--workload", default="turn",
                     choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b"],
                     help="turn (default) or tree-verify attention alone at one shape")
@@ -335,6 +338,13 @@ def main():
     tg.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 18          # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if args.workload != "turn":
         attention_bench(args, tg, torch, dev)
         return

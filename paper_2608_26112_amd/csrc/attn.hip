@@ -43,17 +43,20 @@ __device__ __forceinline__ bool bad_prefix(int L, int N, int S_max) {
 }
 
 // ------------------------------------------------------------ bf16 / MFMA
-// LDS row pitches (bf16 elements): K rows are read 16 bytes per lane with one
-// key per lane, V rows with the transposed 8-byte read in 4-row x 16-column
-// blocks; the paddings put the rows a lane group touches on distinct banks.
+// LDS tiles: K and V rows of D bf16, unpadded, written straight from global
+// memory by global_load_lds (lane l of an instruction lands at base + 16 l).
+// 16-byte chunks are XOR-swizzled with the row (chunk' = chunk ^ (row & CM)) so
+// that the lanes of one K-fragment read (one key per lane) and of one
+// transposed V read (4 keys x 16 d per lane group) hit distinct banks.
 template <int D> struct AttnLds {
-  static constexpr int KP = D + 8;    // K row pitch
-  static constexpr int VP = D + 32;   // V row pitch
-  static constexpr int KBUF = BN * KP;
-  static constexpr int VBUF = BN * VP;
-  static constexpr int STAGE = KBUF + VBUF;
-  static constexpr size_t bytes(int anc_words) {
-    return (size_t)2 * STAGE * 2 + (size_t)anc_words * 4;
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int CM = CPR - 1;          // swizzle mask
+  static constexpr int TILE = BN * D;         // bf16 elements per K (or V) tile
+  static constexpr int STAGE = 2 * TILE;      // K then V
+  static constexpr size_t bytes(int anc_words) { return (size_t)anc_words * 4; }
+  // element offset of (row, d) inside a tile
+  static __device__ __forceinline__ int at(int row, int d) {
+    return row * D + ((((d >> 3) ^ row) & CM) << 3) + (d & 7);
   }
 };
 
@@ -75,11 +78,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   using Lds = AttnLds<D>;
   constexpr int KS = D / 16;  // k-steps of the QK^T product
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
-  constexpr int CPR = D / 8;  // 16-byte chunks per K/V row
-  constexpr int LOADS = BN * CPR / kThreads;
-  extern __shared__ __attribute__((aligned(16))) __bf16 lds[];
-  uint32_t *anc_s = reinterpret_cast<uint32_t *>(lds + 2 * Lds::STAGE);
-  int *par_s = reinterpret_cast<int *>(lds);  // prologue only (aliases stage 0)
+  constexpr int LOADS = BN * D * 2 / 16 / kThreads;  // 16-byte loads per thread per tile
+  // two stages as distinct objects, so the compiler can tell that loads in
+  // flight into one stage do not alias reads of the other
+  __shared__ __attribute__((aligned(16))) __bf16 stage0[Lds::STAGE];
+  __shared__ __attribute__((aligned(16))) __bf16 stage1[Lds::STAGE];
+  extern __shared__ __attribute__((aligned(16))) uint32_t anc_s[];
+  int *par_s = reinterpret_cast<int *>(stage0);  // prologue only
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
@@ -170,60 +175,81 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   float m = -__builtin_inff();  // running max, scaled log2 units
   float l = 0.0f;               // this lane's share of the running sum
 
-  bf16x8 kreg[LOADS], vreg[LOADS];
   auto tile_k0 = [&](int t) { return t >= n_ptiles ? L + (t - n_ptiles) * BN : p_beg + t * BN; };
   auto tile_lim = [&](int t) { return t >= n_ptiles ? L + N : p_end; };
-  auto fetch = [&](int t) {
+  // Direct global -> LDS loads.  Instruction i of wave w fills the 1 KB
+  // block j = w * LOADS + i of a tile: rows j * RPI .. + RPI - 1, and lane l
+  // writes physical chunk l % CPR of its row, i.e. loads logical chunk
+  // (l % CPR) ^ (row & CM).  Offsets are per-thread constants.
+  constexpr int RPI = 64 / Lds::CPR;  // rows per 1 KB instruction
+  int goff[LOADS];
+  int grow[LOADS];
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) {
+    const int row = (w * LOADS + i) * RPI + lane / Lds::CPR;
+    const int chunk = ((lane % Lds::CPR) ^ row) & Lds::CM;
+    grow[i] = row;
+    goff[i] = row * D + chunk * 8;
+  }
+  auto issue = [&](int t, __bf16 *dst) {
     const int k0 = tile_k0(t), lim = tile_lim(t);
+    const __bf16 *kt = kb + (size_t)k0 * D;  // wave-uniform tile base
+    const __bf16 *vt = vb + (size_t)k0 * D;
+    __bf16 *dk = dst;
+    __bf16 *dv = dst + Lds::TILE;
+    auto one = [&](int i, int off) {
+      const int blk_off = (w * LOADS + i) * 512;   // 1 KB block, in bf16 elements
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void *)(kt + off),
+          (__attribute__((address_space(3))) void *)(dk + blk_off), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void *)(vt + off),
+          (__attribute__((address_space(3))) void *)(dv + blk_off), 16, 0, 0);
+    };
+    if (k0 + BN <= lim) {
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int row = k0 + c / CPR;
-      const int cc = c % CPR;
-      if (row < lim) {
-        kreg[i] = *reinterpret_cast<const bf16x8 *>(kb + (size_t)row * D + cc * 8);
-        vreg[i] = *reinterpret_cast<const bf16x8 *>(vb + (size_t)row * D + cc * 8);
-      } else {
-        kreg[i] = bf16x8{};
-        vreg[i] = bf16x8{};
-      }
-    }
-  };
-  auto stash = [&](__bf16 *st) {
+      for (int i = 0; i < LOADS; ++i) one(i, goff[i]);
+    } else {
+      // rows past the range re-read the last valid row (finite, masked later)
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int kr = c / CPR, cc = c % CPR;
-      *reinterpret_cast<bf16x8 *>(st + kr * Lds::KP + cc * 8) = kreg[i];
-      *reinterpret_cast<bf16x8 *>(st + Lds::KBUF + kr * Lds::VP + cc * 8) = vreg[i];
+      for (int i = 0; i < LOADS; ++i)
+        one(i, goff[i] - max(0, k0 + grow[i] - (lim - 1)) * D);
     }
   };
 
-  if (n_tiles_all > 0) {
-    fetch(0);
-    stash(lds);
-  }
+  if (n_tiles_all > 0) issue(0, stage0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  for (int t = 0; t < n_tiles_all; ++t) {
-    const __bf16 *Kt = lds + (t & 1) * Lds::STAGE;
-    const __bf16 *Vt = Kt + Lds::KBUF;
-    const bool has_next = t + 1 < n_tiles_all;
-    if (has_next) fetch(t + 1);  // global loads stay in flight during compute
+  auto step = [&](int t, const __bf16 *cur, __bf16 *nxt) {
+    const __bf16 *Kt = cur;
+    const __bf16 *Vt = cur + Lds::TILE;
+    if (t + 1 < n_tiles_all) issue(t + 1, nxt);  // lands in LDS while tile t computes
     const bool tree_tile = t >= n_ptiles;
     const int k0 = tile_k0(t);
     const int k_lim = tile_lim(t);
 
     // ---- S^T = K Q^T for two 32-key blocks
-    f32x16 acc[2];
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      acc[blk] = f32x16{};
-      const __bf16 *kp = Kt + (blk * 32 + r32) * Lds::KP + 8 * h;
+    f32x16 acc[2] = {f32x16{}, f32x16{}};
+    {
+      // K fragments one step ahead of the MFMAs that consume them
+      const int kr0 = r32, kr1 = 32 + r32;
+      auto kfrag = [&](int kr, int s) {
+        return *reinterpret_cast<const bf16x8 *>(Kt + Lds::at(kr, 16 * s + 8 * h));
+      };
+      bf16x8 a0 = kfrag(kr0, 0);
+      bf16x8 a1 = kfrag(kr1, 0);
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        bf16x8 a = *reinterpret_cast<const bf16x8 *>(kp + 16 * s);
-        acc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], acc[blk], 0, 0, 0);
+        bf16x8 n0 = a0, n1 = a1;
+        if (s + 1 < KS) {
+          n0 = kfrag(kr0, s + 1);
+          n1 = kfrag(kr1, s + 1);
+        }
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], acc[1], 0, 0, 0);
+        a0 = n0;
+        a1 = n1;
       }
     }
 
@@ -248,12 +274,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     }
 
     // ---- online softmax: one cross-lane max per tile, lazy O rescale
-    float mx = -__builtin_inff();
+    float mx;
+    {
+      // 32 values -> 11 three-input maxima -> 4 -> 2 -> 1
+      float t3[11];
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(acc[blk][r], acc[blk][r + 1]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      for (int i = 0; i < 10; ++i) {
+        const int a = 3 * i, b = a + 1, c = a + 2;
+        t3[i] = __builtin_fmaxf(acc[a >> 4][a & 15],
+                                __builtin_fmaxf(acc[b >> 4][b & 15], acc[c >> 4][c & 15]));
+      }
+      t3[10] = __builtin_fmaxf(acc[1][14], acc[1][15]);
+      const float u0 = __builtin_fmaxf(t3[0], __builtin_fmaxf(t3[1], t3[2]));
+      const float u1 = __builtin_fmaxf(t3[3], __builtin_fmaxf(t3[4], t3[5]));
+      const float u2 = __builtin_fmaxf(t3[6], __builtin_fmaxf(t3[7], t3[8]));
+      const float u3 = __builtin_fmaxf(t3[9], t3[10]);
+      mx = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
+    }
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m, mx * scale2);
     if (__any(m_new > m)) {
       // some row's max grew: rescale that row's running sum and output
@@ -266,17 +304,26 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     // rows whose keys are all masked so far keep m = -inf and use 0 as the
     // reference, so every p is exactly 0
     const float m_use = m == -__builtin_inff() ? 0.0f : m;
-    float ps = 0.0f;
+    bf16x8 pb[2][2];
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
+    for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(acc[blk][r], scale2, -m_use));
-        acc[blk][r] = p;
-        ps += p;
-      }
+      for (int r = 0; r < 16; ++r)
+        pb[blk][r >> 3][r & 7] =
+            (__bf16)__builtin_amdgcn_exp2f(fmaf(acc[blk][r], scale2, -m_use));
+    // the normaliser sums exactly the bf16 probabilities the PV product uses
+    {
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; e += 2)
+            l = __builtin_amdgcn_fdot2_f32_bf16(
+                bf16x2{pb[blk][u][e], pb[blk][u][e + 1]}, one2, l, false);
     }
-    l += ps;
 
     // ---- O^T += V^T P^T, four 16-key steps; V^T fragments by transposed
     // reads of the row-major V tile (lane group: 4 keys x 16 d)
@@ -287,21 +334,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        bf16x8 pb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pb[e] = (__bf16)acc[blk][8 * u + e];
-        const __bf16 *vp = Vt + (blk * 32 + 16 * u + vrow) * Lds::VP + vcol;
+        const int vr = blk * 32 + 16 * u + vrow;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x4 lo = lds_read_tr4(vp + db * 32);
-          const bf16x4 hi = lds_read_tr4(vp + 8 * Lds::VP + db * 32);
-          const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[db], 0, 0, 0);
+          const bf16x4 lo = lds_read_tr4(Vt + Lds::at(vr, db * 32 + vcol));
+          const bf16x4 hi = lds_read_tr4(Vt + Lds::at(vr + 8, db * 32 + vcol));
+          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[blk][u], o[db], 0, 0, 0);
         }
       }
     }
-    if (has_next) stash(lds + ((t + 1) & 1) * Lds::STAGE);
+    // this thread's loads into the next stage have landed; then every wave's
+    // loads have landed and nobody reads the current stage any more
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+  // unrolled by two so each half reads and fills fixed stages
+  for (int t = 0; t < n_tiles_all; t += 2) {
+    step(t, stage0, stage1);
+    if (t + 1 < n_tiles_all) step(t + 1, stage1, stage0);
   }
 
   // ---- finalize
