@@ -122,12 +122,13 @@ class Step:
         self.tg, self.inp, self.tr = tg, inp, trees
         i32 = dict(dtype=torch.int32, device=dev)
         self.tree = tg.TreeState(B, CAP, dev)
-        self.ws_r = torch.empty(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
+        # zero-filled once (the library's row counters start at zero)
+        self.ws_r = torch.zeros(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
                                 dtype=torch.uint8, device=dev)
-        self.ws_e = torch.empty(tg.expand_topk_workspace(B, W_FR, V, M_CH, W_FR),
+        self.ws_e = torch.zeros(tg.expand_topk_workspace(B, W_FR, V, M_CH, W_FR),
                                 dtype=torch.uint8, device=dev)
         nv = tg.verify_attention_workspace(B, N_VER, HQ, HKV, D, L + N_VER, tg.BF16)
-        self.ws_v = torch.empty(max(nv, 1), dtype=torch.uint8, device=dev)
+        self.ws_v = torch.zeros(max(nv, 1), dtype=torch.uint8, device=dev)
         self.r_lse = [torch.empty((B, R_ROWS), dtype=torch.float32, device=dev) for _ in range(3)]
         self.gf = [torch.empty((B, W_FR), **i32) for _ in range(3)]
         self.ng = [torch.empty((B,), **i32) for _ in range(3)]
@@ -271,7 +272,7 @@ def attention_bench(args, tg, torch, dev):
     parent = torch.from_numpy(par.astype(np.int32)).to(dev)
     plen = torch.full((Bq,), Lp, dtype=torch.int32, device=dev)
     nws = tg.verify_attention_workspace(Bq, Nn, Hq, Hkv, Dh, S, tg.BF16)
-    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(max(nws, 1), dtype=torch.uint8, device=dev)
 
     def call(i):
         q, k, v, o = bufs[i % copies]
@@ -424,6 +425,8 @@ def main():
         d[1] += ms
     kernels = {k: {"launches_per_step": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0],
                    "us_per_step": 1e3 * v[1] / args.steps} for k, v in kern.items()}
+    per_step = len(recs) // args.steps
+    timeline = [[name, round(1e3 * ms, 2)] for name, ms in recs[-per_step:]]
 
     # ---- accounting
     rows_r, rows_e = rows_read_per_step()
@@ -472,6 +475,7 @@ def main():
         "step_bytes": step_bytes,
         "eager_ms_per_step": ms_eager,
         "kernels": kernels,
+        "step_timeline_us": timeline,
     }
     if not args.no_cpu_baseline:
         turns, el, blas = cpu_baseline(inputs[0], trees, args.cpu_seconds)

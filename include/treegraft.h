@@ -19,7 +19,8 @@
  *   - Every pointer argument is DEVICE memory owned by the caller, except the
  *     tg_tree struct itself, which is a host struct holding device pointers.
  *     The library never allocates per call; scratch memory is the caller's
- *     `workspace`, sized by the matching *_workspace() query.
+ *     `workspace`, sized by the matching *_workspace() query (any contents;
+ *     one call at a time per workspace).
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream).  The returned tg_status reports host-side argument checks and
  *     the kernel launch only.

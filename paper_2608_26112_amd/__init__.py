@@ -149,8 +149,8 @@ def _stream(stream):
 def _workspace(nbytes, device, workspace):
     if nbytes == 0:
         return None, 0
-    if workspace is None:
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if workspace is None:   # zero-filled: the counter block must start at zero
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
     _dev(workspace, "workspace")
     return workspace, workspace.numel() * workspace.element_size()
 

@@ -9,8 +9,8 @@ namespace {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workspace of the row-statistics pass: per (row slot, chunk) the partial
-// (max, sum-exp) pair and the chunk's top-K keys.
+// Workspace of the row-statistics pass: per (row, grain) (max, sum-exp)
+// partials, per (row, chunk) top-K keys, then `extra` bytes for the caller.
 struct RowWs {
   size_t ms_off, keys_off, extra_off, bytes;
 };
@@ -116,12 +116,11 @@ tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
   float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
   uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = tg::launch_row_partials(logits, B, F, V, K, plan, n_frontier,
-                                         nullptr, ms, keys, d_err, st);
+  hipError_t e = tg::launch_row_partials(logits, B, F, V, K, plan, n_frontier, nullptr, ms,
+                                         keys, d_err, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  return from_hip(tg::launch_expand_tree(*tree, frontier, n_frontier, B, F, K, N,
-                                         plan, ms, keys, row_lse, next_frontier,
-                                         n_next, d_err, st));
+  return from_hip(tg::launch_expand_tree(*tree, frontier, n_frontier, B, F, K, N, plan, ms,
+                                         keys, row_lse, next_frontier, n_next, d_err, st));
 }
 
 // ------------------------------------------------------------ rescore + graft
@@ -146,7 +145,8 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   if (B <= 0 || R <= 0 || V <= 0 || W <= 0 || M <= 0) return TG_ERR_INVALID_ARG;
   if (M > V) return TG_ERR_INVALID_ARG;
   if (flags != 0) return TG_ERR_UNSUPPORTED;
-  if (M > TG_MAX_TOPK || tree->cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  if (M > TG_MAX_TOPK || tree->cap > TG_MAX_CAP)
+    return TG_ERR_UNSUPPORTED;
   RowWs w = row_ws((long long)B * R, V, M, (size_t)B * R);
   if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
   tg::RowPlan plan = tg::plan_rows((long long)B * R, V);
@@ -157,13 +157,13 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = tg::launch_rescore_pool(*tree, B, R, needed, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  e = tg::launch_row_partials(strong_logits, B, R, V, M, plan, nullptr, needed, ms,
-                              keys, d_err, st);
+  e = tg::launch_row_partials(strong_logits, B, R, V, M, plan, nullptr, needed, ms, keys,
+                              d_err, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan,
-                                          needed, ms, keys, row_lse, graft_frontier,
-                                          n_graft, next_frontier, n_next,
-                                          next_frontier ? N : 0, d_err, st));
+  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan, needed,
+                                          ms, keys, row_lse, graft_frontier, n_graft,
+                                          next_frontier, n_next, next_frontier ? N : 0,
+                                          d_err, st));
 }
 
 // ------------------------------------------------------------------- accept

@@ -16,7 +16,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
-constexpr int kUnroll = 4;  // float4 loads in flight per thread
+constexpr int kUnroll = 8;  // float4 loads in flight per thread (one grain)
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int KC>
@@ -144,9 +144,9 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     thr = key_threshold(thr_key);
   };
 
-  // Each grain of kGrain elements yields one (max, sum-exp) partial per wave
-  // over a fixed set of elements, so the merged log-sum-exp of a row is the
-  // same bits whatever the chunking.  Trip counts are uniform per workgroup
+  // Each grain of kGrain elements yields one (max, sum-exp) partial over a
+  // fixed set of elements in a fixed reduction order, so the merged
+  // log-sum-exp of a row is the same bits whatever the chunking.  Trip counts are uniform per workgroup
   // (the threshold refresh shuffles across lanes).
   for (int gr = g_beg; gr < g_end; ++gr) {
     m = -__builtin_inff();
@@ -189,12 +189,24 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
         refresh();
       }
     }
+    // one (max, sum-exp) partial per grain: waves by a fixed shuffle tree,
+    // then the four waves in order (LDS double-buffered by grain parity)
+    __shared__ float gm[2][kWavesPerBlock], gs[2][kWavesPerBlock];
     const float mw = wave_max_f32(m);
     const float sc = (m == -__builtin_inff()) ? 0.0f
                                               : s * __builtin_amdgcn_exp2f((m - mw) * kLog2e);
     const float sw = wave_sum_f32(sc);
-    if (lane == 0)
-      part_ms[((size_t)slot * n_grains + gr) * kWavesPerBlock + w] = make_float2(mw, sw);
+    const int par = gr & 1;
+    if (lane == 0) {
+      gm[par][w] = mw;
+      gs[par][w] = sw;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      float M = gm[par][0], S = gs[par][0];
+      for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[par][i], gs[par][i]);
+      part_ms[(size_t)slot * n_grains + gr] = make_float2(M, S);
+    }
   }
   if (bad) report(d_err, TG_DERR_NONFINITE);
 
@@ -223,21 +235,21 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     for (int u = 0; u < nc; ++u) real += cand[u] != 0;
     if (t >= real) part_keys[part * K + t] = 0;
   }
+
 }
 
 }  // namespace
 
 RowPlan plan_rows(long long rows, int V) {
-  // Whole grains per workgroup: enough workgroups to fill the chip when the
-  // call has few rows, whole rows when it has many.
-  const long long target = 2048;
+  // One grain per workgroup (all of it loaded in one batch), so every row is
+  // spread over the chip whatever the row count; rows wider than 64 grains
+  // give each workgroup several grains (the per-row merge holds one chunk
+  // list per lane).
+  (void)rows;
   const int n_grains = (V + kGrain - 1) / kGrain;
-  long long want = rows > 0 ? (target + rows - 1) / rows : 1;  // chunks per row
-  if (want > n_grains) want = n_grains;
-  if (want < 1) want = 1;
-  int per = (int)((n_grains + want - 1) / want);
-  int chunks = (n_grains + per - 1) / per;
-  return RowPlan{chunks, per, n_grains * kWavesPerBlock};
+  const int per = (n_grains + 63) / 64;
+  const int chunks = (n_grains + per - 1) / per;
+  return RowPlan{chunks, per, n_grains};
 }
 
 hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,

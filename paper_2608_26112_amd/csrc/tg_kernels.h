@@ -36,14 +36,14 @@ constexpr int kGrain = 8192;
 struct RowPlan {
   int chunks;
   int grains_per_chunk;
-  int ms_per_row;  // (max, sum-exp) partials per row
+  int ms_per_row;  // (max, sum-exp) partials per row (one per grain)
 };
 RowPlan plan_rows(long long rows, int V);
 
-// Partial (max, sum-exp) and top-K keys of every live (row, chunk).
-//   rows are slots s = b * rows_per_batch + r of a [*, rows_per_batch, V] array;
-//   live iff r < n_live[b] (n_live may be NULL = all) when `needed` is NULL,
-//   else iff needed[s] != 0.
+// Row partials of every live row slot s = b * rows_per_batch + r of a
+// [*, rows_per_batch, V] logits array: live iff r < n_live[b] (n_live may be
+// NULL = all) when `needed` is NULL, else iff needed[s] != 0.  Writes per
+// grain (max, sum-exp) and per chunk top-K keys; the tree kernels finish rows.
 hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
                                int V, int K, RowPlan plan,
                                const int32_t *n_live, const uint8_t *needed,

@@ -8,6 +8,8 @@
 // new children grafted without touching existing nodes (rescore_graft).
 // Node selection (Top_W) is a bitonic sort of 64-bit keys in LDS ordered by
 // (cum desc, depth asc, id asc).
+#include <algorithm>
+
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -18,39 +20,79 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
-// Merge the partials of one row with one wave: the row's `n_ms` (max,
-// sum-exp) partials (lane l folds partials l, l + 64, ... in order, then a
-// fixed shuffle tree) and its `chunks` top-K lists.  Returns the row's
-// log-sum-exp (every lane).  When `mykey` is non-null, lane j < K receives
-// the row's j-th best key (0 for lanes >= K).
-__device__ float merge_row_wave(const float2 *__restrict__ ms, int n_ms,
-                                const uint64_t *__restrict__ keys, int chunks,
-                                int K, uint64_t *mykey) {
-  const int lane = threadIdx.x & (kWave - 1);
+// ------------------------------------------------------- finishing rows
+// log-sum-exp of one row from its per-grain (max, sum-exp) partials, folded
+// in grain order (the same bits whatever the call's chunking).
+__device__ float finish_lse(const float2 *__restrict__ ms, int n) {
   float m = -__builtin_inff(), s = 0.0f;
-  for (int i = lane; i < n_ms; i += kWave) {
-    float2 p = ms[i];
+#pragma unroll 8
+  for (int i = 0; i < n; ++i) {
+    const float2 p = ms[i];
     merge_ms(m, s, p.x, p.y);
   }
-  float M = wave_max_f32(m);
-  float sc = (m == -__builtin_inff()) ? 0.0f : s * exp2f((m - M) * kLog2e);
-  float S = wave_sum_f32(sc);
-  float lse = (M == -__builtin_inff()) ? -__builtin_inff() : M + logf(S);
-  if (mykey) {
-    int idx = 0;
-    uint64_t head = lane < chunks ? keys[(size_t)lane * K] : 0;
-    uint64_t mine = 0;
-    for (int j = 0; j < K; ++j) {
-      uint64_t best = wave_max_u64(head);
-      if (head == best && best != 0) {
-        ++idx;
-        head = idx < K ? keys[(size_t)lane * K + idx] : 0;
-      }
-      if (lane == j) mine = best;
+  return m == -__builtin_inff() ? -__builtin_inff() : m + logf(s);
+}
+
+// K-round merge of one row's `chunks` sorted lists (each K keys, best
+// first) staged in LDS at `lists`: lane c holds list c's head, the wave takes
+// the largest head, that list advances.  Lane j < K returns the j-th best key.
+__device__ uint64_t wave_merge_lists(const uint64_t *lists, int chunks, int K) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int idx = 0;
+  uint64_t head = lane < chunks ? lists[lane * K] : 0;
+  uint64_t mine = 0;
+  for (int j = 0; j < K; ++j) {
+    const uint64_t best = wave_max_u64(head);
+    if (head == best && best != 0) {
+      ++idx;
+      head = idx < K ? lists[lane * K + idx] : 0;
     }
-    *mykey = mine;
+    if (lane == j) mine = best;
   }
-  return lse;
+  return mine;
+}
+
+// Top-K of nr consecutive rows (row r's `chunks` lists of K keys at
+// lists + r * chunks * K) into out[r * K + j], best first.  The lists are
+// staged in LDS (`stage`, room for stage_cap >= chunks * K keys) with one
+// global round trip per batch, then a wave merges each row.  chunks <= 64.
+// Called by the whole block; ends synchronised.
+__device__ void block_finish_topk(const uint64_t *__restrict__ lists, int chunks, int K,
+                                  int nr, uint64_t *out, uint64_t *stage, int stage_cap) {
+  const int nk = chunks * K;
+  if (chunks == 1) {
+    for (int i = threadIdx.x; i < nr * K; i += blockDim.x) out[i] = lists[i];
+    __syncthreads();
+    return;
+  }
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const int per = stage_cap / nk;
+  for (int r0 = 0; r0 < nr; r0 += per) {
+    const int rb = min(per, nr - r0);
+    for (int i = threadIdx.x; i < rb * nk; i += blockDim.x) stage[i] = lists[(size_t)r0 * nk + i];
+    __syncthreads();
+    for (int r = w; r < rb; r += kWaves) {
+      const uint64_t key = wave_merge_lists(stage + r * nk, chunks, K);
+      if (lane < K) out[(r0 + r) * K + lane] = key;
+    }
+    __syncthreads();
+  }
+}
+
+// One wave finishes one row's top-K: lane j < K returns the j-th best key.
+// `ws` is this wave's LDS scratch (chunks * K keys).  chunks <= 64.
+__device__ uint64_t wave_finish_topk(const uint64_t *__restrict__ lists, int chunks, int K,
+                                     uint64_t *ws) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (chunks == 1) return lane < K ? lists[lane] : 0;
+  const int nk = chunks * K;
+  for (int i = lane; i < nk; i += kWave) ws[i] = lists[i];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const uint64_t r = wave_merge_lists(ws, chunks, K);
+  __builtin_amdgcn_wave_barrier();   // ws is reused by the wave's next row
+  return r;
 }
 
 __device__ __forceinline__ int sane_parent(int p, int v, bool &bad) {
@@ -65,19 +107,18 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
     const int32_t *__restrict__ n_frontier, int F, int K, int N, int chunks,
     int n_ms, const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
     float *__restrict__ row_lse, int32_t *__restrict__ next_frontier,
-    int32_t *__restrict__ n_next, uint32_t *d_err) {
+    int32_t *__restrict__ n_next, uint32_t *d_err, int skey_cap) {
   extern __shared__ uint64_t smem[];
   const int b = blockIdx.x, tid = threadIdx.x;
-  const int lane = tid & (kWave - 1), w = tid / kWave;
   const int cap = tree.cap;
   int Fb = n_frontier ? n_frontier[b] : F;
   Fb = Fb < 0 ? 0 : (Fb > F ? F : Fb);
   const int nb = tree.n_nodes[b];
   const int total = Fb * K;
   const int P2 = pow2_at_least(total > 0 ? total : 1);
-  uint64_t *topk = smem;                 // [F*K]
-  uint64_t *skey = smem + (size_t)F * K; // [P2]
-  float *lse_s = reinterpret_cast<float *>(skey + P2);  // [F]
+  uint64_t *topk = smem;                       // [F*K]
+  uint64_t *skey = smem + (size_t)F * K;       // [skey_cap >= max(P2, chunks*K)]
+  float *lse_s = reinterpret_cast<float *>(skey + skey_cap);  // [F]
 
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
@@ -86,18 +127,15 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
   }
   bad = __syncthreads_or(bad);
 
-  for (int f = w; f < Fb; f += kWaves) {
-    size_t slot = (size_t)b * F + f;
-    uint64_t mine;
-    float lse = merge_row_wave(part_ms + slot * n_ms, n_ms,
-                               part_keys + slot * chunks * K, chunks, K, &mine);
-    if (lane < K) topk[(size_t)f * K + lane] = mine;
-    if (lane == 0) {
-      row_lse[slot] = lse;
-      lse_s[f] = lse;
-    }
+  // finish the live rows: lse (a thread per row) and top-K (skey as stage)
+  for (int f = tid; f < Fb; f += kThreads) {
+    const size_t slot = (size_t)b * F + f;
+    const float lse = finish_lse(part_ms + slot * n_ms, n_ms);
+    lse_s[f] = lse;
+    row_lse[slot] = lse;
   }
-  __syncthreads();
+  block_finish_topk(part_keys + (size_t)b * F * chunks * K, chunks, K, Fb, topk, skey,
+                    skey_cap);
 
   const bool full = !bad && (nb + total > cap);
   if (bad || full) {
@@ -178,7 +216,7 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
     float *__restrict__ row_lse, int32_t *__restrict__ graft_frontier,
     int32_t *__restrict__ n_graft, int32_t *__restrict__ next_frontier,
-    int32_t *__restrict__ n_next, int N, uint32_t *d_err) {
+    int32_t *__restrict__ n_next, int N, uint32_t *d_err, int stage_off) {
   extern __shared__ uint64_t smem[];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & (kWave - 1), w = tid / kWave;
@@ -230,16 +268,14 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   int poolC = root_in;
   for (int i = 0; i < kWaves; ++i) poolC += red[i];
 
-  // ---- log-sum-exp of every needed row (exported)
+  // ---- log-sum-exp of every needed row (a thread per row), exported
   const uint8_t *need = needed + (size_t)b * R;
-  for (int r = w; r <= nb; r += kWaves) {
+  for (int r = tid; r <= nb; r += kThreads) {
     if (!need[r]) continue;
-    size_t slot = (size_t)b * R + r;
-    float lse = merge_row_wave(part_ms + slot * n_ms, n_ms, nullptr, chunks, M, nullptr);
-    if (lane == 0) {
-      lse_s[r] = lse;
-      row_lse[slot] = lse;
-    }
+    const size_t slot = (size_t)b * R + r;
+    const float lse = finish_lse(part_ms + slot * n_ms, n_ms);
+    lse_s[r] = lse;
+    row_lse[slot] = lse;
   }
   __syncthreads();
 
@@ -303,14 +339,24 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   __syncthreads();
   block_bitonic_desc(skey, P2);
 
+  // ---- P <- P u C; write back rescored path scores (before the graft,
+  // whose staging reuses the per-node scratch)
+  for (int v = tid; v < nb; v += kThreads) {
+    if (inC[v]) tree.cum[base + v] = cum_s[v];
+    tree.visited[base + v] = 1;
+  }
+  __syncthreads();
+
   // ---- non-destructive graft: new children only, ids nb + f*M + j
+  // (wave-private LDS for finishing each graft point's top-M; the region of
+  // the per-node scratch, free by now, or extra room past it)
+  uint64_t *wstage = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(smem) + stage_off) +
+                     (size_t)w * (chunks * M);
   for (int f = w; f < nF; f += kWaves) {
     const int v = node_key_id(skey[f]);
     const int row = v + 1;
     const size_t slot = (size_t)b * R + row;
-    uint64_t key;
-    merge_row_wave(part_ms + slot * n_ms, n_ms, part_keys + slot * chunks * M,
-                   chunks, M, &key);
+    const uint64_t key = wave_finish_topk(part_keys + slot * chunks * M, chunks, M, wstage);
     const float cv = v < 0 ? 0.0f : cum_s[v];
     const int dv = v < 0 ? 0 : tree.depth[base + v];
     const float lse = lse_s[row];
@@ -328,11 +374,6 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   }
   for (int f = tid; f < W; f += kThreads)
     graft_frontier[(size_t)b * W + f] = f < nF ? node_key_id(skey[f]) : TG_NO_NODE;
-  // ---- P <- P u C; write back rescored path scores
-  for (int v = tid; v < nb; v += kThreads) {
-    if (inC[v]) tree.cum[base + v] = cum_s[v];
-    tree.visited[base + v] = 1;
-  }
   if (tid == 0) {
     tree.root_visited[b] = 1;
     tree.n_nodes[b] = nb + nF * M;
@@ -376,10 +417,12 @@ hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream) {
   return hipGetLastError();
 }
 
-static size_t expand_lds(int F, int K) {
-  int total = F * K;
-  return (size_t)F * K * 8 + (size_t)pow2_at_least(total > 0 ? total : 1) * 8 +
-         (size_t)F * 4;
+static int expand_skey_cap(int F, int K, int chunks) {
+  // the sort needs pow2(F*K) keys; finishing rows wants every row's chunk
+  // lists staged at once (one global round trip), up to 64 KiB of them
+  const int total = F * K;
+  const int stage_all = std::min(F * chunks * K, 8192);
+  return std::max({pow2_at_least(total > 0 ? total : 1), chunks * K, stage_all});
 }
 
 hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
@@ -388,14 +431,15 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
                               const uint64_t *part_keys, float *row_lse,
                               int32_t *next_frontier, int32_t *n_next,
                               uint32_t *d_err, hipStream_t stream) {
-  size_t lds = expand_lds(F, K);
+  const int skey_cap = expand_skey_cap(F, K, plan.chunks);
+  const size_t lds = (size_t)F * K * 8 + (size_t)skey_cap * 8 + (size_t)F * 4;
   hipError_t e = hipFuncSetAttribute((const void *)expand_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  launch("expand_tree", expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
-                     tree, frontier, n_frontier, F, K, N, plan.chunks, plan.ms_per_row, part_ms,
-                     part_keys, row_lse, next_frontier, n_next, d_err);
+  launch("expand_tree", expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
+         frontier, n_frontier, F, K, N, plan.chunks, plan.ms_per_row, part_ms, part_keys,
+         row_lse, next_frontier, n_next, d_err, skey_cap);
   return hipGetLastError();
 }
 
@@ -413,18 +457,27 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t *d_err, hipStream_t stream) {
-  // worst case over any live node count up to cap
+  // layout sized by cap (the kernel uses it up to the live node count):
+  // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent [cap] | inC, done [cap]
   const int n = tree.cap;
-  size_t lds = (size_t)pow2_at_least(n + 1) * 8 + (size_t)(n + 1) * 4 +
-               (size_t)n * (4 + 4 + 4 + 1 + 1);
+  const size_t keys_b = (size_t)pow2_at_least(n + 1) * 8;
+  const size_t head_b = keys_b + (size_t)(n + 1) * 4 + (size_t)n * 4;  // up to logp
+  const size_t scratch_b = (size_t)n * (4 + 4 + 1 + 1);                // logp..done
+  size_t lds = head_b + scratch_b;
+  // per-wave top-M staging reuses logp..done when they are large enough
+  const size_t stage_b = (size_t)(kThreads / kWave) * plan.chunks * M * 8;
+  size_t stage_off = (head_b + 7) / 8 * 8;
+  if (plan.chunks > 1 && stage_off + stage_b > head_b + scratch_b) {
+    stage_off = (lds + 7) / 8 * 8;
+    lds = stage_off + stage_b;
+  }
   hipError_t e = hipFuncSetAttribute((const void *)rescore_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream,
-                     tree, strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms,
-                     part_keys, row_lse, graft_frontier, n_graft, next_frontier,
-                     n_next, N, d_err);
+  launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
+         strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms, part_keys,
+         row_lse, graft_frontier, n_graft, next_frontier, n_next, N, d_err, (int)stage_off);
   return hipGetLastError();
 }
 
