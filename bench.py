@@ -71,7 +71,8 @@ def parse():
                     help="profiling aid: run one device copy of this many MiB first, so a "
                          "counter pass can scale FETCH_SIZE/WRITE_SIZE by a known size")
     ap.add_argument("--workload", default="turn",
-                    choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b"],
+                    choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b",
+                             "expand-twodrafter", "rescore-twodrafter"],
                     help="turn (default) or tree-verify attention alone at one shape")
     return ap.parse_args()
 
@@ -324,6 +325,103 @@ def attention_bench(args, tg, torch, dev):
     print(json.dumps(out), flush=True)
 
 
+# --------------------------------------------------- tree calls alone
+
+def tree_bench(args, tg, torch, dev):
+    """Two-drafter shapes: expand of 64 frontier rows per tree (K=10, N=60)
+    or a middle step over 256-node trees (257 strong rows, W=60, m=10), B=8,
+    vocabulary 128256, logits N(0,3).  The trees are grown on the GPU from the
+    root (16 children, then 15 under each: 256 nodes in two levels) with the
+    library's own expansion; inputs rotate over copies beyond 512 MB."""
+    import workloads as W
+    Bt, Vv, K, Nn, Wd, Mm, F, R = 8, 128256, 10, 60, 60, 10, 64, 257
+    rescore = args.workload == "rescore-twodrafter"
+    rows = R if rescore else F
+    per_copy = Bt * rows * Vv * 4
+    copies = max(1, min(8, -(-(512 << 20) // per_copy)))
+    g = W.rng(3000)
+    logits = []
+    for c in range(copies):
+        t = torch.empty((Bt, rows, Vv), dtype=torch.float32, device=dev)
+        for b in range(Bt):
+            t[b] = torch.from_numpy(W.normal(g, (rows, Vv), 3.0)).to(dev)
+        logits.append(t)
+    grow = torch.from_numpy(W.normal(g, (Bt, 16, Vv), 3.0)).to(dev)
+
+    def base_tree():
+        ts = tg.TreeState(Bt, 1024, dev)
+        fr = torch.full((Bt, 16), -1, dtype=torch.int32, device=dev)
+        one = torch.ones(Bt, dtype=torch.int32, device=dev)
+        _, nx, nn = tg.expand_topk(ts, grow[:, :1].contiguous(), fr[:, :1].contiguous(), one,
+                                   16, 16)
+        tg.expand_topk(ts, grow, nx, nn, 15, 16)
+        return ts
+
+    template = base_tree()
+    torch.cuda.synchronize()
+    assert int(template.n_nodes[0].item()) == 256
+    # per-iteration fresh copies of the tree (the calls append to it)
+    trees = [tg.TreeState(Bt, 1024, dev) for _ in range(args.steps + args.warmup)]
+    for ts in trees:
+        for f in tg.TreeState.FIELDS:
+            getattr(ts, f).copy_(getattr(template, f))
+    fr = torch.arange(192, 256, dtype=torch.int32, device=dev).repeat(Bt, 1).contiguous()
+    if rescore:
+        ws = torch.zeros(tg.rescore_graft_workspace(Bt, R, Vv, Wd, Mm, 1024), dtype=torch.uint8,
+                         device=dev)
+        lse = torch.empty((Bt, R), dtype=torch.float32, device=dev)
+        gf = torch.empty((Bt, Wd), dtype=torch.int32, device=dev)
+        ng = torch.empty((Bt,), dtype=torch.int32, device=dev)
+        call = lambda i: tg.rescore_graft(trees[i], logits[i % copies], Wd, Mm, row_lse=lse,
+                                          graft_frontier=gf, n_graft=ng, workspace=ws)
+        nbytes = Bt * R * Vv * 4
+        nodes = Bt * (256 + Wd * Mm)
+    else:
+        ws = torch.zeros(tg.expand_topk_workspace(Bt, F, Vv, K, Nn), dtype=torch.uint8,
+                         device=dev)
+        lse = torch.empty((Bt, F), dtype=torch.float32, device=dev)
+        nx = torch.empty((Bt, Nn), dtype=torch.int32, device=dev)
+        nn = torch.empty((Bt,), dtype=torch.int32, device=dev)
+        call = lambda i: tg.expand_topk(trees[i], logits[i % copies], fr, None, K, Nn,
+                                        row_lse=lse, next_frontier=nx, n_next=nn, workspace=ws)
+        nbytes = Bt * F * Vv * 4
+        nodes = Bt * F * K
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    tg.trace_begin(8 * (args.steps + 1))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.warmup, args.warmup + args.steps):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    recs = tg.trace_end()
+    ms = e0.elapsed_time(e1) / args.steps
+    kern = {}
+    for name, t in recs:
+        d = kern.setdefault(name, [0, 0.0])
+        d[0] += 1
+        d[1] += t
+    row_us = 1e3 * kern["row_partial"][1] / kern["row_partial"][0]
+    ach = nbytes / (row_us * 1e-6)
+    out = {
+        "metric": METRIC, "value": nodes / (ms * 1e-3), "unit": "nodes/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": Bt, "vocab": Vv, "rows_per_tree": rows,
+                   "K_or_m": Mm if rescore else K, "input_copies": copies},
+        "roofline": {"bound": "hbm", "kernel": "row_partial", "achieved": ach / 1e9,
+                     "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": ach / PEAK_HBM,
+                     "traffic": None, "avg_launch_us": row_us},
+        "call_TB/s": nbytes / (ms * 1e-3) / 1e12,
+        "kernels": {k: {"launches_per_call": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0]}
+                    for k, v in kern.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -346,8 +444,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.workload != "turn":
+    if args.workload.startswith("attn-"):
         attention_bench(args, tg, torch, dev)
+        return
+    if args.workload.endswith("-twodrafter"):
+        tree_bench(args, tg, torch, dev)
         return
 
     trees = make_trees(dev)

@@ -1,12 +1,13 @@
 // Per-row log-sum-exp and top-K over a logits vocabulary, in chunks.
 //
 // Each workgroup streams one chunk of one fp32 logits row once from HBM
-// (float4 loads, 16 elements in flight per thread) and produces the chunk's
-// partial statistics: m = max, s = sum exp(x - m), and its top-K tokens by
-// (logit desc, token asc) as 64-bit keys.  The tree-phase kernels merge the
-// chunks of a row.  This is the "run the drafter, take Top_m of the
-// next-token logits" step of Alg. 1 / Alg. 2 and the normaliser of the edge
-// score p(u) (Sec. 3.1).
+// (a grain of 8192 values at a time, 32 per thread in one batch of float4
+// loads) and produces the chunk's partial statistics: m = max,
+// s = sum exp(x - m), and its top-K tokens by (logit desc, token asc) as
+// 64-bit keys.  The tree-phase kernels merge the chunks of a row.  Top-m
+// selection over a drafter's next-token distribution is the expansion step
+// of Alg. 1 / Alg. 2; the log-sum-exp normalises the edge score p(u)
+// (Sec. 3.1).
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -16,52 +17,109 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
-constexpr int kUnroll = 8;  // float4 loads in flight per thread (one grain)
+constexpr int kPer = kGrain / kThreads;  // elements per thread per grain (32)
+constexpr int kCandCap = 256;            // candidates per grain on the fast path
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <int KC>
-struct TopList {
-  uint64_t a[KC];  // descending; 0 = empty
-
-  __device__ __forceinline__ void clear() {
-#pragma unroll
-    for (int j = 0; j < KC; ++j) a[j] = 0;
-  }
-  __device__ __forceinline__ void insert(uint64_t k) {
-    if (k <= a[KC - 1]) return;
-    a[KC - 1] = k;
-#pragma unroll
-    for (int j = KC - 1; j > 0; --j) {
-      uint64_t hi = a[j - 1], lo = a[j];
-      bool sw = lo > hi;
-      a[j - 1] = sw ? lo : hi;
-      a[j] = sw ? hi : lo;
-    }
-  }
-  __device__ __forceinline__ uint64_t kth(int k) const {  // a[k-1], k in [1, KC]
-    uint64_t r = 0;
-#pragma unroll
-    for (int j = 0; j < KC; ++j) r = (j == k - 1) ? a[j] : r;
-    return r;
-  }
-  __device__ __forceinline__ void pop() {
-#pragma unroll
-    for (int j = 0; j < KC - 1; ++j) a[j] = a[j + 1];
-    a[KC - 1] = 0;
-  }
-};
-
+// Logit of a running-list key; -inf for an empty slot.
 __device__ __forceinline__ float key_threshold(uint64_t k) {
   uint32_t hi = (uint32_t)(k >> 32);
   return hi == 0 ? -__builtin_inff() : order_float(hi);
 }
 
-template <int KC>
+// Token of a thread's j-th element in the grain starting at e0.  16-byte rows
+// use float4 columns (four consecutive tokens per thread, 1024 tokens per
+// load step); other rows use one token per thread per step.
+__device__ __forceinline__ int elem_token(bool vec, int e0, int tid, int j) {
+  return vec ? e0 + (j >> 2) * (4 * kThreads) + 4 * tid + (j & 3) : e0 + j * kThreads + tid;
+}
+
+__device__ __forceinline__ float lane_max(const float (&x)[kPer]) {
+  float a = fmaxf(x[0], x[1]), b = fmaxf(x[2], x[3]);
+#pragma unroll
+  for (int j = 4; j < kPer; j += 4) {
+    a = fmaxf(a, fmaxf(x[j], x[j + 1]));
+    b = fmaxf(b, fmaxf(x[j + 2], x[j + 3]));
+  }
+  return fmaxf(a, b);
+}
+
+// sum_j exp(x_j - m) in the exp2 domain, four interleaved partial sums.
+// A NaN element, or +inf (then m = +inf), makes the result NaN.
+__device__ __forceinline__ float lane_sumexp(const float (&x)[kPer], float m) {
+  const float ml = m == -__builtin_inff() ? 0.0f : m * kLog2e;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) s[j & 3] += __builtin_amdgcn_exp2f(fmaf(x[j], kLog2e, -ml));
+  return (s[0] + s[1]) + (s[2] + s[3]);
+}
+
+// Descending bitonic sort of one value per lane across the wave.
+__device__ __forceinline__ float wave_sort_desc(float v, int lane) {
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const float p = __shfl_xor(v, j, kWave);
+      const bool take_max = ((lane & j) == 0) == ((lane & k) == 0);
+      v = take_max ? fmaxf(v, p) : fminf(v, p);
+    }
+  }
+  return v;
+}
+
+// Entries of a descending list that are >= v (or_equal) / > v.
+__device__ __forceinline__ int count_desc(const float *a, int n, float v, bool or_equal) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (or_equal ? a[mid] >= v : a[mid] > v)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+// Workgroup-wide sum of one int per thread (one barrier; slots alternate).
+__device__ __forceinline__ int block_sum(int c, int *slots, int &par) {
+  c = wave_sum_i32(c);
+  if ((threadIdx.x & (kWave - 1)) == 0) slots[par * kWavesPerBlock + threadIdx.x / kWave] = c;
+  __syncthreads();
+  int t = 0;
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) t += slots[par * kWavesPerBlock + i];
+  par ^= 1;
+  return t;
+}
+
+// One workgroup per chunk of a row; see the file comment.  Per grain:
+//  1. the grain sits in registers (32 elements per thread, one batch of
+//     loads); per thread max, then sum of exp (a NaN result flags NaN/+inf
+//     input, and only then are the values cleaned);
+//  2. one (max, sum-exp) partial per grain, waves by a fixed shuffle tree,
+//     then the four waves in order: the same bits whatever the chunking;
+//  3. a lower bound T on the grain's K-th largest logit: the K-th largest of
+//     the 256 thread maxima (K threads each hold an element >= it), raised to
+//     the running chunk list's K-th entry;
+//  4. elements >= T are compacted into LDS (about K of them for continuous
+//     logits); with more than kCandCap (heavy ties) the grain's exact K-th
+//     key is found by bisection over the key bits instead;
+//  5. the running list and the candidates are ranked by (logit desc, token
+//     asc) and the best K kept.
 __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     const float *__restrict__ logits, int rows_per_batch, int V, int K,
     int chunks, int grains_per_chunk, const int32_t *__restrict__ n_live,
     const uint8_t *__restrict__ needed, float2 *__restrict__ part_ms,
     uint64_t *__restrict__ part_keys, uint32_t *d_err) {
+  __shared__ uint64_t cand[TG_MAX_TOPK + kCandCap];  // [0, K): running list
+  __shared__ uint64_t run[TG_MAX_TOPK];
+  __shared__ float lmax[kWavesPerBlock][TG_MAX_TOPK];
+  __shared__ float gm[kWavesPerBlock], gs[kWavesPerBlock];
+  __shared__ float thr_s;
+  __shared__ int cnt_s, cntf_s;
+  __shared__ int red[2 * kWavesPerBlock];
+
   const int slot = blockIdx.x / chunks;
   const int c = blockIdx.x - slot * chunks;
   const int b = slot / rows_per_batch;
@@ -79,163 +137,175 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
   const int g_end = min(n_grains, g_beg + grains_per_chunk);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), w = tid / kWave;
-  // Rows are 16-byte aligned iff V % 4 == 0 (the base is); the choice depends
-  // on V only, so a row's partials never depend on where it sits.
+  // Rows are 16-byte aligned iff V % 4 == 0 (the base is); the layout
+  // depends on V only, so a row's partials never depend on where it sits.
   const bool vec = (V & 3) == 0;
+  const float ninf = -__builtin_inff();
 
-  float m = -__builtin_inff();
-  float s = 0.0f;
+  if (tid < K) run[tid] = 0;
   bool bad = false;
-  TopList<KC> top;
-  top.clear();
-  uint64_t thr_key = 0;  // keys <= thr_key can never reach the row's top-K
-  float thr = -__builtin_inff();
+  int rpar = 0;
 
-  auto consume1 = [&](float x, int idx) {
-    x = clean_logit(x, bad);
-    if (x > m) {
-      s *= __builtin_amdgcn_exp2f((m - x) * kLog2e);
-      m = x;
-    }
-    if (m != -__builtin_inff()) s += __builtin_amdgcn_exp2f(fmaf(x, kLog2e, -m * kLog2e));
-    if (x >= thr) {
-      uint64_t k = token_key(x, idx);
-      if (k > thr_key) top.insert(k);
-    }
-  };
-  auto consume4 = [&](float x0, float x1, float x2, float x3, int idx) {
-    x0 = clean_logit(x0, bad);
-    x1 = clean_logit(x1, bad);
-    x2 = clean_logit(x2, bad);
-    x3 = clean_logit(x3, bad);
-    float bm = fmaxf(fmaxf(x0, x1), fmaxf(x2, x3));
-    if (bm > m) {
-      s *= __builtin_amdgcn_exp2f((m - bm) * kLog2e);
-      m = bm;
-    }
-    if (m != -__builtin_inff()) {
-      float ml = m * kLog2e;
-      s += __builtin_amdgcn_exp2f(fmaf(x0, kLog2e, -ml)) +
-           __builtin_amdgcn_exp2f(fmaf(x1, kLog2e, -ml)) +
-           __builtin_amdgcn_exp2f(fmaf(x2, kLog2e, -ml)) +
-           __builtin_amdgcn_exp2f(fmaf(x3, kLog2e, -ml));
-    }
-    if (x0 >= thr) {
-      uint64_t k = token_key(x0, idx);
-      if (k > thr_key) top.insert(k);
-    }
-    if (x1 >= thr) {
-      uint64_t k = token_key(x1, idx + 1);
-      if (k > thr_key) top.insert(k);
-    }
-    if (x2 >= thr) {
-      uint64_t k = token_key(x2, idx + 2);
-      if (k > thr_key) top.insert(k);
-    }
-    if (x3 >= thr) {
-      uint64_t k = token_key(x3, idx + 3);
-      if (k > thr_key) top.insert(k);
-    }
-  };
-  auto refresh = [&]() {
-    uint64_t wk = wave_max_u64(top.kth(K));
-    uint64_t t = top.a[KC - 1];
-    thr_key = wk > t ? wk : t;
-    thr = key_threshold(thr_key);
-  };
-
-  // Each grain of kGrain elements yields one (max, sum-exp) partial over a
-  // fixed set of elements in a fixed reduction order, so the merged
-  // log-sum-exp of a row is the same bits whatever the chunking.  Trip counts are uniform per workgroup
-  // (the threshold refresh shuffles across lanes).
   for (int gr = g_beg; gr < g_end; ++gr) {
-    m = -__builtin_inff();
-    s = 0.0f;
     const int e0 = gr * kGrain;
     const int e1 = min(V, e0 + kGrain);
+    const bool full = e1 - e0 == kGrain;
+    float x[kPer];
     if (vec) {
-      for (int base0 = e0; base0 < e1; base0 += 4 * kThreads * kUnroll) {
-        const int base = base0 + 4 * tid;
-        f32x4 v[kUnroll];
+      // e1 is a multiple of 4 here, so a float4 is wholly in or out
+      const f32x4 *p = reinterpret_cast<const f32x4 *>(row + e0) + tid;
+      if (full) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          int idx = base + u * 4 * kThreads;
-          if (idx < e1)
-            v[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(row + idx));
-          else
-            v[u] = f32x4{-__builtin_inff(), -__builtin_inff(), -__builtin_inff(),
-                         -__builtin_inff()};
+        for (int u = 0; u < kPer / 4; ++u) {
+          f32x4 v = __builtin_nontemporal_load(p + u * kThreads);
+          x[4 * u] = v.x, x[4 * u + 1] = v.y, x[4 * u + 2] = v.z, x[4 * u + 3] = v.w;
         }
+      } else {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          int idx = base + u * 4 * kThreads;
-          if (idx < e1) consume4(v[u].x, v[u].y, v[u].z, v[u].w, idx);
+        for (int u = 0; u < kPer / 4; ++u) {
+          f32x4 v = {ninf, ninf, ninf, ninf};
+          if (elem_token(true, e0, tid, 4 * u) < e1) v = __builtin_nontemporal_load(p + u * kThreads);
+          x[4 * u] = v.x, x[4 * u + 1] = v.y, x[4 * u + 2] = v.z, x[4 * u + 3] = v.w;
         }
-        refresh();
       }
     } else {
-      for (int base0 = e0; base0 < e1; base0 += kThreads * 16) {
-        float xs[16];
+      if (full) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          int i = base0 + tid + j * kThreads;
-          xs[j] = i < e1 ? row[i] : -__builtin_inff();
-        }
+        for (int j = 0; j < kPer; ++j) x[j] = row[e0 + j * kThreads + tid];
+      } else {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          int i = base0 + tid + j * kThreads;
-          if (i < e1) consume1(xs[j], i);
+        for (int j = 0; j < kPer; ++j) {
+          const int i = e0 + j * kThreads + tid;
+          x[j] = i < e1 ? row[i] : ninf;
         }
-        refresh();
       }
     }
-    // one (max, sum-exp) partial per grain: waves by a fixed shuffle tree,
-    // then the four waves in order (LDS double-buffered by grain parity)
-    __shared__ float gm[2][kWavesPerBlock], gs[2][kWavesPerBlock];
+
+    // ---- 1. thread statistics
+    float m = lane_max(x);
+    float s = lane_sumexp(x, m);
+    if (__any(!(s == s) || m == __builtin_inff())) {
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) x[j] = clean_logit(x[j], bad);
+      m = lane_max(x);
+      s = lane_sumexp(x, m);
+    }
+
+    // ---- 2. wave partials; 3. wave-sorted thread maxima
     const float mw = wave_max_f32(m);
-    const float sc = (m == -__builtin_inff()) ? 0.0f
-                                              : s * __builtin_amdgcn_exp2f((m - mw) * kLog2e);
+    const float sc = (m == ninf) ? 0.0f : s * __builtin_amdgcn_exp2f((m - mw) * kLog2e);
     const float sw = wave_sum_f32(sc);
-    const int par = gr & 1;
+    const float ms = wave_sort_desc(m, lane);
+    if (lane < K) lmax[w][lane] = ms;
     if (lane == 0) {
-      gm[par][w] = mw;
-      gs[par][w] = sw;
+      gm[w] = mw;
+      gs[w] = sw;
+    }
+    if (tid < K) cand[tid] = run[tid];
+    if (tid == 0) {
+      cnt_s = 0;
+      cntf_s = 0;
     }
     __syncthreads();
+    if (tid < K) run[tid] = 0;
     if (tid == 0) {
-      float M = gm[par][0], S = gs[par][0];
-      for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[par][i], gs[par][i]);
+      float M = gm[0], S = gs[0];
+      for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[i], gs[i]);
       part_ms[(size_t)slot * n_grains + gr] = make_float2(M, S);
     }
+    if (tid < kWavesPerBlock * K) {
+      // rank of this entry in the four lists merged (value desc, list asc)
+      const int wl = tid / K, i = tid - wl * K;
+      const float v = lmax[wl][i];
+      int rank = i;
+#pragma unroll
+      for (int o = 0; o < kWavesPerBlock; ++o)
+        if (o != wl) rank += count_desc(lmax[o], K, v, o < wl);
+      if (rank == K - 1) thr_s = v;
+    }
+    __syncthreads();
+
+    // ---- 4. candidates
+    const float T = fmaxf(thr_s, key_threshold(cand[K - 1]));
+    if (T > ninf) {
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        if (x[j] >= T) {
+          const int p = atomicAdd(&cnt_s, 1);
+          if (p < kCandCap) cand[K + p] = token_key(x[j], elem_token(vec, e0, tid, j));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const int t = elem_token(vec, e0, tid, j);
+        if (t < e1) {
+          const int p = atomicAdd(&cnt_s, 1);
+          if (p < kCandCap) cand[K + p] = token_key(x[j], t);
+        }
+      }
+    }
+    __syncthreads();
+    int n = cnt_s;
+    if (n > kCandCap) {
+      // Exact K-th key of the grain: the largest order image o with at least
+      // K elements >= o, then among the elements equal to o the smallest
+      // token bound that completes K.  (n > kCandCap >= K valid elements.)
+      uint32_t ord[kPer];
+#pragma unroll
+      for (int j = 0; j < kPer; ++j)
+        ord[j] = elem_token(vec, e0, tid, j) < e1 ? float_order(x[j]) : 0u;
+      uint32_t o = 0;
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cb = o | (1u << bit);
+        int q = 0;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) q += ord[j] >= cb;
+        if (block_sum(q, red, rpar) >= K) o = cb;
+      }
+      int q = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) q += ord[j] > o;
+      const int need = K - block_sum(q, red, rpar);
+      int lo = e0, hi = e1 - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        int qq = 0;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j)
+          qq += ord[j] == o && elem_token(vec, e0, tid, j) <= mid;
+        if (block_sum(qq, red, rpar) >= need)
+          hi = mid;
+        else
+          lo = mid + 1;
+      }
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const int t = elem_token(vec, e0, tid, j);
+        if (ord[j] > o || (ord[j] == o && t <= lo)) {
+          const int p = atomicAdd(&cntf_s, 1);
+          cand[K + p] = ((uint64_t)ord[j] << 32) | (uint64_t)(0xffffffffu - (uint32_t)t);
+        }
+      }
+      __syncthreads();
+      n = cntf_s;
+    }
+
+    // ---- 5. rank the running list (empty on a chunk's first grain) and
+    // the candidates; keys are distinct (distinct tokens)
+    const int r0 = gr == g_beg ? K : 0;
+    const int total = K + n;
+    for (int t = r0 + tid; t < total; t += kThreads) {
+      const uint64_t key = cand[t];
+      if (key == 0) continue;
+      int rank = 0;
+      for (int u = r0; u < total; ++u) rank += cand[u] > key;
+      if (rank < K) run[rank] = key;
+    }
+    __syncthreads();
   }
   if (bad) report(d_err, TG_DERR_NONFINITE);
-
-  // ---- wave top-K: K rounds of "largest head wins, winner pops"
-  __shared__ uint64_t cand[kWavesPerBlock * TG_MAX_TOPK];
-  for (int j = 0; j < K; ++j) {
-    uint64_t head = top.a[0];
-    uint64_t best = wave_max_u64(head);
-    if (head == best && best != 0) top.pop();
-    if (lane == 0) cand[w * K + j] = best;
-  }
-  __syncthreads();
-  const size_t part = (size_t)slot * chunks + c;
-  // ---- workgroup top-K by rank counting over the waves' candidates
-  const int nc = kWavesPerBlock * K;
-  for (int t = tid; t < nc; t += kThreads) {
-    uint64_t key = cand[t];
-    if (key == 0) continue;
-    int rank = 0;
-    for (int u = 0; u < nc; ++u) rank += cand[u] > key;
-    if (rank < K) part_keys[part * K + rank] = key;
-  }
-  // slots past the number of real keys (chunks shorter than K) stay empty
-  for (int t = tid; t < K; t += kThreads) {
-    int real = 0;
-    for (int u = 0; u < nc; ++u) real += cand[u] != 0;
-    if (t >= real) part_keys[part * K + t] = 0;
-  }
-
+  if (tid < K) part_keys[((size_t)slot * chunks + c) * K + tid] = run[tid];
 }
 
 }  // namespace
@@ -262,21 +332,8 @@ hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   dim3 g((unsigned)grid), blk(kThreads);
-#define TG_ROWS(KC)                                                          \
-  launch("row_partial", (row_partial_kernel<KC>), g, blk, 0, stream, logits,     \
-                     rows_per_batch, V, K, plan.chunks, plan.grains_per_chunk,      \
-                     n_live, needed, part_ms, part_keys, d_err)
-  if (K <= 4)
-    TG_ROWS(4);
-  else if (K <= 8)
-    TG_ROWS(8);
-  else if (K <= 16)
-    TG_ROWS(16);
-  else if (K <= 32)
-    TG_ROWS(32);
-  else
-    TG_ROWS(64);
-#undef TG_ROWS
+launch("row_partial", row_partial_kernel, g, blk, 0, stream, logits, rows_per_batch, V, K,
+         plan.chunks, plan.grains_per_chunk, n_live, needed, part_ms, part_keys, d_err);
   return hipGetLastError();
 }
 

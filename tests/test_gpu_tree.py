@@ -167,6 +167,33 @@ def test_expand_ties_and_special_values(tg):
     run_expand(tg, base, logits, fr, None, K, N)
 
 
+ROW_CASES = [
+    # F, V, K, note
+    (3, 20000, 10, "heavy ties, several grains"),
+    (3, 20001, 64, "heavy ties, scalar rows, K = 64"),
+    (2, 600000, 16, "two grains per chunk"),
+]
+
+
+@pytest.mark.parametrize("case", ROW_CASES, ids=[c[-1] for c in ROW_CASES])
+def test_expand_row_selection_ties(tg, case):
+    """Rows where hundreds or thousands of logits tie at the top of a grain
+    (a constant row, a row clipped at 1.0) or where fewer than K are finite
+    (the rest -inf), next to a continuous row: the per-grain selection must
+    still return the K best by (logit desc, token asc)."""
+    F, V, K, _ = case
+    g = W.rng(V + K)
+    base, _ = C.scored_tree(5, 1, 30, steps=1, width=3, K=3)
+    fr = np.array([[-1, 0, 1][:F]], np.int32)
+    logits = W.normal(g, (1, F, V), 3.0)
+    logits[0, 1] = 0.0
+    if F > 2:
+        logits[0, 2] = np.minimum(np.round(logits[0, 2] / 3.0), 1.0)
+        logits[0, 2, : V // 2] = -np.inf
+        logits[0, 2, g.choice(V // 2, 5, replace=False)] = 2.0
+    run_expand(tg, base, logits, fr, None, K, 3 * K)
+
+
 def test_expand_nonfinite_capacity_and_bad_node(tg):
     g = W.rng(4)
     base, _ = C.scored_tree(5, 3, 30, steps=1, width=3, K=3, cap=20)
