@@ -45,18 +45,30 @@ __device__ __forceinline__ bool bad_prefix(int L, int N, int S_max) {
 // ------------------------------------------------------------ bf16 / MFMA
 // LDS tiles: K and V rows of D bf16, unpadded, written straight from global
 // memory by global_load_lds (lane l of an instruction lands at base + 16 l).
-// 16-byte chunks are XOR-swizzled with the row (chunk' = chunk ^ (row & CM)) so
-// that the lanes of one K-fragment read (one key per lane) and of one
-// transposed V read (4 keys x 16 d per lane group) hit distinct banks.
+// 16-byte chunks are XOR-swizzled with a function of the row,
+// chunk' = chunk ^ swz(row), chosen for 64 banks of 4 bytes so that both
+// read patterns are conflict-free:
+//   K fragment (ds_read_b128, 16 lanes per pass): 16 consecutive rows, one
+//     logical chunk -> swz must be a bijection on any 16 aligned rows
+//     (D = 128: 16 rows per bank cycle; D = 64: two rows share a cycle, so on
+//     each parity class);
+//   transposed V (ds_read_b64_tr_b16, 32 lanes per pass): 4 consecutive rows
+//     x 4 consecutive chunks -> the 4 rows must move the chunk's upper bits.
 template <int D> struct AttnLds {
   static constexpr int CPR = D / 8;           // 16-byte chunks per row
   static constexpr int CM = CPR - 1;          // swizzle mask
   static constexpr int TILE = BN * D;         // bf16 elements per K (or V) tile
   static constexpr int STAGE = 2 * TILE;      // K then V
   static constexpr size_t bytes(int anc_words) { return (size_t)anc_words * 4; }
+  static __device__ __forceinline__ int swz(int row) {
+    if constexpr (D == 128)
+      return ((row & 3) << 2) | ((row >> 2) & 3);
+    else
+      return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+  }
   // element offset of (row, d) inside a tile
   static __device__ __forceinline__ int at(int row, int d) {
-    return row * D + ((((d >> 3) ^ row) & CM) << 3) + (d & 7);
+    return row * D + ((((d >> 3) ^ swz(row)) & CM) << 3) + (d & 7);
   }
 };
 
@@ -180,14 +192,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   // Direct global -> LDS loads.  Instruction i of wave w fills the 1 KB
   // block j = w * LOADS + i of a tile: rows j * RPI .. + RPI - 1, and lane l
   // writes physical chunk l % CPR of its row, i.e. loads logical chunk
-  // (l % CPR) ^ (row & CM).  Offsets are per-thread constants.
+  // (l % CPR) ^ swz(row).  Offsets are per-thread constants.
   constexpr int RPI = 64 / Lds::CPR;  // rows per 1 KB instruction
   int goff[LOADS];
   int grow[LOADS];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
     const int row = (w * LOADS + i) * RPI + lane / Lds::CPR;
-    const int chunk = ((lane % Lds::CPR) ^ row) & Lds::CM;
+    const int chunk = ((lane % Lds::CPR) ^ Lds::swz(row)) & Lds::CM;
     grow[i] = row;
     goff[i] = row * D + chunk * 8;
   }
@@ -585,24 +597,18 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   // bitset words of the nodes one 128-row tile can hold
   const int nodes_per_tile = std::min(s.N, (BM + G - 1) / G + 1);
   const int anc_words = nodes_per_tile * ((s.N + 31) / 32);
-  hipError_t e;
-  if (s.D == 64) {
-    const size_t lds = AttnLds<64>::bytes(anc_words);
-    e = hipFuncSetAttribute((const void *)attn_mfma_kernel<64>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    launch("attn_mfma", attn_mfma_kernel<64>, dim3((unsigned)grid), dim3(kThreads), lds,
-           stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq,
-           s.Hkv, s.S_max, scale2, tiles, sp, d_err);
-  } else {
-    const size_t lds = AttnLds<128>::bytes(anc_words);
-    e = hipFuncSetAttribute((const void *)attn_mfma_kernel<128>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    launch("attn_mfma", attn_mfma_kernel<128>, dim3((unsigned)grid), dim3(kThreads), lds,
-           stream, qb, kb, vb, parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq,
-           s.Hkv, s.S_max, scale2, tiles, sp, d_err);
-  }
+  auto go = [&](auto kernel, size_t lds) {
+    hipError_t r = hipFuncSetAttribute((const void *)kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (r != hipSuccess) return r;
+    launch("attn_mfma", kernel, dim3((unsigned)grid), dim3(kThreads), lds, stream, qb, kb, vb,
+           parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2,
+           tiles, sp, d_err);
+    return hipSuccess;
+  };
+  hipError_t e = s.D == 64 ? go(attn_mfma_kernel<64>, AttnLds<64>::bytes(anc_words))
+                           : go(attn_mfma_kernel<128>, AttnLds<128>::bytes(anc_words));
+  if (e != hipSuccess) return e;
   e = hipGetLastError();
   if (e != hipSuccess || sp <= 1) return e;
   const unsigned cgrid = (unsigned)((rows + 3) / 4);
