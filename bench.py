@@ -48,6 +48,7 @@ if ROOT not in sys.path:
 METRIC = "tree-verify attention TB/s & TFLOP/s (% roofline); draft-tree nodes/sec"
 PEAK_HBM = 8.0e12        # B/s, MI355X HBM3E
 PEAK_BF16 = 2.5e15       # flop/s, dense bf16 MFMA
+ATTN_MAIN = ("attn_pingpong", "attn_mfma", "attn_f32")   # tree-verify attention kernels
 
 # workload (Llama-3-8B-shaped turn)
 V, W_FR, M_CH = 128256, 10, 8
@@ -296,7 +297,8 @@ def attention_bench(args, tg, torch, dev):
         d = kern.setdefault(name, [0, 0.0])
         d[0] += 1
         d[1] += t
-    main_us = 1e3 * kern["attn_mfma"][1] / kern["attn_mfma"][0]
+    main_k = next(k for k in ATTN_MAIN if k in kern)
+    main_us = 1e3 * kern[main_k][1] / kern[main_k][0]
     keys = sum(Nn * Lp + path_len_sum(par[b]) for b in range(Bq))
     flops = 4 * Dh * Hq * keys
     nbytes = 2 * Bq * Hkv * S * Dh * 2 + 2 * Bq * Nn * Hq * Dh * 2 + par.nbytes
@@ -314,7 +316,7 @@ def attention_bench(args, tg, torch, dev):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "batch": Bq, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": Dh, "prefix": Lp, "tree_nodes": Nn, "input_copies": copies},
-        "roofline": {"bound": bound, "kernel": "attn_mfma", "achieved": ach, "peak": peak,
+        "roofline": {"bound": bound, "kernel": main_k, "achieved": ach, "peak": peak,
                      "unit": unit, "frac": ach / peak, "traffic": None,
                      "avg_launch_us": main_us},
         "TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
@@ -553,7 +555,7 @@ def main():
         t_us = kernels[dom]["us_per_step"]
         roof = {"bound": "hbm", "kernel": dom, "achieved": None, "peak": PEAK_HBM / 1e9,
                 "unit": "GB/s", "frac": None, "traffic": None, "avg_launch_us": t_us}
-    attn_us = sum(kernels[k]["us_per_step"] for k in ("attn_mfma", "attn_combine") if k in kernels)
+    attn_us = sum(kernels[k]["us_per_step"] for k in ATTN_MAIN + ("attn_combine",) if k in kernels)
     verify = {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
               "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
               "frac_hbm": v_bytes / (attn_us * 1e-6) / PEAK_HBM,

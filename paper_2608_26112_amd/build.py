@@ -26,6 +26,9 @@ HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]
+# Per-source extras.  attn.hip: its inputs are finite and masking uses -inf,
+# so maxima need no NaN canonicalisation of MFMA results.
+EXTRA = {"attn.hip": ["-fno-honor-nans"]}
 
 
 def _run(cmd):
@@ -46,7 +49,8 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src):
         obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-        log = _run([HIPCC, *COMMON, *DEVICE_FLAGS, "-c", src, "-o", obj])
+        extra = EXTRA.get(os.path.basename(src), [])
+        log = _run([HIPCC, *COMMON, *DEVICE_FLAGS, *extra, "-c", src, "-o", obj])
         return obj, log
 
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:

@@ -72,6 +72,15 @@ template <int D> struct AttnLds {
   }
 };
 
+// max / sum with the lane 32 apart (the other half of a query row's keys),
+// by v_permlane32_swap: no LDS round trip
+__device__ __forceinline__ float half_swap(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  // lanes < 32: r[0] = own, r[1] = lane + 32; lanes >= 32: r[0] = lane - 32, r[1] = own
+  return __uint_as_float(threadIdx.x & 32 ? r[0] : r[1]);
+}
+
 __device__ __forceinline__ bf16x4 lds_read_tr4(const __bf16 *p) {
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -273,13 +282,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
         tw0 = my_anc[wj];
         tw1 = wj + 1 < NW ? my_anc[wj + 1] : 0u;
       }
+      // key kk = blk*32 + 8(r/4) + 4h + r%4: shifts by 4h once, then by constants
+      const int lim_h = k_lim - k0 - 4 * h;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
-        const uint32_t tw = blk ? tw1 : tw0;
+        const uint32_t tw = (blk ? tw1 : tw0) >> (4 * h);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int kk = blk * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-          const bool valid = (k0 + kk) < k_lim && ((tw >> (kk & 31)) & 1u);
+          const int kc = blk * 32 + 8 * (r >> 2) + (r & 3);
+          const bool valid = kc < lim_h && ((tw >> (kc & 31)) & 1u);
           acc[blk][r] = valid ? acc[blk][r] : -__builtin_inff();
         }
       }
@@ -369,6 +380,400 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
 
   // ---- finalize
   const float lt = l + __shfl_xor(l, 32, 64);
+  if (!qvalid) return;
+  const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+  if (n_splits == 1) {
+    __bf16 *op = out + (((size_t)b * N + qnode) * Hq + qhead) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int d = db * 32 + 8 * j + 4 * h;
+        bf16x4 v4 = bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
+                           (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
+        *reinterpret_cast<bf16x4 *>(op + d) = v4;
+      }
+    }
+  } else {
+    const size_t prow = (((size_t)split * B + b) * N + qnode) * Hq + qhead;
+    float *op = part_o + prow * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int d = db * 32 + 8 * j + 4 * h;
+        *reinterpret_cast<f32x4 *>(op + d) =
+            f32x4{o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
+                  o[db][4 * j + 3] * inv};
+      }
+    }
+    if (h == 0) part_lse[prow] = lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
+  }
+}
+
+// --------------------------------------------- bf16, ping-pong schedule
+// For long prefixes: 8 waves (two per SIMD) share each K/V tile; a
+// workgroup owns 256 query rows (32 per wave, the same MFMA layout as
+// attn_mfma_kernel).  Each wave alternates an MFMA phase M(t) = {PV of tile
+// t-1, QK^T of tile t} and a vector phase S(t) = {mask, row max, rescale,
+// exponentials of tile t}.  Waves 4-7 run one phase behind waves 0-3, so on
+// every SIMD one wave feeds the matrix core while the other runs its
+// softmax; a workgroup barrier ends every phase.
+//   phase 2j  : loads of K(j+1) and V(j) are issued; group A runs M(j),
+//               group B runs S(j-1)
+//   phase 2j+1: group A runs S(j), group B runs M(j); the loads have landed
+//               by the barrier that ends the phase
+// K(j) is read in phases 2j and 2j+1, V(j) in 2j+2 and 2j+3, so two stages
+// of each suffice.
+template <int D>
+__global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
+    const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
+    const __bf16 *__restrict__ vc, const int32_t *__restrict__ parent,
+    const int32_t *__restrict__ prefix_len, __bf16 *__restrict__ out,
+    float *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
+    int Hq, int Hkv, int S_max, float scale2, int n_tiles, int n_splits,
+    uint32_t *d_err) {
+  using Lds = AttnLds<D>;
+  constexpr int NT = 512;
+  constexpr int BMP = 256;
+  constexpr int KS = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int LOADS = BN * D * 2 / 16 / NT;  // 16-byte loads per thread per tile
+  // two stages each of K and V (distinct objects, so the compiler knows a
+  // read of one stage does not alias loads in flight into another)
+  __shared__ __attribute__((aligned(16))) __bf16 kst0[Lds::TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 kst1[Lds::TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 vst0[Lds::TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 vst1[Lds::TILE];
+  extern __shared__ __attribute__((aligned(16))) uint32_t anc_s[];
+  int *par_s = reinterpret_cast<int *>(kst0);  // prologue only (N ints fit a tile)
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int h = lane >> 5, r32 = lane & 31;
+  const int G = Hq / Hkv;
+  // Group A / B by SIMD: the first wave (in wave order) placed on each SIMD
+  // leads.  HW_ID bits [5:4] hold the wave's SIMD (s_getreg, size 2, offset 4).
+  // Only the overlap depends on this; every wave runs the same barriers.
+  __shared__ int simd_s[NT / 64];
+  const int my_simd = __builtin_amdgcn_s_getreg((1 << 11) | (4 << 6) | 4);
+  if (lane == 0) simd_s[w] = my_simd;
+
+  const int total = gridDim.x;
+  int li = blockIdx.x;
+  if ((total & 7) == 0) li = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  const int tile = li % n_tiles;
+  int rest = li / n_tiles;
+  const int split = rest % n_splits;
+  rest /= n_splits;
+  const int g = rest % Hkv;
+  const int b = rest / Hkv;
+
+  const int L = prefix_len[b];
+  const int rows_total = N * G;
+  const int row0 = tile * BMP;
+  if (bad_prefix(L, N, S_max)) {
+    if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
+    if (n_splits == 1) {
+      for (int rr = w; rr < BMP; rr += NT / 64) {
+        int row = row0 + rr;
+        if (row >= rows_total) break;
+        int node = row / G, hq = g * G + row % G;
+        __bf16 *o = out + (((size_t)b * N + node) * Hq + hq) * D;
+        for (int d = lane; d < D; d += 64) o[d] = (__bf16)0.0f;
+      }
+    }
+    return;
+  }
+
+  // ---- ancestor-or-self bitsets of this tile's nodes (a1)
+  const int node_lo = row0 / G;
+  const int node_hi = min(N, (row0 + BMP - 1) / G + 1);
+  const int nloc = node_hi - node_lo;
+  const int NW = (N + 31) >> 5;
+  bool badp = false;
+  for (int i = tid; i < N; i += NT) {
+    int p = parent[(size_t)b * N + i];
+    if (p < -1 || p >= i) {
+      badp = true;
+      p = -1;
+    }
+    par_s[i] = p;
+  }
+  if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
+  for (int i = tid; i < nloc * NW; i += NT) anc_s[i] = 0;
+  __syncthreads();
+  for (int i = tid; i < nloc; i += NT) {
+    uint32_t *row = anc_s + i * NW;
+    for (int u = node_lo + i; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
+  }
+  bool lead = true;
+  for (int i = 0; i < w; ++i) lead = lead && simd_s[i] != my_simd;
+  __syncthreads();
+
+  // ---- this lane's query row, Q fragment in registers
+  const int qrow = row0 + w * 32 + r32;
+  const bool qvalid = qrow < rows_total;
+  const int qnode = qvalid ? qrow / G : node_lo;
+  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
+  // Q pre-scaled by sm_scale * log2(e) (one bf16 rounding), so that scores
+  // come out of the MFMA in log2 units
+  bf16x8 qf[KS];
+  {
+    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8 raw = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)((float)raw[e] * scale2);
+    }
+  }
+
+  int chunk = (L + n_splits - 1) / n_splits;
+  chunk = ((chunk + BN - 1) / BN) * BN;
+  const int p_beg = min(L, split * chunk);
+  const int p_end = min(L, p_beg + chunk);
+  const bool do_tree = split == n_splits - 1;
+  const int n_ptiles = (p_end - p_beg + BN - 1) / BN;
+  const int n = n_ptiles + (do_tree ? (N + BN - 1) / BN : 0);
+
+  const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
+  const __bf16 *kb = kc + kv_base;
+  const __bf16 *vb = vc + kv_base;
+
+  // Running row reference m (log2 units): the max of the row's first tile
+  // with a visible key, then moved up only when a tile's scores exceed it by
+  // more than kSlack, so the exponentials stay below 2^kSlack and the O / l
+  // rescale is rare.
+  constexpr float kSlack = 8.0f;
+  f32x16 o[DB];
+#pragma unroll
+  for (int i = 0; i < DB; ++i) o[i] = f32x16{};
+  float m = 0.0f;
+  bool m_set = false;
+  float l = 0.0f;
+  f32x16 acc[2];
+  bf16x8 pb[2][2];
+
+  auto tile_k0 = [&](int t) { return t >= n_ptiles ? L + (t - n_ptiles) * BN : p_beg + t * BN; };
+  auto tile_lim = [&](int t) { return t >= n_ptiles ? L + N : p_end; };
+  constexpr int RPI = 64 / Lds::CPR;
+  // offsets recomputed per issue (a few VALU ops) rather than held in registers
+  auto issue = [&](const __bf16 *src, int t, __bf16 *dst) __attribute__((always_inline)) {
+    const int k0 = tile_k0(t), lim = tile_lim(t);
+    const __bf16 *st = src + (size_t)k0 * D;
+    int goff[LOADS], grow[LOADS];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int row = (w * LOADS + i) * RPI + lane / Lds::CPR;
+      grow[i] = row;
+      goff[i] = row * D + (((lane % Lds::CPR) ^ Lds::swz(row)) & Lds::CM) * 8;
+    }
+    auto one = [&](int i, int off) {
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void *)(st + off),
+          (__attribute__((address_space(3))) void *)(dst + (w * LOADS + i) * 512), 16, 0, 0);
+    };
+    if (k0 + BN <= lim) {
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) one(i, goff[i]);
+    } else {
+      // rows past the range re-read the last valid row (finite, masked later)
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) one(i, goff[i] - max(0, k0 + grow[i] - (lim - 1)) * D);
+    }
+  };
+
+  // Per-lane LDS element offsets of the fragment reads.  The swizzle only
+  // looks at the low four row bits, so the row offset of a 16- or 32-key
+  // block is a constant added to these.
+  const int grp = lane >> 4, gl = lane & 15;
+  const int vrow = 4 * (grp >> 1) + (gl >> 2);
+  const int vcol = 16 * (grp & 1) + 4 * (gl & 3);
+  int voff[DB][2];  // V^T fragment (transposed reads): [d block][key half]
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    voff[db][0] = Lds::at(vrow, db * 32 + vcol);
+    voff[db][1] = Lds::at(vrow + 8, db * 32 + vcol);
+  }
+  int koff[KS];  // K fragment: [k-step], key r32 (the second block is +32 rows)
+#pragma unroll
+  for (int s = 0; s < KS; ++s) koff[s] = Lds::at(r32, 16 * s + 8 * h);
+
+  // MFMA phase: PV of the previous tile (pb, V in Vp) then QK^T of this one
+  // (fragment reads one MFMA group ahead)
+  auto mphase = [&](bool do_pv, const __bf16 *Vp, bool do_qk, const __bf16 *Kt)
+                    __attribute__((always_inline)) {
+    // the MFMA wave issues first whenever the matrix core is free; the
+    // softmax wave on the same SIMD fills the remaining issue slots
+    __builtin_amdgcn_s_setprio(1);
+    if (do_pv) {
+      auto vfrag = [&](int blk, int u, int db) {
+        const __bf16 *vb0 = Vp + (blk * 32 + 16 * u) * D;
+        const bf16x4 lo = lds_read_tr4(vb0 + voff[db][0]);
+        const bf16x4 hi = lds_read_tr4(vb0 + voff[db][1]);
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          bf16x8 cur = vfrag(blk, u, 0);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            bf16x8 nxt = cur;
+            if (db + 1 < DB) nxt = vfrag(blk, u, db + 1);
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, pb[blk][u], o[db], 0, 0, 0);
+            cur = nxt;
+          }
+        }
+    }
+    if (do_qk) {
+      auto kfrag = [&](int kblk, int s) {
+        return *reinterpret_cast<const bf16x8 *>(Kt + kblk * 32 * D + koff[s]);
+      };
+      bf16x8 a0 = kfrag(0, 0), a1 = kfrag(1, 0);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        bf16x8 n0 = a0, n1 = a1;
+        if (s + 1 < KS) {
+          n0 = kfrag(0, s + 1);
+          n1 = kfrag(1, s + 1);
+        }
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], s == 0 ? f32x16{} : acc[0],
+                                                         0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], s == 0 ? f32x16{} : acc[1],
+                                                         0, 0, 0);
+        a0 = n0;
+        a1 = n1;
+      }
+    }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  // vector phase: softmax of tile t's scores (acc) into pb, m, l, o scale
+  auto sphase = [&](int t) __attribute__((always_inline)) {
+    const bool tree_tile = t >= n_ptiles;
+    const int k0 = tile_k0(t);
+    const int k_lim = tile_lim(t);
+    if (tree_tile || k0 + BN > k_lim) {
+      uint32_t tw0 = 0xffffffffu, tw1 = 0xffffffffu;
+      if (tree_tile) {
+        const int wj = (k0 - L) >> 5;
+        tw0 = my_anc[wj];
+        tw1 = wj + 1 < NW ? my_anc[wj + 1] : 0u;
+      }
+      // key kk = blk*32 + 8(r/4) + 4h + r%4: shifts by 4h once, then by constants
+      const int lim_h = k_lim - k0 - 4 * h;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        const uint32_t tw = (blk ? tw1 : tw0) >> (4 * h);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kc = blk * 32 + 8 * (r >> 2) + (r & 3);
+          const bool valid = kc < lim_h && ((tw >> (kc & 31)) & 1u);
+          acc[blk][r] = valid ? acc[blk][r] : -__builtin_inff();
+        }
+      }
+    }
+    float mx;
+    {
+      float t3[11];
+#pragma unroll
+      for (int i = 0; i < 10; ++i) {
+        const int a = 3 * i, bb = a + 1, c = a + 2;
+        t3[i] = __builtin_fmaxf(acc[a >> 4][a & 15],
+                                __builtin_fmaxf(acc[bb >> 4][bb & 15], acc[c >> 4][c & 15]));
+      }
+      t3[10] = __builtin_fmaxf(acc[1][14], acc[1][15]);
+      const float u0 = __builtin_fmaxf(t3[0], __builtin_fmaxf(t3[1], t3[2]));
+      const float u1 = __builtin_fmaxf(t3[3], __builtin_fmaxf(t3[4], t3[5]));
+      const float u2 = __builtin_fmaxf(t3[6], __builtin_fmaxf(t3[7], t3[8]));
+      const float u3 = __builtin_fmaxf(t3[9], t3[10]);
+      mx = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
+    }
+    // max over the row's 64 keys, relative to the reference
+    mx = __builtin_fmaxf(mx, half_swap(mx)) - m;
+    // the normaliser sums the fp32 probabilities (plain adds: the bf16 dot
+    // instruction would wait for the other wave's MFMAs)
+    float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const bool need = m_set ? mx > kSlack : mx != -__builtin_inff();
+    if (__any(need)) {
+      // set or move this row's reference (rows that need neither keep theirs)
+      float shift = 0.0f, alpha = 1.0f;
+      if (!m_set) {
+        if (mx != -__builtin_inff()) {
+          shift = mx;  // o and l are still 0: no rescale
+          m_set = true;
+        }
+      } else if (mx > 0.0f) {
+        shift = mx;
+        alpha = __builtin_amdgcn_exp2f(-mx);
+      }
+      l *= alpha;
+#pragma unroll
+      for (int i = 0; i < DB; ++i) o[i] *= alpha;
+      m += shift;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
+          ls[r & 3] += p;
+          pb[blk][r >> 3][r & 7] = (__bf16)p;
+        }
+    } else {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
+          ls[r & 3] += p;
+          pb[blk][r >> 3][r & 7] = (__bf16)p;
+        }
+    }
+    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+  };
+
+  // phase barriers: the even ones leave loads in flight
+  auto bar_even = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto bar_odd = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+
+  if (n > 0) issue(kb, 0, kst0);
+  bar_odd();
+  // one pair of phases per j; stage parity is fixed per half of the unrolled loop
+  auto pair = [&](int j, __bf16 *kj, __bf16 *kj1, __bf16 *vj, __bf16 *vjm1)
+                  __attribute__((always_inline)) {
+    // phase 2j
+    if (j + 1 < n) issue(kb, j + 1, kj1);
+    if (j < n) issue(vb, j, vj);
+    if (lead)
+      mphase(j >= 1, vjm1, j < n, kj);
+    else if (j >= 1)
+      sphase(j - 1);
+    bar_even();
+    // phase 2j+1
+    if (lead) {
+      if (j < n) sphase(j);
+    } else {
+      mphase(j >= 1, vjm1, j < n, kj);
+    }
+    bar_odd();
+  };
+  for (int j = 0; j <= n; j += 2) {
+    pair(j, kst0, kst1, vst0, vst1);
+    if (j + 1 <= n) pair(j + 1, kst1, kst0, vst1, vst0);
+  }
+
+  // ---- finalize
+  const float lt = l + half_swap(l);
   if (!qvalid) return;
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
   if (n_splits == 1) {
@@ -539,20 +944,35 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
 
 }  // namespace
 
-int attn_splits(const AttnShape &s) {
+// Kernel choice and prefix splits of a bf16 shape.  Long prefixes over at
+// least 256 query rows per KV head take the ping-pong kernel (one 8-wave
+// workgroup per CU); the rest the 4-wave kernel (two per CU).  Splits bring
+// the grid to about one (ping-pong) or two (4-wave) workgroups per CU.
+struct AttnPlan {
+  bool pingpong;
+  int tiles;
+  int splits;
+};
+static AttnPlan attn_plan(const AttnShape &s) {
   const int G = s.Hq / s.Hkv;
-  const int tiles = (s.N * G + BM - 1) / BM;
-  const long long base = (long long)s.B * s.Hkv * tiles;
-  const long long want_wgs = 512;  // two workgroups per CU
-  if (base >= want_wgs) return 1;
+  const int rows = s.N * G;
   const int max_prefix = s.S_max - s.N;
-  int by_len = max_prefix / 512;  // keep >= 512 keys per split
-  if (by_len < 1) by_len = 1;
-  long long sp = (want_wgs + base - 1) / base;
-  if (sp > by_len) sp = by_len;
-  if (sp > 64) sp = 64;
-  return (int)(sp < 1 ? 1 : sp);
+  const bool pp = rows >= 256 && max_prefix >= 4096;
+  const int bm = pp ? 256 : BM;
+  const int tiles = (rows + bm - 1) / bm;
+  const long long base = (long long)s.B * s.Hkv * tiles;
+  const long long want_wgs = pp ? 256 : 512;
+  int sp = 1;
+  if (base < want_wgs) {
+    const int by_len = std::max(1, max_prefix / (pp ? 1024 : 512));  // keys per split
+    long long x = (want_wgs + base - 1) / base;
+    x = std::min<long long>(std::min<long long>(x, by_len), 64);
+    sp = (int)std::max<long long>(x, 1);
+  }
+  return AttnPlan{pp, tiles, sp};
 }
+
+int attn_splits(const AttnShape &s) { return attn_plan(s).splits; }
 
 size_t attn_workspace_bytes(const AttnShape &s, tg_dtype dtype) {
   if (dtype != TG_BF16) return 0;
@@ -583,8 +1003,9 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
                             void *workspace, uint32_t *d_err,
                             hipStream_t stream) {
   const int G = s.Hq / s.Hkv;
-  const int tiles = (s.N * G + BM - 1) / BM;
-  const int sp = attn_splits(s);
+  const AttnPlan plan = attn_plan(s);
+  const int tiles = plan.tiles;
+  const int sp = plan.splits;
   const size_t rows = (size_t)s.B * s.N * s.Hq;
   float *part_o = sp > 1 ? reinterpret_cast<float *>(workspace) : nullptr;
   float *part_lse = sp > 1 ? part_o + (size_t)sp * rows * s.D : nullptr;
@@ -594,20 +1015,26 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   auto kb = reinterpret_cast<const __bf16 *>(k);
   auto vb = reinterpret_cast<const __bf16 *>(v);
   auto ob = reinterpret_cast<__bf16 *>(out);
-  // bitset words of the nodes one 128-row tile can hold
-  const int nodes_per_tile = std::min(s.N, (BM + G - 1) / G + 1);
-  const int anc_words = nodes_per_tile * ((s.N + 31) / 32);
-  auto go = [&](auto kernel, size_t lds) {
+  // bitset words of the nodes one row tile can hold
+  const int bm = plan.pingpong ? 256 : BM;
+  const int nodes_per_tile = std::min(s.N, (bm + G - 1) / G + 1);
+  const size_t lds = (size_t)nodes_per_tile * ((s.N + 31) / 32) * 4;
+  auto go = [&](auto kernel, const char *name, int threads) {
     hipError_t r = hipFuncSetAttribute((const void *)kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (r != hipSuccess) return r;
-    launch("attn_mfma", kernel, dim3((unsigned)grid), dim3(kThreads), lds, stream, qb, kb, vb,
-           parent, prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2,
-           tiles, sp, d_err);
+    launch(name, kernel, dim3((unsigned)grid), dim3(threads), lds, stream, qb, kb, vb, parent,
+           prefix_len, ob, part_o, part_lse, s.B, s.N, s.Hq, s.Hkv, s.S_max, scale2, tiles, sp,
+           d_err);
     return hipSuccess;
   };
-  hipError_t e = s.D == 64 ? go(attn_mfma_kernel<64>, AttnLds<64>::bytes(anc_words))
-                           : go(attn_mfma_kernel<128>, AttnLds<128>::bytes(anc_words));
+  hipError_t e;
+  if (plan.pingpong)
+    e = s.D == 64 ? go(attn_pingpong_kernel<64>, "attn_pingpong", 512)
+                  : go(attn_pingpong_kernel<128>, "attn_pingpong", 512);
+  else
+    e = s.D == 64 ? go(attn_mfma_kernel<64>, "attn_mfma", kThreads)
+                  : go(attn_mfma_kernel<128>, "attn_mfma", kThreads);
   if (e != hipSuccess) return e;
   e = hipGetLastError();
   if (e != hipSuccess || sp <= 1) return e;
