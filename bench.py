@@ -78,6 +78,31 @@ def parse():
     return ap.parse_args()
 
 
+# ------------------------------------------------------- measured traffic
+
+def profile_traffic(name):
+    """HBM bytes per launch from a committed counter summary
+    (profiles/<name>), or None when the kernel sources listed there no longer
+    hash to the recorded value (the counters describe an older kernel)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", name)
+    try:
+        fields = {}
+        for line in open(path):
+            if line.startswith("traffic_") and ":" in line:
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+        h = hashlib.sha256()
+        for src in fields["traffic_sources"].split(","):
+            with open(os.path.join(ROOT, src), "rb") as f:
+                h.update(f.read())
+        if h.hexdigest() != fields["traffic_sha256"]:
+            return None
+        return float(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 # ---------------------------------------------------------------- inputs
 
 def make_inputs(c, dev):
@@ -317,7 +342,9 @@ def attention_bench(args, tg, torch, dev):
         "config": {"workload": args.workload, "batch": Bq, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": Dh, "prefix": Lp, "tree_nodes": Nn, "input_copies": copies},
         "roofline": {"bound": bound, "kernel": main_k, "achieved": ach, "peak": peak,
-                     "unit": unit, "frac": ach / peak, "traffic": None,
+                     "unit": unit, "frac": ach / peak,
+                     "traffic": profile_traffic("attn_pingpong_llama70b_traffic.md")
+                     if args.workload == "attn-llama70b" and main_k == "attn_pingpong" else None,
                      "avg_launch_us": main_us},
         "TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
         "bytes": nbytes, "flops": flops,
@@ -416,7 +443,9 @@ def tree_bench(args, tg, torch, dev):
                    "K_or_m": Mm if rescore else K, "input_copies": copies},
         "roofline": {"bound": "hbm", "kernel": "row_partial", "achieved": ach / 1e9,
                      "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": ach / PEAK_HBM,
-                     "traffic": None, "avg_launch_us": row_us},
+                     "traffic": None if rescore else
+                     profile_traffic("row_partial_expand_twodrafter_traffic.md"),
+                     "avg_launch_us": row_us},
         "call_TB/s": nbytes / (ms * 1e-3) / 1e12,
         "kernels": {k: {"launches_per_call": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0]}
                     for k, v in kern.items()},
@@ -548,7 +577,8 @@ def main():
         launches = kern[dom][0]
         achieved = dom_bytes * args.steps / (kern[dom][1] * 1e-3)
         roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": achieved / PEAK_HBM, "traffic": None,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM,
+                "traffic": profile_traffic("row_partial_turn_llama8b_traffic.md"),
                 "bytes_per_launch": dom_bytes * args.steps / launches,
                 "avg_launch_us": 1e3 * kern[dom][1] / launches}
     else:

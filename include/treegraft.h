@@ -251,14 +251,19 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
 /* Kernel timing (benchmarks and profiling; not part of the hot path).      */
 /*
  * tg_trace_begin(capacity) creates `capacity` HIP event pairs and turns
- * tracing on: from then on every kernel the library launches is dispatched
- * with its own start/stop events (hipExtLaunchKernelGGL), so each record is
- * the device time of one kernel on the stream it ran on.  Launches beyond
- * `capacity` are not recorded.  tg_trace_end waits for the recorded events,
- * writes at most max_records records in launch order (kernel names are
- * static strings owned by the library), frees the events and turns tracing
- * off.  Tracing state is process-global and not thread-safe; while it is
- * off (the default) no event is created or recorded.
+ * tracing on: from then on every kernel the library launches is bracketed by
+ * hipEventRecord(start) / hipEventRecord(stop) on the stream it is launched
+ * on, so each record is the device time of one kernel including its
+ * dispatch (a few microseconds more than a profiler's kernel time).
+ * Launches beyond `capacity` are not recorded.  Meant for eager launches:
+ * event records captured into a HIP graph cannot be timed.
+ * tg_trace_read waits for the recorded events and writes at most
+ * max_records records in launch order (kernel names are static strings
+ * owned by the library) without ending the trace.  tg_trace_end does the
+ * same once, then frees the events and turns tracing off.  Tracing state is process-global
+ * and not thread-safe; while it is off (the default) no event is created or
+ * recorded.  Errors: TG_ERR_INVALID_ARG when tracing is not on (read, end)
+ * or already on (begin), or capacity <= 0; TG_ERR_HIP when an event fails.
  */
 typedef struct {
   const char *kernel;
@@ -266,6 +271,7 @@ typedef struct {
 } tg_trace_record;
 
 tg_status tg_trace_begin(int capacity);
+tg_status tg_trace_read(tg_trace_record *out, int max_records, int *n_records);
 tg_status tg_trace_end(tg_trace_record *out, int max_records, int *n_records);
 
 #ifdef __cplusplus

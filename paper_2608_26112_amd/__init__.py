@@ -39,6 +39,7 @@ EXPORTED = (
     "tg_status_str",
     "tg_tree_reset",
     "tg_trace_begin",
+    "tg_trace_read",
     "tg_trace_end",
     "tg_verify_attention_workspace",
     "tg_tree_verify_attention",
@@ -114,6 +115,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_trace_begin.argtypes = [_i32]
     lib.tg_trace_end.restype = _i32
     lib.tg_trace_end.argtypes = [ctypes.POINTER(TgTraceRecord), _i32, ctypes.POINTER(_i32)]
+    lib.tg_trace_read.restype = _i32
+    lib.tg_trace_read.argtypes = [ctypes.POINTER(TgTraceRecord), _i32, ctypes.POINTER(_i32)]
     _lib = lib
     return lib
 
@@ -334,6 +337,15 @@ def tree_reset(tree: TreeState, stream=None):
 def trace_begin(capacity: int = 4096):
     """Turn on per-kernel device timing (see tg_trace_begin)."""
     _check("tg_trace_begin", load().tg_trace_begin(int(capacity)))
+
+
+def trace_read(max_records: int = 1 << 16):
+    """Current per-kernel records without ending the trace (see tg_trace_read)."""
+    lib = load()
+    recs = (TgTraceRecord * max_records)()
+    n = ctypes.c_int(0)
+    _check("tg_trace_read", lib.tg_trace_read(recs, max_records, ctypes.byref(n)))
+    return [(recs[i].kernel.decode(), float(recs[i].ms)) for i in range(n.value)]
 
 
 def trace_end(max_records: int = 1 << 16):

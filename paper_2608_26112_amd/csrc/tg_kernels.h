@@ -7,7 +7,6 @@
 
 #include "../../include/treegraft.h"
 
-#include <hip/hip_ext.h>
 
 namespace tg {
 
@@ -20,10 +19,10 @@ template <typename F, typename... Args>
 void launch(const char *name, F kernel, dim3 grid, dim3 block, size_t shmem,
             hipStream_t stream, Args... args) {
   hipEvent_t a, b;
-  if (trace_slot(name, &a, &b))
-    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shmem, stream, a, b, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, args...);
+  const bool traced = trace_slot(name, &a, &b);
+  if (traced) (void)hipEventRecord(a, stream);
+  hipLaunchKernelGGL(kernel, grid, block, shmem, stream, args...);
+  if (traced) (void)hipEventRecord(b, stream);
 }
 
 // ------------------------------------------------------------ logits rows

@@ -1,7 +1,6 @@
 // Optional kernel timing.  While tracing is on, every kernel the library
-// launches is dispatched with hipExtLaunchKernelGGL and a start/stop event
-// pair from a preallocated pool, so the measured interval is the dispatch
-// itself on the caller's stream.  Off by default; process-global; not
+// launches is bracketed by a start/stop event pair from a preallocated pool,
+// recorded on the launch stream.  Off by default; process-global; not
 // thread-safe (meant for benchmarks and profiling runs).
 #include <hip/hip_runtime.h>
 
@@ -50,10 +49,8 @@ tg_status tg_trace_begin(int capacity) {
   return TG_OK;
 }
 
-tg_status tg_trace_end(tg_trace_record *out, int max_records, int *n_records) {
+static tg_status trace_collect(tg_trace_record *out, int max_records, int *n_records) {
   auto &t = tg::g_trace;
-  if (!t.on) return TG_ERR_INVALID_ARG;
-  t.on = false;
   tg_status st = TG_OK;
   int n = 0;
   for (int i = 0; i < t.n; ++i) {
@@ -70,6 +67,19 @@ tg_status tg_trace_end(tg_trace_record *out, int max_records, int *n_records) {
     }
   }
   if (n_records) *n_records = n;
+  return st;
+}
+
+tg_status tg_trace_read(tg_trace_record *out, int max_records, int *n_records) {
+  if (!tg::g_trace.on) return TG_ERR_INVALID_ARG;
+  return trace_collect(out, max_records, n_records);
+}
+
+tg_status tg_trace_end(tg_trace_record *out, int max_records, int *n_records) {
+  auto &t = tg::g_trace;
+  if (!t.on) return TG_ERR_INVALID_ARG;
+  t.on = false;
+  const tg_status st = trace_collect(out, max_records, n_records);
   for (size_t i = 0; i < t.start.size(); ++i) {
     if (t.start[i]) (void)hipEventDestroy(t.start[i]);
     if (t.stop[i]) (void)hipEventDestroy(t.stop[i]);

@@ -177,6 +177,7 @@ def test_reset_and_trace_host_checks(lib):
     assert lib.tg_trace_begin(0) == tg.ERR_INVALID_ARG
     n = ctypes.c_int(7)
     assert lib.tg_trace_end(None, 0, ctypes.byref(n)) == tg.ERR_INVALID_ARG  # not tracing
+    assert lib.tg_trace_read(None, 0, ctypes.byref(n)) == tg.ERR_INVALID_ARG
 
 
 def test_python_binding_rejects_cpu_tensors():
