@@ -18,6 +18,8 @@ Grafting for Tree-Based Speculative Decoding):
     App. E sets temperature 0).
   * ``tree.global_prune`` - Alg. 3 taken step by step, with the verification
     buffers (mask, position ids, retrieval paths).
+  * ``attention.kv_compact`` - the cache update after acceptance: the accepted
+    chain's K/V rows become the continuation of the prefix.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library

@@ -126,3 +126,45 @@ def tree_verify_attention_fast(q, k_cache, v_cache, parent, prefix_len, sm_scale
                 p = e / e.sum(axis=1, keepdims=True)
                 out[b, i, g * G:(g + 1) * G] = p[:, :L] @ Vp + p[:, L:] @ Vt[path]
     return out
+
+
+def kv_compact(k_cache, v_cache, prefix_len, path, n_path):
+    """Cache update after acceptance, as a plain gather (returns new arrays).
+
+    The verified tokens become the next turn's prefix (Sec. 3.1: the root of
+    the draft tree is the verified prefix).  In the verify layout tree slot a
+    of sequence b holds the K/V of tree node a at cache row L_b + a; the
+    accepted chain is given as tree slots path[b, 0:n_b] (the root's slot 0
+    first when it carries a token, then the accepted nodes, parents before
+    children).  Afterwards rows L_b + j, j < n_b, hold what rows
+    L_b + path[b, j] held, the other rows are unchanged, and the prefix
+    length becomes L_b + n_b.
+
+    Reading where the paper is silent: the chain must be strictly increasing
+    with path[b, j] >= j (it is, for a root-to-node path in a parents-first
+    layout) and fit the cache (L_b + path[b, j] < S_max); a sequence that
+    violates this is left untouched, keeps its length and raises
+    DERR_BAD_NODE.
+    """
+    k2 = np.array(k_cache, copy=True)
+    v2 = np.array(v_cache, copy=True)
+    B, _, S_max, _ = k2.shape
+    new_len = np.zeros(B, dtype=np.int32)
+    err = 0
+    for b in range(B):
+        L, n = int(prefix_len[b]), int(n_path[b])
+        new_len[b] = L
+        p = [int(x) for x in path[b, :max(n, 0)]]
+        ok = 0 <= n <= path.shape[1] and L >= 0
+        ok = ok and all(p[j] >= j and (j == 0 or p[j] > p[j - 1]) for j in range(n))
+        ok = ok and all(L + x < S_max for x in p)
+        if not ok:
+            err |= 16
+            continue
+        rows_k = [k_cache[b, :, L + x, :].copy() for x in p]
+        rows_v = [v_cache[b, :, L + x, :].copy() for x in p]
+        for j in range(n):
+            k2[b, :, L + j, :] = rows_k[j]
+            v2[b, :, L + j, :] = rows_v[j]
+        new_len[b] = L + n
+    return k2, v2, new_len, err

@@ -12,7 +12,7 @@ import torch
 import torch.nn.functional as Fnn
 
 import workloads as W
-from oracle.attention import (path_of, sanitize_parent, tree_verify_attention,
+from oracle.attention import (kv_compact, path_of, sanitize_parent, tree_verify_attention,
                               tree_verify_attention_fast)
 
 
@@ -181,3 +181,61 @@ def test_sampled_rows_equal_full():
     part = tree_verify_attention(q, k, v, parent, plen, 0.3, rows=rows)
     for r, (b, i, h) in enumerate(rows):
         assert np.array_equal(part[r], full[b, i, h])
+
+
+# ---------------------------------------------------------------- kv compact
+
+def _accepted_chain(parent, leaf):
+    """Tree slots of the root-to-leaf chain (parents first)."""
+    return path_of(sanitize_parent(parent), leaf)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_kv_compact_turns_the_accepted_chain_into_causal_prefix(seed):
+    """After compaction, the accepted leaf's output equals plain causal
+    attention over the new prefix: the node attends to the old prefix plus
+    its root-to-node chain, exactly the rows the compaction lines up at
+    [L, L + n).  Pins the gather against the attention definition."""
+    g = W.rng(700 + seed)
+    B, N, Hq, Hkv, D = 2, 12, 4, 2, 16
+    L = [5, 9]
+    S = max(L) + N + 3
+    parent = np.stack([W.uniform_parents(g, N) for _ in range(B)]).astype(np.int32)
+    q = W.normal(g, (B, N, Hq, D))
+    k = W.normal(g, (B, Hkv, S, D))
+    v = W.normal(g, (B, Hkv, S, D))
+    leaves = [int(g.integers(0, N)) for _ in range(B)]
+    paths = [_accepted_chain(parent[b], leaves[b]) for b in range(B)]
+    width = max(len(p) for p in paths) + 2
+    path = np.full((B, width), -7, np.int32)
+    n_path = np.array([len(p) for p in paths], np.int32)
+    for b in range(B):
+        path[b, :len(paths[b])] = paths[b]
+    before = tree_verify_attention(q, k, v, parent, np.array(L), 0.3)
+    k2, v2, new_len, err = kv_compact(k, v, np.array(L), path, n_path)
+    assert err == 0 and list(new_len) == [L[b] + n_path[b] for b in range(B)]
+    for b in range(B):
+        n = int(n_path[b])
+        chain = np.arange(-1, n - 1, dtype=np.int32)[None]      # 0 <- 1 <- ... <- n-1
+        qb = q[b:b + 1, leaves[b]:leaves[b] + 1]
+        qq = np.zeros((1, n, Hq, D))
+        qq[0, n - 1] = qb[0, 0]
+        after = tree_verify_attention(qq, k2[b:b + 1], v2[b:b + 1], chain, np.array([L[b]]), 0.3)
+        assert np.allclose(after[0, n - 1], before[b, leaves[b]], rtol=1e-12, atol=1e-12)
+
+
+def test_kv_compact_identity_and_errors():
+    g = W.rng(710)
+    B, Hkv, S, D = 3, 2, 20, 4
+    k = W.normal(g, (B, Hkv, S, D))
+    v = W.normal(g, (B, Hkv, S, D))
+    L = np.array([4, 6, 2])
+    path = np.array([[0, 1, 2, 3], [0, 2, 1, 5], [0, 3, 9, 18]], np.int32)
+    n = np.array([4, 3, 4], np.int32)
+    k2, v2, new_len, err = kv_compact(k, v, L, path, n)
+    assert np.array_equal(k2[0], k[0]) and new_len[0] == 8          # identity chain
+    assert np.array_equal(k2[1], k[1]) and new_len[1] == 6          # not increasing
+    assert np.array_equal(k2[2], k[2]) and new_len[2] == 2          # 2 + 18 >= 20
+    assert err == 16
+    _, _, nl, e0 = kv_compact(k, v, L, path, np.zeros(3, np.int32))
+    assert e0 == 0 and list(nl) == list(L)
