@@ -248,6 +248,68 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
                          void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Final pruning and the verification buffers (Alg. 3, global score-based
+ * pruning with ancestor closure).                                          */
+/*
+ * tg_tree_global_prune keeps at most B_ver non-root nodes of each tree b:
+ * the non-root nodes are ranked by (cum desc, depth asc, id asc); in rank
+ * order each node is kept together with its not-yet-kept ancestors when the
+ * kept set (root included) stays within M = B_ver + 1, until it holds M
+ * nodes; a tree with n_nodes <= B_ver keeps everything.  Depths are
+ * recomputed from `parent` (root depth 0).  The kept nodes are re-indexed by
+ * (depth, original id), which puts parents before children.  Verify index 0
+ * is the root and verify index j + 1 is kept node j.  Outputs for tree b
+ * (nk = n_keep[b] kept non-root nodes, nl = n_leaves[b]):
+ *   kept[b, j]          original node id of kept node j         [B, B_ver]
+ *   vparent[b, j]       its parent as a kept-node index, -1 = root [B, B_ver]
+ *   vtoken[b, j]        its token                               [B, B_ver]
+ *   position_ids[b, u]  depth of verify row u (root 0)          [B, B_ver + 1]
+ *   mask[b, u, w]       bit v of word w = v / 32 is set iff verify node v
+ *                       is the root, an ancestor of u or u itself
+ *                                               [B, B_ver + 1, ceil((B_ver + 1) / 32)]
+ *   retrieval[b, r, c]  the root-to-leaf path of the r-th leaf (leaves in
+ *                       verify order), as verify indices with the root at
+ *                       column 0, padded with -1          [B, B_ver + 1, max_path]
+ *   n_keep[b], n_leaves[b]                                      [B]
+ * Entries past nk, past nl and past a path are -1 (mask words 0).  Errors
+ * (device word): n_nodes outside [0, cap] -> TG_DERR_BAD_NODE (nothing
+ * kept); a parent outside [-1, v-1] -> TG_DERR_BAD_PARENT (read as the root);
+ * a root-to-leaf path longer than max_path -> TG_DERR_CAPACITY (that tree's
+ * retrieval rows are all -1).  When the ranking puts every parent before its
+ * children (always so for trees this library grows: cum never increases
+ * along a path and ties go to the smaller depth) the kept set is the first
+ * B_ver ranked nodes; other inputs take the literal loop on one thread
+ * (O(n * depth)).  Host checks: 1 <= B_ver <= TG_MAX_CAP, 1 <= max_path,
+ * tree cap <= TG_MAX_CAP, every pointer non-NULL except d_err / stream.
+ */
+tg_status tg_tree_global_prune(const tg_tree *tree, int B, int B_ver, int max_path,
+                               int32_t *kept, int32_t *vparent, int32_t *vtoken,
+                               int32_t *position_ids, uint32_t *mask, int32_t *retrieval,
+                               int32_t *n_keep, int32_t *n_leaves, uint32_t *d_err,
+                               void *stream);
+
+/*
+ * tg_kv_compact: the cache update after acceptance.  The verified tokens
+ * extend the prefix (Sec. 3.1: the draft tree's root is the verified
+ * prefix).  For sequence b with L = prefix_len[b] and n = n_path[b], the K
+ * and V rows at cache positions L + path[b, j] move to L + j for j < n, in
+ * every KV head, and new_prefix_len[b] = L + n.  path[b, .] holds tree slots
+ * of the verify layout (slot a lives at cache row L + a): the root's slot 0
+ * first when it carries a token, then the accepted nodes, parents first.
+ * It must be strictly increasing with path[b, j] >= j and
+ * L + path[b, j] < S_max; otherwise sequence b is left untouched,
+ * new_prefix_len[b] = L and TG_DERR_BAD_NODE is raised.  k_cache, v_cache
+ * [B, Hkv, S_max, D] in `dtype`, updated in place; path [B, max_path];
+ * prefix_len, n_path, new_prefix_len [B] device int32 (new_prefix_len must
+ * not alias prefix_len).  Host checks: D in {64, 128}, 0 <= max_path,
+ * positive sizes.
+ */
+tg_status tg_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
+                        const int32_t *path, const int32_t *n_path, int B, int Hkv, int S_max,
+                        int D, int max_path, tg_dtype dtype, int32_t *new_prefix_len,
+                        uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (benchmarks and profiling; not part of the hot path).      */
 /*
  * tg_trace_begin(capacity) creates `capacity` HIP event pairs and turns

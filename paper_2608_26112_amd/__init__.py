@@ -48,6 +48,8 @@ EXPORTED = (
     "tg_rescore_graft_workspace",
     "tg_tree_rescore_graft",
     "tg_tree_accept",
+    "tg_tree_global_prune",
+    "tg_kv_compact",
 )
 
 
@@ -111,6 +113,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_tree_accept.argtypes = [_vp] * 4 + [_i32] * 3 + [_vp] * 5
     lib.tg_tree_reset.restype = _i32
     lib.tg_tree_reset.argtypes = [ctypes.POINTER(TgTree), _i32, _vp]
+    lib.tg_tree_global_prune.restype = _i32
+    lib.tg_tree_global_prune.argtypes = [ctypes.POINTER(TgTree)] + [_i32] * 3 + [_vp] * 10
+    lib.tg_kv_compact.restype = _i32
+    lib.tg_kv_compact.argtypes = [_vp] * 5 + [_i32] * 6 + [_vp] * 3
     lib.tg_trace_begin.restype = _i32
     lib.tg_trace_begin.argtypes = [_i32]
     lib.tg_trace_end.restype = _i32
@@ -325,6 +331,56 @@ def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_pa
                             _ptr(d_err), _stream(stream))
     _check("tg_tree_accept", st)
     return accept_len, accept_path, bonus
+
+
+def global_prune(tree: TreeState, B_ver: int, max_path: int | None = None, d_err=None,
+                 stream=None):
+    """Alg. 3 pruning of every tree to B_ver non-root nodes plus the
+    verification buffers (see tg_tree_global_prune).  Returns a dict of device
+    tensors: kept, vparent, vtoken [B, B_ver]; position_ids [B, B_ver+1];
+    mask [B, B_ver+1, W] uint32 bitsets; retrieval [B, B_ver+1, max_path];
+    n_keep, n_leaves [B]."""
+    lib = load()
+    B, dev = tree.B, tree.parent.device
+    M = B_ver + 1
+    max_path = M if max_path is None else int(max_path)
+    i32 = dict(dtype=torch.int32, device=dev)
+    out = dict(kept=torch.empty((B, B_ver), **i32), vparent=torch.empty((B, B_ver), **i32),
+               vtoken=torch.empty((B, B_ver), **i32), position_ids=torch.empty((B, M), **i32),
+               mask=torch.empty((B, M, (M + 31) // 32), dtype=torch.int32, device=dev),
+               retrieval=torch.empty((B, M, max_path), **i32),
+               n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
+    ts = tree.struct()
+    st = lib.tg_tree_global_prune(ctypes.byref(ts), B, int(B_ver), max_path,
+                                  *(_ptr(out[k]) for k in ("kept", "vparent", "vtoken",
+                                                           "position_ids", "mask", "retrieval",
+                                                           "n_keep", "n_leaves")),
+                                  _ptr(d_err), _stream(stream))
+    _check("tg_tree_global_prune", st)
+    return out
+
+
+def kv_compact(k_cache, v_cache, prefix_len, path, n_path, new_prefix_len=None, d_err=None,
+               stream=None):
+    """Move the accepted chain's K/V rows to the end of the prefix, in place
+    (see tg_kv_compact).  k_cache/v_cache [B, Hkv, S_max, D] (bf16 or fp32);
+    path [B, max_path]; prefix_len, n_path [B].  Returns new_prefix_len [B]."""
+    lib = load()
+    _dev(k_cache, "k_cache")
+    _dev(v_cache, "v_cache")
+    for t, n in ((prefix_len, "prefix_len"), (path, "path"), (n_path, "n_path")):
+        _dev(t, n, torch.int32)
+    if k_cache.shape != v_cache.shape or k_cache.dtype != v_cache.dtype:
+        raise ValueError("k_cache and v_cache must match")
+    B, Hkv, S_max, D = k_cache.shape
+    dt = {torch.bfloat16: BF16, torch.float32: F32}[k_cache.dtype]
+    if new_prefix_len is None:
+        new_prefix_len = torch.empty((B,), dtype=torch.int32, device=k_cache.device)
+    st = lib.tg_kv_compact(_ptr(k_cache), _ptr(v_cache), _ptr(prefix_len), _ptr(path),
+                           _ptr(n_path), B, Hkv, S_max, D, path.shape[1], dt,
+                           _ptr(new_prefix_len), _ptr(d_err), _stream(stream))
+    _check("tg_kv_compact", st)
+    return new_prefix_len
 
 
 def tree_reset(tree: TreeState, stream=None):

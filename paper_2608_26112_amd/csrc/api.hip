@@ -182,4 +182,35 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
                                     reinterpret_cast<hipStream_t>(stream)));
 }
 
+tg_status tg_tree_global_prune(const tg_tree *tree, int B, int B_ver, int max_path,
+                               int32_t *kept, int32_t *vparent, int32_t *vtoken,
+                               int32_t *position_ids, uint32_t *mask, int32_t *retrieval,
+                               int32_t *n_keep, int32_t *n_leaves, uint32_t *d_err,
+                               void *stream) {
+  if (!tree_ok(tree) || !kept || !vparent || !vtoken || !position_ids || !mask ||
+      !retrieval || !n_keep || !n_leaves)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || B_ver < 1 || max_path < 1) return TG_ERR_INVALID_ARG;
+  if (B_ver > TG_MAX_CAP || tree->cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  return from_hip(tg::launch_global_prune(*tree, B, B_ver, max_path, kept, vparent, vtoken,
+                                          position_ids, mask, retrieval, n_keep, n_leaves,
+                                          d_err, reinterpret_cast<hipStream_t>(stream)));
+}
+
+tg_status tg_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
+                        const int32_t *path, const int32_t *n_path, int B, int Hkv, int S_max,
+                        int D, int max_path, tg_dtype dtype, int32_t *new_prefix_len,
+                        uint32_t *d_err, void *stream) {
+  if (!k_cache || !v_cache || !prefix_len || !n_path || !new_prefix_len)
+    return TG_ERR_INVALID_ARG;
+  if ((const void *)new_prefix_len == (const void *)prefix_len) return TG_ERR_INVALID_ARG;
+  if (B <= 0 || Hkv <= 0 || S_max <= 0 || max_path < 0) return TG_ERR_INVALID_ARG;
+  if (max_path > 0 && !path) return TG_ERR_INVALID_ARG;
+  if (dtype != TG_F32 && dtype != TG_BF16) return TG_ERR_INVALID_ARG;
+  if (D != 64 && D != 128) return TG_ERR_UNSUPPORTED;
+  return from_hip(tg::launch_kv_compact(k_cache, v_cache, prefix_len, path, n_path, B, Hkv,
+                                        S_max, D, max_path, dtype, new_prefix_len, d_err,
+                                        reinterpret_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -1,0 +1,286 @@
+// Final pruning to the verification budget with ancestor closure and the
+// verification buffers (Alg. 3), and the cache update after acceptance.
+//
+// prune_kernel: one workgroup per tree, everything in LDS (n <= 4096):
+//   depths by pointer jumping over the parent links (log2 n rounds);
+//   rank: bitonic sort of the node keys (cum desc, depth asc, id asc);
+//   keep: when every parent ranks before its children the kept set is the
+//         first B_ver ranked nodes (one parallel check); otherwise one thread
+//         runs the literal loop (chains added while they fit);
+//   re-index: second bitonic sort of the kept nodes by (depth, id);
+//   buffers: parents, tokens, depths, ancestor bitsets, root-to-leaf paths.
+// kv_compact_kernel: one workgroup per (sequence, KV head); every thread
+// copies its 16-byte column of the accepted rows in path order, which is
+// safe in place because a row is only overwritten after it has been read
+// (path[j] >= j, strictly increasing).
+#include "tg_device.h"
+#include "tg_kernels.h"
+
+namespace tg {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void prune_kernel(
+    tg_tree tree, int B_ver, int max_path, int32_t *__restrict__ kept,
+    int32_t *__restrict__ vparent, int32_t *__restrict__ vtoken,
+    int32_t *__restrict__ position_ids, uint32_t *__restrict__ mask,
+    int32_t *__restrict__ retrieval, int32_t *__restrict__ n_keep,
+    int32_t *__restrict__ n_leaves, uint32_t *d_err) {
+  __shared__ uint64_t key[TG_MAX_CAP];
+  __shared__ int16_t par[TG_MAX_CAP];
+  __shared__ int16_t anc[2][TG_MAX_CAP];
+  __shared__ int16_t dep[2][TG_MAX_CAP];
+  __shared__ int16_t newid[TG_MAX_CAP];    // original id -> verify index (0 = dropped)
+  __shared__ int16_t order[TG_MAX_CAP];    // kept index -> original id
+  __shared__ uint8_t flag[TG_MAX_CAP + 1];
+  __shared__ int cnt[kThreads];
+  __shared__ int nk_s, nl_s, viol_s, deep_s;
+
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int cap = tree.cap;
+  const int M = B_ver + 1;
+  const int W = (M + 31) / 32;
+  const size_t base = (size_t)b * cap;
+  int n = tree.n_nodes[b];
+  if (n < 0 || n > cap) {
+    if (tid == 0) report(d_err, TG_DERR_BAD_NODE);
+    n = -1;  // nothing kept, outputs padded below
+  }
+  const int nn = n < 0 ? 0 : n;
+
+  // ---- parents (sanitised) and depths by pointer jumping
+  bool badp = false;
+  for (int v = tid; v < nn; v += kThreads) {
+    int p = tree.parent[base + v];
+    if (p < -1 || p >= v) {
+      badp = true;
+      p = -1;
+    }
+    par[v] = (int16_t)p;
+    anc[0][v] = (int16_t)p;
+    dep[0][v] = 1;
+  }
+  if (badp) report(d_err, TG_DERR_BAD_PARENT);
+  if (tid == 0) {
+    viol_s = 0;
+    deep_s = 0;
+  }
+  __syncthreads();
+  int cur = 0;
+  for (int span = 1; span < nn; span <<= 1) {
+    const int nxt = cur ^ 1;
+    for (int v = tid; v < nn; v += kThreads) {
+      const int a = anc[cur][v];
+      anc[nxt][v] = a >= 0 ? anc[cur][a] : (int16_t)-1;
+      dep[nxt][v] = a >= 0 ? (int16_t)(dep[cur][v] + dep[cur][a]) : dep[cur][v];
+    }
+    cur = nxt;
+    __syncthreads();
+  }
+  const int16_t *depth = dep[cur];
+
+  // ---- rank by (cum desc, depth asc, id asc)
+  const int P2 = pow2_at_least(nn > 0 ? nn : 1);
+  for (int i = tid; i < P2; i += kThreads)
+    key[i] = i < nn ? node_key(tree.cum[base + i], depth[i], i) : 0;
+  __syncthreads();
+  block_bitonic_desc(key, P2);
+
+  // ---- keep
+  for (int v = tid; v < nn; v += kThreads) flag[v] = 0;
+  __syncthreads();
+  int16_t *rank = anc[cur ^ 1];  // free now
+  if (nn <= B_ver) {
+    for (int v = tid; v < nn; v += kThreads) flag[v] = 1;
+  } else {
+    for (int i = tid; i < nn; i += kThreads) rank[node_key_id(key[i])] = (int16_t)i;
+    __syncthreads();
+    bool viol = false;
+    for (int v = tid; v < nn; v += kThreads) viol |= par[v] >= 0 && rank[par[v]] > rank[v];
+    if (viol) viol_s = 1;
+    __syncthreads();
+    if (!viol_s) {
+      for (int i = tid; i < B_ver; i += kThreads) flag[node_key_id(key[i])] = 1;
+    } else if (tid == 0) {
+      // the literal loop: add each ranked node's missing ancestor chain if it fits
+      int size = 1;
+      for (int i = 0; i < nn && size < M; ++i) {
+        int len = 0;
+        for (int u = node_key_id(key[i]); u >= 0 && !flag[u]; u = par[u]) ++len;
+        if (size + len <= M) {
+          for (int u = node_key_id(key[i]); u >= 0 && !flag[u]; u = par[u]) flag[u] = 1;
+          size += len;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- re-index the kept nodes by (depth, id): descending sort of the
+  // complemented keys puts them first, in ascending (depth, id)
+  for (int i = tid; i < P2; i += kThreads)
+    key[i] = (i < nn && flag[i]) ? ~(((uint64_t)depth[i] << 32) | (uint64_t)i) : 0;
+  __syncthreads();
+  block_bitonic_desc(key, P2);
+  int c = 0;
+  for (int i = tid; i < P2; i += kThreads) c += key[i] != 0;
+  c = wave_sum_i32(c);
+  if ((tid & (kWave - 1)) == 0) cnt[tid / kWave] = c;
+  for (int v = tid; v < nn; v += kThreads) newid[v] = 0;
+  __syncthreads();
+  if (tid == 0) {
+    int t = 0;
+    for (int i = 0; i < kThreads / kWave; ++i) t += cnt[i];
+    nk_s = t;
+  }
+  __syncthreads();
+  const int nk = nk_s;
+  for (int j = tid; j < nk; j += kThreads) {
+    const int v = (int)(uint32_t)~key[j];
+    order[j] = (int16_t)v;
+    newid[v] = (int16_t)(j + 1);
+  }
+  __syncthreads();
+
+  // ---- per-node buffers
+  const size_t ob = (size_t)b * B_ver;
+  for (int j = tid; j < B_ver; j += kThreads) {
+    if (j < nk) {
+      const int v = order[j];
+      const int p = par[v];
+      kept[ob + j] = v;
+      vparent[ob + j] = p < 0 ? -1 : newid[p] - 1;
+      vtoken[ob + j] = tree.token[base + v];
+    } else {
+      kept[ob + j] = -1;
+      vparent[ob + j] = -1;
+      vtoken[ob + j] = -1;
+    }
+  }
+  const size_t pb = (size_t)b * M;
+  for (int u = tid; u < M; u += kThreads)
+    position_ids[pb + u] = u == 0 ? 0 : (u <= nk ? depth[order[u - 1]] : -1);
+  // verify parent of row u (root row 0 has none)
+  auto vpar = [&](int u) { return u == 0 ? -1 : (par[order[u - 1]] < 0 ? 0 : newid[par[order[u - 1]]]); };
+  // ancestor-or-self bitsets, one row per thread
+  for (int u = tid; u < M; u += kThreads) {
+    uint32_t *row = mask + (pb + u) * W;
+    for (int w = 0; w < W; ++w) row[w] = 0;
+    if (u <= nk && n >= 0)
+      for (int a = u; a >= 0; a = vpar(a)) row[a >> 5] |= 1u << (a & 31);
+  }
+
+  // ---- leaves in verify order and their root-to-leaf paths
+  for (int u = tid; u <= nk; u += kThreads) flag[u] = 1;
+  __syncthreads();
+  for (int u = 1 + tid; u <= nk; u += kThreads) flag[vpar(u)] = 0;
+  __syncthreads();
+  const int live = n < 0 ? 0 : nk + 1;  // verify rows (no root row for a bad tree)
+  const int per = (live + kThreads - 1) / kThreads;
+  const int lo = min(live, tid * per), hi = min(live, lo + per);
+  int mine = 0;
+  bool deep = false;
+  for (int u = lo; u < hi; ++u) {
+    if (!flag[u]) continue;
+    ++mine;
+    deep |= (u == 0 ? 0 : depth[order[u - 1]]) + 1 > max_path;
+  }
+  cnt[tid] = mine;
+  if (deep) deep_s = 1;
+  __syncthreads();
+  if (tid == 0) {
+    int t = 0;
+    for (int i = 0; i < kThreads; ++i) {
+      const int x = cnt[i];
+      cnt[i] = t;
+      t += x;
+    }
+    nl_s = t;
+    if (deep_s) report(d_err, TG_DERR_CAPACITY);
+  }
+  __syncthreads();
+  const bool write_paths = !deep_s;
+  const size_t rb = (size_t)b * M * max_path;
+  for (size_t i = tid; i < (size_t)M * max_path; i += kThreads) retrieval[rb + i] = -1;
+  __syncthreads();
+  if (write_paths) {
+    int r = cnt[tid];
+    for (int u = lo; u < hi; ++u) {
+      if (!flag[u]) continue;
+      int32_t *row = retrieval + rb + (size_t)r * max_path;
+      for (int a = u; a >= 0; a = vpar(a)) row[a == 0 ? 0 : depth[order[a - 1]]] = a;
+      ++r;
+    }
+  }
+  if (tid == 0) {
+    n_keep[b] = nk;
+    n_leaves[b] = n < 0 ? 0 : nl_s;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(64) void kv_compact_kernel(
+    T *__restrict__ k_cache, T *__restrict__ v_cache, const int32_t *__restrict__ prefix_len,
+    const int32_t *__restrict__ path, const int32_t *__restrict__ n_path, int Hkv, int S_max,
+    int D, int max_path, int32_t *__restrict__ new_prefix_len, uint32_t *d_err) {
+  const int b = blockIdx.x / Hkv, h = blockIdx.x - b * Hkv;
+  const int L = prefix_len[b];
+  const int n = n_path[b];
+  const int32_t *pp = path + (size_t)b * max_path;
+  bool ok = n >= 0 && n <= max_path && L >= 0;
+  for (int j = 0; ok && j < n; ++j) {
+    const int x = pp[j];
+    ok = x >= j && (j == 0 || x > pp[j - 1]) && L + x < S_max;
+  }
+  if (h == 0 && threadIdx.x == 0) {
+    if (!ok) report(d_err, TG_DERR_BAD_NODE);
+    new_prefix_len[b] = ok ? L + n : L;
+  }
+  if (!ok) return;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int cols = D * (int)sizeof(T) / 16;  // 16-byte columns per row
+  const size_t hb = ((size_t)b * Hkv + h) * (size_t)S_max * D;
+  for (int c = threadIdx.x; c < 2 * cols; c += blockDim.x) {
+    T *base = (c < cols ? k_cache : v_cache) + hb;
+    const int col = c < cols ? c : c - cols;
+    for (int j = 0; j < n; ++j) {
+      const int x = pp[j];
+      if (x == j) continue;
+      const u32x4 val = reinterpret_cast<const u32x4 *>(base + (size_t)(L + x) * D)[col];
+      reinterpret_cast<u32x4 *>(base + (size_t)(L + j) * D)[col] = val;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_global_prune(const tg_tree &tree, int B, int B_ver, int max_path,
+                               int32_t *kept, int32_t *vparent, int32_t *vtoken,
+                               int32_t *position_ids, uint32_t *mask, int32_t *retrieval,
+                               int32_t *n_keep, int32_t *n_leaves, uint32_t *d_err,
+                               hipStream_t stream) {
+  launch("global_prune", prune_kernel, dim3(B), dim3(kThreads), 0, stream, tree, B_ver,
+         max_path, kept, vparent, vtoken, position_ids, mask, retrieval, n_keep, n_leaves,
+         d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
+                             const int32_t *path, const int32_t *n_path, int B, int Hkv,
+                             int S_max, int D, int max_path, tg_dtype dtype,
+                             int32_t *new_prefix_len, uint32_t *d_err, hipStream_t stream) {
+  const dim3 grid((unsigned)((long long)B * Hkv)), blk(64);
+  if (dtype == TG_BF16)
+    launch("kv_compact", kv_compact_kernel<__bf16>, grid, blk, 0, stream,
+           reinterpret_cast<__bf16 *>(k_cache), reinterpret_cast<__bf16 *>(v_cache),
+           prefix_len, path, n_path, Hkv, S_max, D, max_path, new_prefix_len, d_err);
+  else
+    launch("kv_compact", kv_compact_kernel<float>, grid, blk, 0, stream,
+           reinterpret_cast<float *>(k_cache), reinterpret_cast<float *>(v_cache), prefix_len,
+           path, n_path, Hkv, S_max, D, max_path, new_prefix_len, d_err);
+  return hipGetLastError();
+}
+
+}  // namespace tg

@@ -76,6 +76,17 @@ hipError_t launch_accept(const int32_t *parent, const int32_t *token,
                          int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
                          hipStream_t stream);
 
+// ------------------------------------------------------- prune / cache
+hipError_t launch_global_prune(const tg_tree &tree, int B, int B_ver, int max_path,
+                               int32_t *kept, int32_t *vparent, int32_t *vtoken,
+                               int32_t *position_ids, uint32_t *mask, int32_t *retrieval,
+                               int32_t *n_keep, int32_t *n_leaves, uint32_t *d_err,
+                               hipStream_t stream);
+hipError_t launch_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
+                             const int32_t *path, const int32_t *n_path, int B, int Hkv,
+                             int S_max, int D, int max_path, tg_dtype dtype,
+                             int32_t *new_prefix_len, uint32_t *d_err, hipStream_t stream);
+
 // -------------------------------------------------------------- attention
 struct AttnShape {
   int B, N, Hq, Hkv, D, S_max;

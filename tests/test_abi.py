@@ -189,3 +189,33 @@ def test_python_binding_rejects_cpu_tensors():
         tg.verify_attention(q, torch.zeros(1, 2, 8, 64), torch.zeros(1, 2, 8, 64),
                             torch.zeros(1, 4, dtype=torch.int32),
                             torch.zeros(1, dtype=torch.int32), 0.125)
+
+
+def test_prune_and_kv_compact_host_checks(lib):
+    import paper_2608_26112_amd as tg
+
+    def prune(tree=None, **kw):
+        a = dict(B=1, B_ver=8, maxp=9, out=P)
+        a.update(kw)
+        t = _tree() if tree is None else tree
+        return lib.tg_tree_global_prune(ctypes.byref(t), a["B"], a["B_ver"], a["maxp"],
+                                        *([a["out"]] * 8), NULL, NULL)
+    assert prune(out=NULL) == tg.ERR_INVALID_ARG
+    assert prune(B_ver=0) == tg.ERR_INVALID_ARG
+    assert prune(maxp=0) == tg.ERR_INVALID_ARG
+    assert prune(B_ver=5000) == tg.ERR_UNSUPPORTED
+    assert prune(tree=_tree(cap=5000)) == tg.ERR_UNSUPPORTED
+    assert prune(tree=_tree(cum=1)) == tg.ERR_INVALID_ARG
+
+    def compact(**kw):
+        a = dict(k=P, v=P, pl=P, path=P, n=P, B=1, H=2, S=64, D=128, maxp=4, dt=tg.BF16,
+                 nl=ctypes.c_void_p(512))
+        a.update(kw)
+        return lib.tg_kv_compact(a["k"], a["v"], a["pl"], a["path"], a["n"], a["B"], a["H"],
+                                 a["S"], a["D"], a["maxp"], a["dt"], a["nl"], NULL, NULL)
+    assert compact(k=NULL) == tg.ERR_INVALID_ARG
+    assert compact(nl=P) == tg.ERR_INVALID_ARG            # aliases prefix_len
+    assert compact(path=NULL) == tg.ERR_INVALID_ARG
+    assert compact(D=96) == tg.ERR_UNSUPPORTED
+    assert compact(dt=5) == tg.ERR_INVALID_ARG
+    assert compact(maxp=-1) == tg.ERR_INVALID_ARG
