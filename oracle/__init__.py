@@ -20,6 +20,10 @@ Grafting for Tree-Based Speculative Decoding):
     buffers (mask, position ids, retrieval paths).
   * ``attention.kv_compact`` - the cache update after acceptance: the accepted
     chain's K/V rows become the continuation of the prefix.
+  * ``signals.tree_signals`` / ``signals.margin`` - the ten candidate tree
+    signals with the reselection preview frontier, and the scheduler's
+    margin predictor forward pass (App. online observations; value system
+    architecture).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library
@@ -31,4 +35,4 @@ attention), brute-force enumeration on tiny inputs, hand-derived golden cases
 under ``tests/golden/`` and invariants the paper's definitions fix.  No function
 here is "parity unpinned".
 """
-from . import attention, tree  # noqa: F401
+from . import attention, signals, tree  # noqa: F401
