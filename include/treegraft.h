@@ -310,6 +310,38 @@ tg_status tg_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
                         uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Scheduler observations and margin predictor (appendix on online
+ * observations: the candidate tree signals and the reselection preview
+ * frontier; appendix on the value system: the margin predictor).           */
+/*
+ * tg_tree_signals computes, for each tree b with current frontier
+ * frontier[b, 0:Fb] (node ids, -1 = root; Fb = n_frontier[b], or F when
+ * n_frontier is NULL), the ten pre-action signals into signals[b, 0:10] in
+ * this order: depth_before, leaf_ratio_before, pre_reselect_depth_delta,
+ * pre_reselect_cands, max_depth_before, collapse_debt,
+ * pre_reselect_past_ratio, pre_reselect_overlap, pre_reselect_score,
+ * finite_score_ratio_before.  The preview frontier is Top_W of the nodes
+ * (root included) whose depth lies within `lookback` below a frontier
+ * depth, ranked by (cum desc, depth asc, id asc).  Scores are the stored
+ * log-domain cum (root 0); "finite" means cum > -inf; depths are the
+ * stored ones (root 0).  An empty mean is NaN.
+ * When params is not NULL it holds the predictor's 3,265 weights, row-major
+ * W1[64,17], b1[64], W2[32,64], b2[32], W3[1,32], b3[1] (fp32), and
+ * context[b, 0:11] the runtime context (4) and scheduling history (7); the
+ * input is context followed by depth_before, leaf_ratio_before,
+ * collapse_debt, pre_reselect_past_ratio, pre_reselect_overlap,
+ * pre_reselect_score, and margin[b] / action[b] (1 = call the middle
+ * drafter iff margin > 0) are written.  Errors: n_nodes outside [0, cap] or
+ * a frontier id outside [-1, n_nodes) -> TG_DERR_BAD_NODE and NaN signals.
+ * Host checks: F, W >= 1, lookback >= 0, cap <= TG_MAX_CAP; context, margin
+ * and action are required with params.
+ */
+tg_status tg_tree_signals(const tg_tree *tree, const int32_t *frontier, const int32_t *n_frontier,
+                          int B, int F, int W, int lookback, const float *context,
+                          const float *params, float *signals, float *margin, int32_t *action,
+                          uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (benchmarks and profiling; not part of the hot path).      */
 /*
  * tg_trace_begin(capacity) creates `capacity` HIP event pairs and turns

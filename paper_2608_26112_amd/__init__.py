@@ -50,6 +50,7 @@ EXPORTED = (
     "tg_tree_accept",
     "tg_tree_global_prune",
     "tg_kv_compact",
+    "tg_tree_signals",
 )
 
 
@@ -115,6 +116,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_tree_reset.argtypes = [ctypes.POINTER(TgTree), _i32, _vp]
     lib.tg_tree_global_prune.restype = _i32
     lib.tg_tree_global_prune.argtypes = [ctypes.POINTER(TgTree)] + [_i32] * 3 + [_vp] * 10
+    lib.tg_tree_signals.restype = _i32
+    lib.tg_tree_signals.argtypes = ([ctypes.POINTER(TgTree), _vp, _vp] + [_i32] * 4 +
+                                    [_vp] * 7)
     lib.tg_kv_compact.restype = _i32
     lib.tg_kv_compact.argtypes = [_vp] * 5 + [_i32] * 6 + [_vp] * 3
     lib.tg_trace_begin.restype = _i32
@@ -381,6 +385,35 @@ def kv_compact(k_cache, v_cache, prefix_len, path, n_path, new_prefix_len=None, 
                            _ptr(new_prefix_len), _ptr(d_err), _stream(stream))
     _check("tg_kv_compact", st)
     return new_prefix_len
+
+
+def tree_signals(tree: TreeState, frontier, n_frontier, W: int, lookback: int = 5,
+                 context=None, params=None, d_err=None, stream=None):
+    """The ten pre-action tree signals per tree (see tg_tree_signals), and
+    with `params` (3265 fp32 predictor weights) and `context` [B, 11] the
+    margin [B] and action [B].  frontier [B, F] int32 (-1 = root);
+    n_frontier [B] or None.  Returns (signals [B, 10], margin, action)."""
+    lib = load()
+    _dev(frontier, "frontier", torch.int32)
+    if n_frontier is not None:
+        _dev(n_frontier, "n_frontier", torch.int32)
+    B, F = frontier.shape
+    dev = frontier.device
+    sig = torch.empty((B, 10), dtype=torch.float32, device=dev)
+    margin = action = None
+    if params is not None:
+        _dev(params, "params", torch.float32)
+        _dev(context, "context", torch.float32)
+        if params.numel() != 3265 or tuple(context.shape) != (B, 11):
+            raise ValueError("params must hold 3265 values and context be [B, 11]")
+        margin = torch.empty((B,), dtype=torch.float32, device=dev)
+        action = torch.empty((B,), dtype=torch.int32, device=dev)
+    ts = tree.struct()
+    st = lib.tg_tree_signals(ctypes.byref(ts), _ptr(frontier), _ptr(n_frontier), B, F, int(W),
+                             int(lookback), _ptr(context), _ptr(params), _ptr(sig),
+                             _ptr(margin), _ptr(action), _ptr(d_err), _stream(stream))
+    _check("tg_tree_signals", st)
+    return sig, margin, action
 
 
 def tree_reset(tree: TreeState, stream=None):

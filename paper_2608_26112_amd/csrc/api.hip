@@ -213,4 +213,17 @@ tg_status tg_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
                                         reinterpret_cast<hipStream_t>(stream)));
 }
 
+tg_status tg_tree_signals(const tg_tree *tree, const int32_t *frontier, const int32_t *n_frontier,
+                          int B, int F, int W, int lookback, const float *context,
+                          const float *params, float *signals, float *margin, int32_t *action,
+                          uint32_t *d_err, void *stream) {
+  if (!tree_ok(tree) || !frontier || !signals) return TG_ERR_INVALID_ARG;
+  if (B <= 0 || F < 1 || W < 1 || lookback < 0) return TG_ERR_INVALID_ARG;
+  if (params && (!context || !margin || !action)) return TG_ERR_INVALID_ARG;
+  if (tree->cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  return from_hip(tg::launch_signals(*tree, frontier, n_frontier, B, F, W, lookback, context,
+                                     params, signals, margin, action, d_err,
+                                     reinterpret_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

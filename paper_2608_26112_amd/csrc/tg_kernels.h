@@ -87,6 +87,12 @@ hipError_t launch_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix
                              int S_max, int D, int max_path, tg_dtype dtype,
                              int32_t *new_prefix_len, uint32_t *d_err, hipStream_t stream);
 
+// ------------------------------------------------------------- scheduler
+hipError_t launch_signals(const tg_tree &tree, const int32_t *frontier, const int32_t *n_frontier,
+                          int B, int F, int W, int lookback, const float *context,
+                          const float *params, float *signals, float *margin, int32_t *action,
+                          uint32_t *d_err, hipStream_t stream);
+
 // -------------------------------------------------------------- attention
 struct AttnShape {
   int B, N, Hq, Hkv, D, S_max;

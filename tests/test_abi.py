@@ -219,3 +219,21 @@ def test_prune_and_kv_compact_host_checks(lib):
     assert compact(D=96) == tg.ERR_UNSUPPORTED
     assert compact(dt=5) == tg.ERR_INVALID_ARG
     assert compact(maxp=-1) == tg.ERR_INVALID_ARG
+
+
+def test_signals_host_checks(lib):
+    import paper_2608_26112_amd as tg
+
+    def sig(tree=None, **kw):
+        a = dict(fr=P, nf=NULL, B=1, F=4, W=4, L=5, ctx=NULL, prm=NULL, out=P, mg=NULL, act=NULL)
+        a.update(kw)
+        t = _tree() if tree is None else tree
+        return lib.tg_tree_signals(ctypes.byref(t), a["fr"], a["nf"], a["B"], a["F"], a["W"],
+                                   a["L"], a["ctx"], a["prm"], a["out"], a["mg"], a["act"],
+                                   NULL, NULL)
+    assert sig(fr=NULL) == tg.ERR_INVALID_ARG
+    assert sig(out=NULL) == tg.ERR_INVALID_ARG
+    assert sig(W=0) == tg.ERR_INVALID_ARG
+    assert sig(L=-1) == tg.ERR_INVALID_ARG
+    assert sig(prm=P) == tg.ERR_INVALID_ARG          # context / margin / action missing
+    assert sig(tree=_tree(cap=5000)) == tg.ERR_UNSUPPORTED
