@@ -12,21 +12,26 @@ m = 8 children per node, 32/8 heads, head_dim 128, prefix 2048, bf16):
                                         reselect 10 graft points, +80 nodes
   k=4  small     tg_tree_expand_topk    expand Top_W of those 80
   k=5  middle    tg_tree_rescore_graft  pool = 160 nodes, rescore, +80 nodes
-  verify         tg_tree_verify_attention  one target layer over a 64-node
-                                        verify tree (root + 63 draft nodes)
-  accept         tg_tree_accept         greedy acceptance on the draft tree
+  prune          tg_tree_global_prune   the 312-node tree -> 64 nodes (Alg. 3)
+                                        + verification buffers
+  verify         tg_tree_verify_attention  one target layer over the pruned
+                                        tree (its parent array as is: -1 =
+                                        the prefix end, which holds the root)
+  accept         tg_tree_accept         greedy acceptance on the pruned tree
+  cache          tg_kv_compact          the accepted rows extend the prefix
 
 The schedule [1,0,1,0,1] is the paper's fixed ablation schedule (Sec. 5.3).
 Drafter and target logits, Q/K/V and tokens are seeded synthetic data of the
 workload's shapes and distributions (logits N(0,3) fp32; Q/K/V N(0,1)/sqrt(128)
-bf16).  Inputs rotate over several resident copies (> the 256 MB MALL) so no
+bf16; the target's greedy token at each pruned-tree node is its first child's
+token with p = 0.7, fixed once per input copy from the tree the turn builds).  Inputs rotate over several resident copies (> the 256 MB MALL) so no
 timed read is served from the last-level cache.
 
 The timed region replays one captured HIP graph per input copy (the whole
 step, so host launch overhead is not measured).  A second, eager pass over the
 same steps records every kernel's device time with the library's trace events
-(dispatch-level start/stop events on the launch stream); the dominant kernel's
-roofline comes from those.  The CPU baseline times the oracle (tests' CPU
+(an event pair on the launch stream around each kernel); the dominant
+kernel's roofline comes from those.  The CPU baseline times the oracle (tests' CPU
 reference) on the same inputs.
 
 Prints ONE JSON line.  N > 1 GPUs is not supported by this build.
@@ -53,8 +58,9 @@ ATTN_MAIN = ("attn_pingpong", "attn_mfma", "attn_f32")   # tree-verify attention
 # workload (Llama-3-8B-shaped turn)
 V, W_FR, M_CH = 128256, 10, 8
 SCHEDULE = (1, 0, 1, 0, 1)
-B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64
+B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64     # N_VER = B_ver pruned nodes
 CAP = 512
+MAX_DEPTH = 8            # accept path width (the turn's trees are at most 5 deep)
 R_ROWS = 313             # strong-logits rows (root + up to 312 nodes)
 
 
@@ -123,30 +129,22 @@ def make_inputs(c, dev):
     return dict(strong=strong, weak=weak, q=q, k=k, v=v)
 
 
-def make_trees(dev):
-    """Verify tree (root + 63 draft nodes shaped like a pruned top-8 /
-    frontier-10 expansion of depth 6) and the accept inputs on its draft nodes:
-    sibling-distinct tokens, target greedy agreeing with the first child with
-    p = 0.7 per level."""
-    import torch
+def greedy_for(tree_host):
+    """Synthetic target for the pruned tree of one input copy: at each node
+    (and at the prefix end) the target's greedy token is the first child's
+    token with p = 0.7 per level, else another token."""
     import workloads as W
-    g = W.rng(1002)
-    draft = W.expansion_shaped_tree(g, N_VER - 1, 6, 8, W_FR)
-    vpar = W.verify_layout_with_root(draft)
-    tok = W.distinct_sibling_tokens(g, draft, V)
-    greedy = W.greedy_match_first_child(g, draft, tok, V, 0.7)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
-    return dict(vparent=t(vpar[None]), plen=t([L]), dparent=t(draft[None]),
-                dtoken=t(tok[None]), dn=t([N_VER - 1]), greedy=t(greedy[None]),
-                host=dict(draft=draft, vpar=vpar, tok=tok, greedy=greedy))
+    par, tok = tree_host
+    g = W.rng([1002, 7, len(par)])
+    return W.greedy_match_first_child(g, par, tok, V, 0.7)
 
 
 class Step:
     """All buffers of one step on one input copy, so it can be captured."""
 
-    def __init__(self, tg, inp, trees, dev):
+    def __init__(self, tg, inp, dev):
         import torch
-        self.tg, self.inp, self.tr = tg, inp, trees
+        self.tg, self.inp = tg, inp
         i32 = dict(dtype=torch.int32, device=dev)
         self.tree = tg.TreeState(B, CAP, dev)
         # zero-filled once (the library's row counters start at zero)
@@ -162,9 +160,19 @@ class Step:
         self.e_lse = [torch.empty((B, W_FR), dtype=torch.float32, device=dev) for _ in range(2)]
         self.fr = [torch.empty((B, W_FR), **i32) for _ in range(5)]
         self.nn = [torch.empty((B,), **i32) for _ in range(5)]
+        M = N_VER + 1
+        self.pr = dict(kept=torch.empty((B, N_VER), **i32), vparent=torch.empty((B, N_VER), **i32),
+                       vtoken=torch.empty((B, N_VER), **i32),
+                       position_ids=torch.empty((B, M), **i32),
+                       mask=torch.empty((B, M, (M + 31) // 32), **i32),
+                       retrieval=torch.empty((B, M, MAX_DEPTH + 1), **i32),
+                       n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
+        self.plen = torch.full((B,), L, **i32)
+        self.new_plen = torch.empty((B,), **i32)
+        self.greedy = torch.zeros((B, N_VER + 1), **i32)
         self.out = torch.empty_like(inp["q"])
         self.A = torch.empty((B,), **i32)
-        self.path = torch.empty((B, 6), **i32)
+        self.path = torch.empty((B, MAX_DEPTH), **i32)
         self.bonus = torch.empty((B,), **i32)
 
     def run(self):
@@ -183,10 +191,13 @@ class Step:
                                row_lse=self.e_lse[small], next_frontier=self.fr[k],
                                n_next=self.nn[k], workspace=self.ws_e)
                 small += 1
-        tg.verify_attention(x["q"], x["k"], x["v"], self.tr["vparent"], self.tr["plen"],
-                            D ** -0.5, out=self.out, workspace=self.ws_v)
-        tg.accept(self.tr["dparent"], self.tr["dtoken"], self.tr["dn"], self.tr["greedy"], 6,
+        p = tg.global_prune(t, N_VER, MAX_DEPTH + 1, out=self.pr)
+        tg.verify_attention(x["q"], x["k"], x["v"], p["vparent"], self.plen, D ** -0.5,
+                            out=self.out, workspace=self.ws_v)
+        tg.accept(p["vparent"], p["vtoken"], p["n_keep"], self.greedy, MAX_DEPTH,
                   accept_len=self.A, accept_path=self.path, bonus=self.bonus)
+        tg.kv_compact(x["k"], x["v"], self.plen, self.path, self.A,
+                      new_prefix_len=self.new_plen)
 
 
 # ------------------------------------------------------------ accounting
@@ -226,7 +237,7 @@ def verify_work(vpar):
 
 # -------------------------------------------------------------- cpu leg
 
-def cpu_baseline(inp, trees, budget_s):
+def cpu_baseline(inp, greedy0, budget_s):
     """The oracle (the tests' CPU reference, untuned) running the same turn on
     input copy 0 until about `budget_s` seconds have been spent."""
     from oracle import attention as OA
@@ -241,7 +252,6 @@ def cpu_baseline(inp, trees, budget_s):
     q = inp["q"].float().cpu().numpy()
     k = inp["k"].float().cpu().numpy()
     v = inp["v"].float().cpu().numpy()
-    h = trees["host"]
     turns, t0 = 0, time.perf_counter()
     while True:
         t = OT.Tree.empty(B, CAP)
@@ -253,8 +263,13 @@ def cpu_baseline(inp, trees, budget_s):
             else:
                 t, _, fr, nn, _ = OT.expand(t, weak[small], fr, nn, M_CH, W_FR)
                 small += 1
-        OA.tree_verify_attention_fast(q, k, v, h["vpar"][None], [L], D ** -0.5)
-        OT.accept(h["draft"][None], h["tok"][None], np.array([N_VER - 1]), h["greedy"][None], 6)
+        n = int(t.n_nodes[0])
+        pr = OT.global_prune(t.parent[0, :n], t.cum[0, :n], n, N_VER)
+        par = pr["parent"][None]
+        tok = t.token[0, pr["kept"]][None]
+        OA.tree_verify_attention_fast(q, k, v, par, [L], D ** -0.5)
+        A, path, _, _ = OT.accept(par, tok, np.array([len(pr["kept"])]), greedy0, MAX_DEPTH)
+        OA.kv_compact(k, v, np.array([L]), path, A)
         turns += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
@@ -482,16 +497,25 @@ def main():
         tree_bench(args, tg, torch, dev)
         return
 
-    trees = make_trees(dev)
     inputs = [make_inputs(c, dev) for c in range(args.copies)]
-    steps = [Step(tg, inputs[c], trees, dev) for c in range(args.copies)]
+    steps = [Step(tg, inputs[c], dev) for c in range(args.copies)]
     torch.cuda.synchronize()
 
-    # correctness guard: the turn produces the structurally expected tree
-    steps[0].run()
+    # set-up (untimed): every copy's turn once; the structural guard, and the
+    # synthetic target's greedy tokens for the pruned tree each copy builds
+    pruned = []
+    for st in steps:
+        st.run()
+        torch.cuda.synchronize()
+        n_nodes = int(st.tree.n_nodes[0].item())
+        assert n_nodes == 8 + 64 + 80 + 80 + 80, n_nodes
+        assert int(st.pr["n_keep"][0].item()) == N_VER
+        par = st.pr["vparent"][0].cpu().numpy()
+        tok = st.pr["vtoken"][0].cpu().numpy()
+        st.greedy.copy_(torch.from_numpy(greedy_for((par, tok))[None]))
+        pruned.append((par, tok))
     torch.cuda.synchronize()
-    n_nodes = int(steps[0].tree.n_nodes[0].item())
-    assert n_nodes == 8 + 64 + 80 + 80 + 80, n_nodes
+    trees = dict(host=dict(pruned=pruned))
 
     # ---- graph capture: one graph per input copy
     graphs = []
@@ -563,8 +587,9 @@ def main():
     # ---- accounting
     rows_r, rows_e = rows_read_per_step()
     row_bytes = V * 4
-    vpar = trees["host"]["vpar"]
-    v_bytes, v_flops = verify_work(vpar)
+    works = [verify_work(par) for par, _ in trees["host"]["pruned"]]
+    v_bytes = sum(w[0] for w in works) / len(works)
+    v_flops = sum(w[1] for w in works) / len(works)
     step_bytes = (sum(rows_r) + sum(rows_e)) * row_bytes + v_bytes
     nodes = 8 + 64 + 80 + 80 + 80            # created per turn
     rescored = 72 + 160                       # non-root pool nodes rescored
@@ -611,7 +636,8 @@ def main():
         "step_timeline_us": timeline,
     }
     if not args.no_cpu_baseline:
-        turns, el, blas = cpu_baseline(inputs[0], trees, args.cpu_seconds)
+        turns, el, blas = cpu_baseline(inputs[0], steps[0].greedy.cpu().numpy(),
+                                       args.cpu_seconds)
         out["cpu_baseline"] = {"value": step_bytes * turns / el / 1e12, "unit": "TB/s",
                                "cores": blas, "kind": "oracle",
                                "sample": f"{turns} full turns of the same workload on input "

@@ -338,7 +338,7 @@ def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_pa
 
 
 def global_prune(tree: TreeState, B_ver: int, max_path: int | None = None, d_err=None,
-                 stream=None):
+                 stream=None, out=None):
     """Alg. 3 pruning of every tree to B_ver non-root nodes plus the
     verification buffers (see tg_tree_global_prune).  Returns a dict of device
     tensors: kept, vparent, vtoken [B, B_ver]; position_ids [B, B_ver+1];
@@ -349,11 +349,15 @@ def global_prune(tree: TreeState, B_ver: int, max_path: int | None = None, d_err
     M = B_ver + 1
     max_path = M if max_path is None else int(max_path)
     i32 = dict(dtype=torch.int32, device=dev)
-    out = dict(kept=torch.empty((B, B_ver), **i32), vparent=torch.empty((B, B_ver), **i32),
-               vtoken=torch.empty((B, B_ver), **i32), position_ids=torch.empty((B, M), **i32),
-               mask=torch.empty((B, M, (M + 31) // 32), dtype=torch.int32, device=dev),
-               retrieval=torch.empty((B, M, max_path), **i32),
-               n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
+    if out is None:
+        out = dict(kept=torch.empty((B, B_ver), **i32), vparent=torch.empty((B, B_ver), **i32),
+                   vtoken=torch.empty((B, B_ver), **i32),
+                   position_ids=torch.empty((B, M), **i32),
+                   mask=torch.empty((B, M, (M + 31) // 32), dtype=torch.int32, device=dev),
+                   retrieval=torch.empty((B, M, max_path), **i32),
+                   n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
+    elif tuple(out["retrieval"].shape) != (B, M, max_path):
+        raise ValueError("out['retrieval'] must be [B, B_ver + 1, max_path]")
     ts = tree.struct()
     st = lib.tg_tree_global_prune(ctypes.byref(ts), B, int(B_ver), max_path,
                                   *(_ptr(out[k]) for k in ("kept", "vparent", "vtoken",

@@ -164,12 +164,26 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     position_ids[pb + u] = u == 0 ? 0 : (u <= nk ? depth[order[u - 1]] : -1);
   // verify parent of row u (root row 0 has none)
   auto vpar = [&](int u) { return u == 0 ? -1 : (par[order[u - 1]] < 0 ? 0 : newid[par[order[u - 1]]]); };
-  // ancestor-or-self bitsets, one row per thread
+  // ancestor-or-self bitsets, one row per thread: verify indices decrease
+  // up the chain, so each word is complete when the walk leaves it and is
+  // written once (highest word first)
   for (int u = tid; u < M; u += kThreads) {
     uint32_t *row = mask + (pb + u) * W;
-    for (int w = 0; w < W; ++w) row[w] = 0;
-    if (u <= nk && n >= 0)
-      for (int a = u; a >= 0; a = vpar(a)) row[a >> 5] |= 1u << (a & 31);
+    uint32_t acc = 0;
+    int cw = W - 1;
+    if (u <= nk && n >= 0) {
+      for (int a = u; a >= 0; a = vpar(a)) {
+        for (; cw > (a >> 5); --cw) {
+          row[cw] = acc;
+          acc = 0;
+        }
+        acc |= 1u << (a & 31);
+      }
+    }
+    for (; cw >= 0; --cw) {
+      row[cw] = acc;
+      acc = 0;
+    }
   }
 
   // ---- leaves in verify order and their root-to-leaf paths
@@ -187,17 +201,26 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     ++mine;
     deep |= (u == 0 ? 0 : depth[order[u - 1]]) + 1 > max_path;
   }
-  cnt[tid] = mine;
+  // exclusive scan of the per-thread leaf counts: waves by shuffles, then
+  // the wave totals
+  int incl = mine;
+  const int lane = tid & (kWave - 1), wv = tid / kWave;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) cnt[wv] = incl;
   if (deep) deep_s = 1;
   __syncthreads();
+  int before = 0, total = 0;
+  for (int i = 0; i < kThreads / kWave; ++i) {
+    before += i < wv ? cnt[i] : 0;
+    total += cnt[i];
+  }
+  const int first_rank = before + incl - mine;
   if (tid == 0) {
-    int t = 0;
-    for (int i = 0; i < kThreads; ++i) {
-      const int x = cnt[i];
-      cnt[i] = t;
-      t += x;
-    }
-    nl_s = t;
+    nl_s = total;
     if (deep_s) report(d_err, TG_DERR_CAPACITY);
   }
   __syncthreads();
@@ -206,7 +229,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   for (size_t i = tid; i < (size_t)M * max_path; i += kThreads) retrieval[rb + i] = -1;
   __syncthreads();
   if (write_paths) {
-    int r = cnt[tid];
+    int r = first_rank;
     for (int u = lo; u < hi; ++u) {
       if (!flag[u]) continue;
       int32_t *row = retrieval + rb + (size_t)r * max_path;
