@@ -3,11 +3,14 @@
 //
 // prune_kernel: one workgroup per tree, everything in LDS (n <= 4096):
 //   depths by pointer jumping over the parent links (log2 n rounds);
-//   rank: bitonic sort of the node keys (cum desc, depth asc, id asc);
+//   rank: exact rank of each node key (cum desc, depth asc, id asc) by
+//         counting the larger keys (keys are distinct), a bitonic sort past
+//         1024 nodes;
 //   keep: when every parent ranks before its children the kept set is the
 //         first B_ver ranked nodes (one parallel check); otherwise one thread
 //         runs the literal loop (chains added while they fit);
-//   re-index: second bitonic sort of the kept nodes by (depth, id);
+//   re-index: the kept nodes, compacted by a block scan, ranked the same way
+//         by (depth, id);
 //   buffers: parents, tokens, depths, ancestor bitsets, root-to-leaf paths.
 // kv_compact_kernel: one workgroup per (sequence, KV head); every thread
 // copies its 16-byte column of the accepted rows in path order, which is
@@ -22,13 +25,38 @@ namespace {
 
 constexpr int kThreads = 256;
 
+constexpr int kRankCountMax = kRankPerThread * kThreads;  // rank by counting up to here
+
+// Exclusive prefix of one int per thread in thread order (waves by shuffles,
+// then the wave totals); `slots` holds kThreads / kWave ints.  Ends
+// synchronised.
+__device__ int block_exclusive_scan(int v, int *slots, int &total) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) slots[wv] = incl;
+  __syncthreads();
+  int before = 0;
+  total = 0;
+  for (int i = 0; i < kThreads / kWave; ++i) {
+    before += i < wv ? slots[i] : 0;
+    total += slots[i];
+  }
+  __syncthreads();
+  return before + incl - v;
+}
+
 __global__ __launch_bounds__(kThreads) void prune_kernel(
     tg_tree tree, int B_ver, int max_path, int32_t *__restrict__ kept,
     int32_t *__restrict__ vparent, int32_t *__restrict__ vtoken,
     int32_t *__restrict__ position_ids, uint32_t *__restrict__ mask,
     int32_t *__restrict__ retrieval, int32_t *__restrict__ n_keep,
     int32_t *__restrict__ n_leaves, uint32_t *d_err) {
-  __shared__ uint64_t key[TG_MAX_CAP];
+  __shared__ __align__(16) uint64_t key[TG_MAX_CAP];
   __shared__ int16_t par[TG_MAX_CAP];
   __shared__ int16_t anc[2][TG_MAX_CAP];
   __shared__ int16_t dep[2][TG_MAX_CAP];
@@ -81,36 +109,51 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   }
   const int16_t *depth = dep[cur];
 
-  // ---- rank by (cum desc, depth asc, id asc)
+  // ---- rank by (cum desc, depth asc, id asc): exact ranks by counting
+  // (keys are distinct) for up to kRankCountMax nodes, else a bitonic sort
+  int16_t *rank = anc[cur ^ 1];  // free now
   const int P2 = pow2_at_least(nn > 0 ? nn : 1);
   for (int i = tid; i < P2; i += kThreads)
     key[i] = i < nn ? node_key(tree.cum[base + i], depth[i], i) : 0;
   __syncthreads();
-  block_bitonic_desc(key, P2);
-
-  // ---- keep
+  if (nn <= kRankCountMax) {
+    uint64_t mk[kRankPerThread];
+    int r[kRankPerThread];
+    count_larger<kThreads>(key, nn, mk, r);
+#pragma unroll
+    for (int j = 0; j < kRankPerThread; ++j)
+      if (tid + j * kThreads < nn) rank[tid + j * kThreads] = (int16_t)r[j];
+    __syncthreads();
+    for (int v = tid; v < nn; v += kThreads) order[rank[v]] = (int16_t)v;  // ranked ids
+  } else {
+    block_bitonic_desc(key, P2);
+    for (int i = tid; i < nn; i += kThreads) {
+      const int v = node_key_id(key[i]);
+      rank[v] = (int16_t)i;
+      order[i] = (int16_t)v;
+    }
+  }
   for (int v = tid; v < nn; v += kThreads) flag[v] = 0;
   __syncthreads();
-  int16_t *rank = anc[cur ^ 1];  // free now
+
+  // ---- keep
   if (nn <= B_ver) {
     for (int v = tid; v < nn; v += kThreads) flag[v] = 1;
   } else {
-    for (int i = tid; i < nn; i += kThreads) rank[node_key_id(key[i])] = (int16_t)i;
-    __syncthreads();
     bool viol = false;
     for (int v = tid; v < nn; v += kThreads) viol |= par[v] >= 0 && rank[par[v]] > rank[v];
     if (viol) viol_s = 1;
     __syncthreads();
     if (!viol_s) {
-      for (int i = tid; i < B_ver; i += kThreads) flag[node_key_id(key[i])] = 1;
+      for (int v = tid; v < nn; v += kThreads) flag[v] = rank[v] < B_ver;
     } else if (tid == 0) {
       // the literal loop: add each ranked node's missing ancestor chain if it fits
       int size = 1;
       for (int i = 0; i < nn && size < M; ++i) {
         int len = 0;
-        for (int u = node_key_id(key[i]); u >= 0 && !flag[u]; u = par[u]) ++len;
+        for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) ++len;
         if (size + len <= M) {
-          for (int u = node_key_id(key[i]); u >= 0 && !flag[u]; u = par[u]) flag[u] = 1;
+          for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) flag[u] = 1;
           size += len;
         }
       }
@@ -118,29 +161,42 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   }
   __syncthreads();
 
-  // ---- re-index the kept nodes by (depth, id): descending sort of the
-  // complemented keys puts them first, in ascending (depth, id)
-  for (int i = tid; i < P2; i += kThreads)
-    key[i] = (i < nn && flag[i]) ? ~(((uint64_t)depth[i] << 32) | (uint64_t)i) : 0;
-  __syncthreads();
-  block_bitonic_desc(key, P2);
-  int c = 0;
-  for (int i = tid; i < P2; i += kThreads) c += key[i] != 0;
-  c = wave_sum_i32(c);
-  if ((tid & (kWave - 1)) == 0) cnt[tid / kWave] = c;
+  // ---- re-index the kept nodes by (depth, id): compact them (id order),
+  // then rank the compacted keys
+  const int per_c = (nn + kThreads - 1) / kThreads;
+  const int c_lo = min(nn, tid * per_c), c_hi = min(nn, c_lo + per_c);
+  int mine_k = 0;
+  for (int v = c_lo; v < c_hi; ++v) mine_k += flag[v];
+  int nk_total = 0;
+  int pos = block_exclusive_scan(mine_k, cnt, nk_total);
+  for (int v = c_lo; v < c_hi; ++v)
+    if (flag[v]) key[pos++] = ~(((uint64_t)depth[v] << 32) | (uint64_t)v);
   for (int v = tid; v < nn; v += kThreads) newid[v] = 0;
-  __syncthreads();
-  if (tid == 0) {
-    int t = 0;
-    for (int i = 0; i < kThreads / kWave; ++i) t += cnt[i];
-    nk_s = t;
-  }
+  if (tid == 0) nk_s = nk_total;
   __syncthreads();
   const int nk = nk_s;
-  for (int j = tid; j < nk; j += kThreads) {
-    const int v = (int)(uint32_t)~key[j];
-    order[j] = (int16_t)v;
-    newid[v] = (int16_t)(j + 1);
+  if (nk <= kRankCountMax) {
+    uint64_t mk[kRankPerThread];
+    int r[kRankPerThread];
+    count_larger<kThreads>(key, nk, mk, r);
+#pragma unroll
+    for (int j = 0; j < kRankPerThread; ++j) {
+      const int i = tid + j * kThreads;
+      if (i >= nk) continue;
+      const int v = (int)(uint32_t)~mk[j];
+      order[r[j]] = (int16_t)v;
+      newid[v] = (int16_t)(r[j] + 1);
+    }
+  } else {
+    const int P2k = pow2_at_least(nk);
+    for (int i = nk + tid; i < P2k; i += kThreads) key[i] = 0;
+    __syncthreads();
+    block_bitonic_desc(key, P2k);
+    for (int j = tid; j < nk; j += kThreads) {
+      const int v = (int)(uint32_t)~key[j];
+      order[j] = (int16_t)v;
+      newid[v] = (int16_t)(j + 1);
+    }
   }
   __syncthreads();
 
@@ -201,24 +257,9 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     ++mine;
     deep |= (u == 0 ? 0 : depth[order[u - 1]]) + 1 > max_path;
   }
-  // exclusive scan of the per-thread leaf counts: waves by shuffles, then
-  // the wave totals
-  int incl = mine;
-  const int lane = tid & (kWave - 1), wv = tid / kWave;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
-  if (lane == kWave - 1) cnt[wv] = incl;
   if (deep) deep_s = 1;
-  __syncthreads();
-  int before = 0, total = 0;
-  for (int i = 0; i < kThreads / kWave; ++i) {
-    before += i < wv ? cnt[i] : 0;
-    total += cnt[i];
-  }
-  const int first_rank = before + incl - mine;
+  int total = 0;
+  const int first_rank = block_exclusive_scan(mine, cnt, total);
   if (tid == 0) {
     nl_s = total;
     if (deep_s) report(d_err, TG_DERR_CAPACITY);

@@ -4,8 +4,8 @@
 //
 // One workgroup per tree, all in LDS: child counts, the frontier's depth set
 // D_F and its lookback closure D_C as bitsets over depth, the candidate set R
-// (root included) as node keys, a bitonic sort for the preview Top_W(R, s),
-// block reductions for the ten signals, then the 3,265-parameter MLP with one
+// (root included) as node keys, ranked by counting (a sort past 1024 keys)
+// for the preview Top_W(R, s), block reductions for the ten signals, then the 3,265-parameter MLP with one
 // thread per hidden unit (fp32, fixed summation order).
 #include "tg_device.h"
 #include "tg_kernels.h"
@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
     key[i] = k;
   }
   __syncthreads();
-  block_bitonic_desc(key, P2);
+  block_top_keys<kThreads>(key, n + 1, P2, W);
 
   // ---- frontier sums: depth, leaves, max depth, finite scores
   float fs[4] = {0.0f, 0.0f, 0.0f, 0.0f};

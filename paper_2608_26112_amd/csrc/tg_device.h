@@ -116,6 +116,61 @@ __device__ inline void block_bitonic_desc(uint64_t *a, int n) {
   }
 }
 
+// ---------------------------------------------------- ranks by counting
+// A key's exact rank among a small set is the number of larger keys: one pass
+// over LDS broadcasts with no barrier, where a bitonic sort of the same set
+// pays a barrier per stage.  Distinct keys get distinct ranks.
+constexpr int kRankPerThread = 4;  // keys a thread ranks (sets up to 4 * block)
+
+// r[j] = how many of key[0..n) are larger than mk[j] = key[threadIdx.x +
+// j * kBlock] (~0, ranking nothing, past n).  n <= kRankPerThread * kBlock.
+template <int kBlock>
+__device__ __forceinline__ void count_larger(const uint64_t *key, int n,
+                                             uint64_t (&mk)[kRankPerThread],
+                                             int (&r)[kRankPerThread]) {
+#pragma unroll
+  for (int j = 0; j < kRankPerThread; ++j) {
+    const int i = threadIdx.x + j * kBlock;
+    mk[j] = i < n ? key[i] : ~0ull;
+    r[j] = 0;
+  }
+  int u = 0;
+#pragma unroll 4
+  for (; u + 1 < n; u += 2) {
+    const uint64_t a = key[u], c = key[u + 1];
+#pragma unroll
+    for (int j = 0; j < kRankPerThread; ++j) r[j] += (int)(a > mk[j]) + (int)(c > mk[j]);
+  }
+  if (u < n) {
+    const uint64_t a = key[u];
+#pragma unroll
+    for (int j = 0; j < kRankPerThread; ++j) r[j] += (int)(a > mk[j]);
+  }
+}
+
+// Moves the k largest of key[0..n) (distinct; 0 = no key) to key[0..k), best
+// first, 0 in the places past the last present key; what lies past
+// min(k, n) is undefined afterwards.  Sets larger than kRankPerThread * kBlock
+// are sorted whole: then key[n..P2) must hold 0, P2 a power of two >= n.
+// Callers synchronise before; ends synchronised.
+template <int kBlock>
+__device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
+  if (n > kRankPerThread * kBlock) {
+    block_bitonic_desc(key, P2);
+    return;
+  }
+  uint64_t mk[kRankPerThread];
+  int r[kRankPerThread];
+  count_larger<kBlock>(key, n, mk, r);
+  __syncthreads();
+  for (int j = threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kRankPerThread; ++j)
+    if (threadIdx.x + j * kBlock < n && mk[j] != 0 && r[j] < k) key[r[j]] = mk[j];
+  __syncthreads();
+}
+
 __host__ __device__ constexpr int pow2_at_least(int n) {
   int p = 1;
   while (p < n) p <<= 1;

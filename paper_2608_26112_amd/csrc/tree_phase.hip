@@ -6,8 +6,9 @@
 // into its log-sum-exp and top-K list, then the tree is edited in place:
 // children appended (expand), pool rescored, graft positions reselected and
 // new children grafted without touching existing nodes (rescore_graft).
-// Node selection (Top_W) is a bitonic sort of 64-bit keys in LDS ordered by
-// (cum desc, depth asc, id asc).
+// Node selection (Top_W) ranks 64-bit keys in LDS ordered by (cum desc,
+// depth asc, id asc): by counting the larger keys, or a bitonic sort past
+// 1024 keys.
 #include <algorithm>
 
 #include "tg_device.h"
@@ -170,8 +171,8 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
     skey[c] = node_key(cum, dv + 1, id);
   }
   __syncthreads();
-  block_bitonic_desc(skey, P2);
   const int nn = min(N, total);
+  block_top_keys<kThreads>(skey, total, P2, nn);
   for (int j = tid; j < N; j += kThreads)
     next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
   if (tid == 0) {
@@ -337,7 +338,7 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     skey[i] = k;
   }
   __syncthreads();
-  block_bitonic_desc(skey, P2);
+  block_top_keys<kThreads>(skey, nb + 1, P2, nF);
 
   // ---- P <- P u C; write back rescored path scores (before the graft,
   // whose staging reuses the per-node scratch)
@@ -393,8 +394,8 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
       skey[c] = k;
     }
     __syncthreads();
-    block_bitonic_desc(skey, P2c);
     const int nn = min(N, total);
+    block_top_keys<kThreads>(skey, total, P2c, nn);
     for (int j = tid; j < N; j += kThreads)
       next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
     if (tid == 0) n_next[b] = nn;

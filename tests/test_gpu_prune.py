@@ -144,6 +144,21 @@ def test_prune_full_capacity_chain_and_path_limit(tg):
     assert got["n_keep"][0] == 63 and list(got["kept"][0, :63]) == list(range(63))
 
 
+def test_prune_large_budget_sorts(tg):
+    """Budgets and trees past 1024 nodes take the sorting paths for both the
+    rank and the re-index (a 4096-node random tree, 1500 kept)."""
+    cap = 4096
+    t = OT.Tree.empty(1, cap)
+    g = W.rng(531)
+    t.parent[0, :cap] = W.uniform_parents(g, cap)
+    t.cum[0, :cap] = -np.abs(W.normal(g, (cap,), 1.0))
+    t.token[0, :cap] = np.arange(cap, dtype=np.int32) * 7 % 32000
+    t.n_nodes[0] = cap
+    got, err = run_prune(tg, t, 1500, 64)
+    assert err == 0
+    check_tree(got, t, 0, 1500, 64)
+
+
 def test_prune_bad_tree_and_parent(tg):
     t = OT.Tree.empty(2, 8)
     t.parent[0, :3] = [-1, 5, 0]     # node 1's parent is not earlier: read as the root
