@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
     const __bf16 *__restrict__ vc, const int32_t *__restrict__ parent,
     const int32_t *__restrict__ prefix_len, __bf16 *__restrict__ out,
-    float *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
+    __bf16 *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
     int Hq, int Hkv, int S_max, float scale2, int n_tiles, int n_splits,
     uint32_t *d_err) {
   using Lds = AttnLds<D>;
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   __shared__ __attribute__((aligned(16))) __bf16 stage0[Lds::STAGE];
   __shared__ __attribute__((aligned(16))) __bf16 stage1[Lds::STAGE];
   extern __shared__ __attribute__((aligned(16))) uint32_t anc_s[];
-  int *par_s = reinterpret_cast<int *>(stage0);  // prologue only
+  int *par_s = reinterpret_cast<int *>(stage1);  // prologue only
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
@@ -140,51 +140,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     return;
   }
 
-  // ---- parents and ancestor-or-self bitsets of this tile's nodes (a1)
-  const int node_lo = row0 / G;
-  const int node_hi = min(N, (row0 + BM - 1) / G + 1);
-  const int nloc = node_hi - node_lo;
-  const int NW = (N + 31) >> 5;
-  bool badp = false;
-  for (int i = tid; i < N; i += kThreads) {
-    int p = parent[(size_t)b * N + i];
-    if (p < -1 || p >= i) {
-      badp = true;
-      p = -1;
-    }
-    par_s[i] = p;
-  }
-  if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
-  for (int i = tid; i < nloc * NW; i += kThreads) anc_s[i] = 0;
-  __syncthreads();
-  if (tid < nloc) {
-    uint32_t *row = anc_s + tid * NW;
-    for (int u = node_lo + tid; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
-  }
-  __syncthreads();  // bitsets ready; par_s (stage 0) free again
-
-  // ---- this lane's query row, Q fragment in registers
-  const int qrow = row0 + w * 32 + r32;
-  const bool qvalid = qrow < rows_total;
-  const int qnode = qvalid ? qrow / G : node_lo;
-  const int qhead = g * G + (qvalid ? qrow % G : 0);
-  const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
-  bf16x8 qf[KS];
-  {
-    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
-#pragma unroll
-    for (int s = 0; s < KS; ++s)
-      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
-  }
-
-  // ---- key ranges: this split's share of the prefix, then (last split) tree
-  int chunk = (L + n_splits - 1) / n_splits;
-  chunk = ((chunk + BN - 1) / BN) * BN;
-  const int p_beg = min(L, split * chunk);
-  const int p_end = min(L, p_beg + chunk);
-  const bool do_tree = split == n_splits - 1;
-  const int n_ptiles = (p_end - p_beg + BN - 1) / BN;
-  const int n_tiles_all = n_ptiles + (do_tree ? (N + BN - 1) / BN : 0);
+  // ---- key tiles: the prefix's 64-key tiles, then the tree's, dealt out to
+  // the splits as equal runs (the tree's tiles weigh like any other)
+  const int n_pt = (L + BN - 1) / BN;
+  const int n_vt = n_pt + (N + BN - 1) / BN;
+  const int per_split = (n_vt + n_splits - 1) / n_splits;
+  const int vt0 = min(n_vt, split * per_split);
+  const int n_tiles_all = min(n_vt, vt0 + per_split) - vt0;
 
   const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
   const __bf16 *kb = kc + kv_base;
@@ -196,8 +158,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   float m = -__builtin_inff();  // running max, scaled log2 units
   float l = 0.0f;               // this lane's share of the running sum
 
-  auto tile_k0 = [&](int t) { return t >= n_ptiles ? L + (t - n_ptiles) * BN : p_beg + t * BN; };
-  auto tile_lim = [&](int t) { return t >= n_ptiles ? L + N : p_end; };
+  auto tree_tile_at = [&](int t) { return vt0 + t >= n_pt; };
+  auto tile_k0 = [&](int t) { return tree_tile_at(t) ? L + (vt0 + t - n_pt) * BN : (vt0 + t) * BN; };
+  auto tile_lim = [&](int t) { return tree_tile_at(t) ? L + N : L; };
   // Direct global -> LDS loads.  Instruction i of wave w fills the 1 KB
   // block j = w * LOADS + i of a tile: rows j * RPI .. + RPI - 1, and lane l
   // writes physical chunk l % CPR of its row, i.e. loads logical chunk
@@ -238,7 +201,46 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     }
   };
 
+  // tile 0 streams in while the prologue runs
   if (n_tiles_all > 0) issue(0, stage0);
+
+  // ---- parents and ancestor-or-self bitsets of this tile's nodes (a1)
+  const int node_lo = row0 / G;
+  const int node_hi = min(N, (row0 + BM - 1) / G + 1);
+  const int nloc = node_hi - node_lo;
+  const int NW = (N + 31) >> 5;
+  bool badp = false;
+  for (int i = tid; i < N; i += kThreads) {
+    int p = parent[(size_t)b * N + i];
+    if (p < -1 || p >= i) {
+      badp = true;
+      p = -1;
+    }
+    par_s[i] = p;
+  }
+  if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
+  for (int i = tid; i < nloc * NW; i += kThreads) anc_s[i] = 0;
+  __syncthreads();
+  if (tid < nloc) {
+    uint32_t *row = anc_s + tid * NW;
+    for (int u = node_lo + tid; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
+  }
+  __syncthreads();  // bitsets ready; par_s (stage 1) free again
+
+  // ---- this lane's query row, Q fragment in registers
+  const int qrow = row0 + w * 32 + r32;
+  const bool qvalid = qrow < rows_total;
+  const int qnode = qvalid ? qrow / G : node_lo;
+  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
+  bf16x8 qf[KS];
+  {
+    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+  }
+
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
@@ -246,7 +248,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *Kt = cur;
     const __bf16 *Vt = cur + Lds::TILE;
     if (t + 1 < n_tiles_all) issue(t + 1, nxt);  // lands in LDS while tile t computes
-    const bool tree_tile = t >= n_ptiles;
+    const bool tree_tile = tree_tile_at(t);
     const int k0 = tile_k0(t);
     const int k_lim = tile_lim(t);
 
@@ -396,15 +398,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     }
   } else {
     const size_t prow = (((size_t)split * B + b) * N + qnode) * Hq + qhead;
-    float *op = part_o + prow * D;
+    __bf16 *op = part_o + prow * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int d = db * 32 + 8 * j + 4 * h;
-        *reinterpret_cast<f32x4 *>(op + d) =
-            f32x4{o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                  o[db][4 * j + 3] * inv};
+        *reinterpret_cast<bf16x4 *>(op + d) =
+            bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
+                   (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
       }
     }
     if (h == 0) part_lse[prow] = lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
@@ -430,7 +432,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
     const __bf16 *__restrict__ vc, const int32_t *__restrict__ parent,
     const int32_t *__restrict__ prefix_len, __bf16 *__restrict__ out,
-    float *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
+    __bf16 *__restrict__ part_o, float *__restrict__ part_lse, int B, int N,
     int Hq, int Hkv, int S_max, float scale2, int n_tiles, int n_splits,
     uint32_t *d_err) {
   using Lds = AttnLds<D>;
@@ -529,13 +531,12 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
   }
 
-  int chunk = (L + n_splits - 1) / n_splits;
-  chunk = ((chunk + BN - 1) / BN) * BN;
-  const int p_beg = min(L, split * chunk);
-  const int p_end = min(L, p_beg + chunk);
-  const bool do_tree = split == n_splits - 1;
-  const int n_ptiles = (p_end - p_beg + BN - 1) / BN;
-  const int n = n_ptiles + (do_tree ? (N + BN - 1) / BN : 0);
+  // key tiles: the prefix's, then the tree's, dealt out as equal runs
+  const int n_pt = (L + BN - 1) / BN;
+  const int n_vt = n_pt + (N + BN - 1) / BN;
+  const int per_split = (n_vt + n_splits - 1) / n_splits;
+  const int vt0 = min(n_vt, split * per_split);
+  const int n = min(n_vt, vt0 + per_split) - vt0;
 
   const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
   const __bf16 *kb = kc + kv_base;
@@ -555,8 +556,9 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   f32x16 acc[2];
   bf16x8 pb[2][2];
 
-  auto tile_k0 = [&](int t) { return t >= n_ptiles ? L + (t - n_ptiles) * BN : p_beg + t * BN; };
-  auto tile_lim = [&](int t) { return t >= n_ptiles ? L + N : p_end; };
+  auto tree_tile_at = [&](int t) { return vt0 + t >= n_pt; };
+  auto tile_k0 = [&](int t) { return tree_tile_at(t) ? L + (vt0 + t - n_pt) * BN : (vt0 + t) * BN; };
+  auto tile_lim = [&](int t) { return tree_tile_at(t) ? L + N : L; };
   constexpr int RPI = 64 / Lds::CPR;
   // offsets recomputed per issue (a few VALU ops) rather than held in registers
   auto issue = [&](const __bf16 *src, int t, __bf16 *dst) __attribute__((always_inline)) {
@@ -653,7 +655,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
 
   // vector phase: softmax of tile t's scores (acc) into pb, m, l, o scale
   auto sphase = [&](int t) __attribute__((always_inline)) {
-    const bool tree_tile = t >= n_ptiles;
+    const bool tree_tile = tree_tile_at(t);
     const int k0 = tile_k0(t);
     const int k_lim = tile_lim(t);
     if (tree_tile || k0 + BN > k_lim) {
@@ -790,15 +792,15 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
   } else {
     const size_t prow = (((size_t)split * B + b) * N + qnode) * Hq + qhead;
-    float *op = part_o + prow * D;
+    __bf16 *op = part_o + prow * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int d = db * 32 + 8 * j + 4 * h;
-        *reinterpret_cast<f32x4 *>(op + d) =
-            f32x4{o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                  o[db][4 * j + 3] * inv};
+        *reinterpret_cast<bf16x4 *>(op + d) =
+            bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
+                   (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
       }
     }
     if (h == 0) part_lse[prow] = lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
@@ -806,11 +808,17 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
 }
 
 // Merge split partials: out = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M).
+// One wave per query row: lane s holds split s's log-sum-exp (n_splits <=
+// 64), read back wave-uniform; the bf16 partial rows are loaded eight splits
+// at a time with no branch in between (an empty split has weight 0 and a
+// zero row), so a round's loads are in flight together.
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
-    const float *__restrict__ part_o, const float *__restrict__ part_lse,
+    const __bf16 *__restrict__ part_o, const float *__restrict__ part_lse,
     const int32_t *__restrict__ prefix_len, __bf16 *__restrict__ out, int B,
     int N, int Hq, int S_max, int n_splits) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  constexpr int E = D / 64;  // elements per lane
   const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int rows = B * N * Hq;
@@ -821,22 +829,45 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     for (int d = lane; d < D; d += 64) op[d] = (__bf16)0.0f;
     return;
   }
+  const float ls = lane < n_splits ? part_lse[(size_t)lane * rows + gw] : -__builtin_inff();
+  auto lse_of = [&](int sp) {  // split sp's log-sum-exp, wave-uniform
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ls), sp & 63));
+  };
   float M = -__builtin_inff();
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, part_lse[(size_t)s * rows + gw]);
-  float acc[D / 64] = {};
+  for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, lse_of(sp));
+  float acc[E] = {};
   float den = 0.0f;
-  for (int s = 0; s < n_splits; ++s) {
-    float ls = part_lse[(size_t)s * rows + gw];
-    if (ls == -__builtin_inff()) continue;
-    float wgt = exp2f(ls - M);
-    den += wgt;
-    const float *po = part_o + ((size_t)s * rows + gw) * D;
+  const __bf16 *po = part_o + (size_t)gw * D + E * lane;
+  const size_t sstride = (size_t)rows * D;
+  // eight splits per round, loads first (indices clamped, weights 0 past the end)
+  for (int s0 = 0; s0 < n_splits; s0 += 8) {
+    float v[8][E];
 #pragma unroll
-    for (int e = 0; e < D / 64; ++e) acc[e] += wgt * po[lane + 64 * e];
+    for (int i = 0; i < 8; ++i) {
+      const __bf16 *pi = po + (size_t)min(s0 + i, n_splits - 1) * sstride;
+      if constexpr (E == 2) {
+        const bf16x2 x = *reinterpret_cast<const bf16x2 *>(pi);
+        v[i][0] = (float)x[0];
+        v[i][1] = (float)x[1];
+      } else {
+        v[i][0] = (float)pi[0];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float lsi = lse_of(s0 + i);
+      const float w = (s0 + i < n_splits && lsi != -__builtin_inff()) ? exp2f(lsi - M) : 0.0f;
+      den += w;
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(w, v[i][e], acc[e]);
+    }
   }
   const float inv = den > 0.0f ? 1.0f / den : 0.0f;
-#pragma unroll
-  for (int e = 0; e < D / 64; ++e) op[lane + 64 * e] = (__bf16)(acc[e] * inv);
+  if constexpr (E == 2) {
+    *reinterpret_cast<bf16x2 *>(op + 2 * lane) = bf16x2{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv)};
+  } else {
+    op[lane] = (__bf16)(acc[0] * inv);
+  }
 }
 
 // ------------------------------------------------------------------- fp32
@@ -947,7 +978,8 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
 // Kernel choice and prefix splits of a bf16 shape.  Long prefixes over at
 // least 256 query rows per KV head take the ping-pong kernel (one 8-wave
 // workgroup per CU); the rest the 4-wave kernel (two per CU).  Splits bring
-// the grid to about one (ping-pong) or two (4-wave) workgroups per CU.
+// the grid to about one (ping-pong) or two (4-wave) workgroups per CU; each
+// split takes a run of at least 16 (ping-pong) or 2 (4-wave) key tiles.
 struct AttnPlan {
   bool pingpong;
   int tiles;
@@ -962,14 +994,15 @@ static AttnPlan attn_plan(const AttnShape &s) {
   const int tiles = (rows + bm - 1) / bm;
   const long long base = (long long)s.B * s.Hkv * tiles;
   const long long want_wgs = pp ? 256 : 512;
+  // key tiles of the longest sequence, dealt out in runs of `per` tiles
+  const int n_vt = (max_prefix + BN - 1) / BN + (s.N + BN - 1) / BN;
   int sp = 1;
   if (base < want_wgs) {
-    const int by_len = std::max(1, max_prefix / (pp ? 1024 : 512));  // keys per split
-    long long x = (want_wgs + base - 1) / base;
-    x = std::min<long long>(std::min<long long>(x, by_len), 64);
-    sp = (int)std::max<long long>(x, 1);
+    const long long min_per = pp ? 16 : 2;
+    const long long per = std::max(min_per, (n_vt * base + want_wgs - 1) / want_wgs);
+    sp = (int)std::min<long long>(64, (n_vt + per - 1) / per);
   }
-  return AttnPlan{pp, tiles, sp};
+  return AttnPlan{pp, tiles, std::max(sp, 1)};
 }
 
 int attn_splits(const AttnShape &s) { return attn_plan(s).splits; }
@@ -979,7 +1012,8 @@ size_t attn_workspace_bytes(const AttnShape &s, tg_dtype dtype) {
   const int sp = attn_splits(s);
   if (sp <= 1) return 0;
   const size_t rows = (size_t)s.B * s.N * s.Hq;
-  return (size_t)sp * rows * (s.D + 1) * sizeof(float) + 256;
+  // bf16 partial rows, then fp32 log-sum-exps
+  return (size_t)sp * rows * s.D * sizeof(__bf16) + (size_t)sp * rows * sizeof(float) + 256;
 }
 
 hipError_t launch_attn_f32(const AttnShape &s, const float *q, const float *k,
@@ -1007,8 +1041,9 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   const int tiles = plan.tiles;
   const int sp = plan.splits;
   const size_t rows = (size_t)s.B * s.N * s.Hq;
-  float *part_o = sp > 1 ? reinterpret_cast<float *>(workspace) : nullptr;
-  float *part_lse = sp > 1 ? part_o + (size_t)sp * rows * s.D : nullptr;
+  __bf16 *part_o = sp > 1 ? reinterpret_cast<__bf16 *>(workspace) : nullptr;
+  float *part_lse =
+      sp > 1 ? reinterpret_cast<float *>(part_o + (size_t)sp * rows * s.D) : nullptr;
   const long long grid = (long long)s.B * s.Hkv * sp * tiles;
   const float scale2 = s.sm_scale * kLog2e;
   auto qb = reinterpret_cast<const __bf16 *>(q);
