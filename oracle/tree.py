@@ -44,6 +44,12 @@ DERR_BAD_NODE = 16
 
 NO_NODE = -2  # padding for frontier outputs (-1 is the root)
 
+# Variant flags of the middle step (the two ablations of Sec. 4.4 and a
+# duplicate-sibling filter); 0 = TreeGraft as described in Sec. 3.2.
+POOL_NEWONLY = 1    # w/o EG: the pool is the previous step's new nodes
+GRAFT_OVERWRITE = 2  # w/o ND: grafting replaces the frontier nodes' subtrees
+GRAFT_DEDUP = 4      # a child whose token an existing sibling has is skipped
+
 
 @dataclass
 class Tree:
@@ -180,29 +186,67 @@ def expand(tree: Tree, logits: np.ndarray, frontier: np.ndarray,
 
 # ------------------------------------------------------------ rescore + graft
 
-def pool_of(tree: Tree, b: int):
-    """Middle-drafter candidate pool C = V(T) minus P (Sec. 3.2): unvisited ids,
-    plus the root (-1) while the root is unvisited."""
+def pool_of(tree: Tree, b: int, flags: int = 0, new_from=None):
+    """Middle-drafter candidate pool (Sec. 3.2): C = V(T) minus P, i.e. the
+    unvisited ids plus the root (-1) while the root is unvisited.  With
+    POOL_NEWONLY (the w/o EG ablation, Sec. 4.4) C = N_k instead: the ids
+    new_from[b] .. n_b - 1 made by the previous step, the root when
+    new_from[b] == -1 (the first step, whose tree is the root alone)."""
     nb = int(tree.n_nodes[b])
+    if flags & POOL_NEWONLY:
+        lo = int(new_from[b])
+        return list(range(max(lo, -1), nb))
     C = [v for v in range(nb) if not tree.visited[b, v]]
     if not tree.root_visited[b]:
         C = [-1] + C
     return C
 
 
-def needed_rows(tree: Tree, b: int):
+def needed_rows(tree: Tree, b: int, flags: int = 0, new_from=None):
     """Logits rows a middle step reads: each pool node's own row (its children)
     and the row of each pool node's parent (its edge score)."""
     rows = set()
-    for v in pool_of(tree, b):
+    for v in pool_of(tree, b, flags, new_from):
         rows.add(v + 1)
         if v != -1:
             rows.add(int(tree.parent[b, v]) + 1)
     return sorted(rows)
 
 
+def overwrite_compact(t: Tree, b: int, F):
+    """The w/o ND reading (Sec. 4.4): attaching under a frontier node
+    overwrites its existing children, so every node with a strict ancestor in
+    F is removed.  Frontier nodes inside a removed subtree are removed with
+    it.  The surviving nodes keep their order and are renumbered densely
+    (parents stay before children).  Returns (old -> new id map, surviving F
+    in the order of F, new id)."""
+    nb = int(t.n_nodes[b])
+    inF = set(F)
+    dead = np.zeros(nb, bool)
+    for u in range(nb):           # ids are topological
+        p = int(t.parent[b, u])
+        dead[u] = (p in inF) or (p >= 0 and dead[p])
+    newid = np.full(nb, -1, np.int64)
+    keep = [u for u in range(nb) if not dead[u]]
+    for i, u in enumerate(keep):
+        newid[u] = i
+    cols = {name: getattr(t, name)[b, :nb].copy()
+            for name in ("parent", "token", "depth", "logp", "cum", "visited")}
+    for name, col in cols.items():
+        arr = getattr(t, name)
+        for i, u in enumerate(keep):
+            arr[b, i] = col[u]
+    for i, u in enumerate(keep):
+        p = int(cols["parent"][u])
+        t.parent[b, i] = -1 if p < 0 else newid[p]
+    t.n_nodes[b] = len(keep)
+    Fs = [(-1 if v < 0 else int(newid[v])) for v in F if v < 0 or not dead[v]]
+    Fold = [v for v in F if v < 0 or not dead[v]]
+    return newid, Fold, Fs
+
+
 def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
-                  lse_override=None, N: int = 0):
+                  lse_override=None, N: int = 0, flags: int = 0, new_from=None):
     """One middle-drafter step of Alg. 2, applied to a copy.
 
     strong: [B, R, V] fp32; row 0 = the middle drafter's logits at the root,
@@ -219,6 +263,17 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
     The grafted children are N_{k+1}, the pool of a following small step
     (Sec. 3.2: a small step's pool is the previous step's new nodes); with
     N > 0 their Top_N by (cum desc, depth asc, id asc) is also returned.
+    Variant flags (Sec. 4.4 ablations; 0 = the paper's method):
+      POOL_NEWONLY   step 1 uses C = N_k (ids >= new_from[b]; see pool_of);
+      GRAFT_OVERWRITE before step 4 the frontier nodes' existing subtrees are
+                     removed and the tree compacted (overwrite_compact); F
+                     and the children then use the new ids;
+      GRAFT_DEDUP    step 4 skips a child whose token an existing child of
+                     the same parent already carries; the kept children take
+                     dense ids in (slot, rank) order.  (With OVERWRITE a
+                     frontier node has no children left, so nothing is
+                     skipped.)
+    The capacity check uses the upper bound n_b + |F|*M in every variant.
     Returns (tree', row_lse [B, R], graft_frontier [B, W], n_graft [B], err)
     and, when N > 0, also (next_frontier [B, N], n_next [B]).  row_lse holds
     NaN for rows that were not needed.
@@ -236,8 +291,8 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
         if nb + 1 > R:
             err |= DERR_BAD_NODE
             continue
-        C = pool_of(t, b)
-        rows = needed_rows(t, b)
+        C = pool_of(t, b, flags, new_from)
+        rows = needed_rows(t, b, flags, new_from)
         for r in rows:
             _, bad = clean_logits(strong[b, r])
             if bad:
@@ -262,15 +317,35 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
         cand = sorted(node_key(0.0, 0, -1) if v == -1 else
                       node_key(t.cum[b, v], t.depth[b, v], v) for v in C)
         Fsel = [k[2] for k in cand[:nF]]
-        # 4. non-destructive grafting
+        # 5 (first half). P <- P u C (all unvisited nodes for the paper's
+        # pool; only N_k with POOL_NEWONLY)
+        for v in C:
+            if v == -1:
+                t.root_visited[b] = 1
+            else:
+                t.visited[b, v] = 1
+        # variant: overwrite the frontier nodes' subtrees
+        Frows = list(Fsel)      # logits rows stay those of the old ids
+        Fids = list(Fsel)
+        if flags & GRAFT_OVERWRITE:
+            _, Frows, Fids = overwrite_compact(t, b, Fsel)
+        nb2 = int(t.n_nodes[b])
+        # 4. grafting (non-destructive unless overwritten above)
         kids = []
-        for f, v in enumerate(Fsel):
-            toks, vals = row_topk(strong[b, v + 1], M)
-            lse = lse_out[b, v + 1]
+        nid = nb2
+        for f, (v_row, v) in enumerate(zip(Frows, Fids)):
+            toks, vals = row_topk(strong[b, v_row + 1], M)
+            lse = lse_out[b, v_row + 1]
             cum_v = F32(0.0) if v == -1 else t.cum[b, v]
             d_v = 0 if v == -1 else int(t.depth[b, v])
+            sib = set()
+            if flags & GRAFT_DEDUP:
+                sib = {int(t.token[b, u]) for u in range(nb2) if int(t.parent[b, u]) == v}
             for j in range(M):
-                nid = nb + f * M + j
+                if not (flags & (GRAFT_OVERWRITE | GRAFT_DEDUP)):
+                    nid = nb2 + f * M + j
+                elif int(toks[j]) in sib:
+                    continue
                 lp = edge_logp(vals[j], lse)
                 t.parent[b, nid] = v
                 t.token[b, nid] = toks[j]
@@ -279,16 +354,14 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
                 t.cum[b, nid] = F32(cum_v + lp)
                 t.visited[b, nid] = 0
                 kids.append(node_key(t.cum[b, nid], d_v + 1, nid))
+                nid += 1
         kids.sort()
         sel = [k[2] for k in kids[:N]]
         nxt[b, :len(sel)] = sel
         n_next[b] = len(sel)
-        # 5. visited update
-        t.visited[b, :nb] = 1
-        t.root_visited[b] = 1
-        t.n_nodes[b] = nb + nF * M
-        fr_out[b, :nF] = Fsel
-        n_graft[b] = nF
+        t.n_nodes[b] = nb2 + len(kids)
+        fr_out[b, :len(Fids)] = Fids
+        n_graft[b] = len(Fids)
     if N > 0:
         return t, lse_out, fr_out, n_graft, err, nxt, n_next
     return t, lse_out, fr_out, n_graft, err
@@ -335,6 +408,31 @@ def accept(parent: np.ndarray, token: np.ndarray, n_nodes: np.ndarray,
             paths[b, :len(best)] = best
             bonus[b] = greedy[b, best[-1] + 1]
     return A, paths, bonus, err
+
+
+def greedy_argmax(logits: np.ndarray, n_nodes: np.ndarray):
+    """The target's greedy tokens (temperature 0, App. E) from its logits
+    [B, R, V]: greedy[b, r] = arg-max of row r for r <= n_nodes[b] (ties to
+    the smallest token id; NaN and +inf read as -inf, NONFINITE bit), -1 for
+    rows past the tree.  Returns (greedy [B, R], err)."""
+    B, R, V = logits.shape
+    g = np.full((B, R), -1, np.int32)
+    err = 0
+    for b in range(B):
+        for r in range(min(R, int(n_nodes[b]) + 1)):
+            x, bad = clean_logits(logits[b, r])
+            if bad:
+                err |= DERR_NONFINITE
+            g[b, r] = int(np.argmax(x))   # first maximum = smallest token id
+    return g, err
+
+
+def accept_logits(parent, token, n_nodes, logits, max_depth: int):
+    """Acceptance straight from the target's logits: greedy_argmax, then
+    accept.  Returns (greedy, accept_len, accept_path, bonus, err)."""
+    g, e1 = greedy_argmax(logits, n_nodes)
+    A, paths, bonus, e2 = accept(parent, token, n_nodes, g, max_depth)
+    return g, A, paths, bonus, e1 | e2
 
 
 # -------------------------------------------------------------- global prune
