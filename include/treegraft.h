@@ -75,6 +75,15 @@ typedef enum { TG_F32 = 0, TG_BF16 = 1 } tg_dtype;
 
 #define TG_NO_NODE (-2)        /* padding of frontier outputs (-1 is the root) */
 
+/* Variant flags of tg_tree_rescore_graft (0 = the method of Sec. 3.2).  The
+ * first two are the Sec. 4.4 ablations. */
+#define TG_POOL_NEWONLY 1u     /* w/o EG: pool C = N_k, the previous step's
+                                  new nodes (ids >= new_from[b]; -1 = root) */
+#define TG_GRAFT_OVERWRITE 2u  /* w/o ND: grafting under a frontier node
+                                  first removes its existing subtrees       */
+#define TG_GRAFT_DEDUP 4u      /* skip a new child whose token an existing
+                                  child of the same parent already carries  */
+
 /* Limits (TG_ERR_UNSUPPORTED outside them). */
 #define TG_MAX_TOPK 64         /* K of expand, M of rescore                     */
 #define TG_MAX_CAP 4096        /* tree capacity (nodes per tree, root excluded) */
@@ -193,7 +202,22 @@ tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
  *      n_b + f*M + j, parent F[f], logp = fl(x - lse), cum = fl(cum(F[f]) +
  *      logp), depth depth(F[f]) + 1, visited 0.  No existing node's parent,
  *      token or depth is written.
- *   5. P <- P u C: visited[0, n_b) = 1, root_visited = 1; n_b += |F|*M.
+ *   5. P <- P u C: visited[v] = 1 for v in C, root_visited = 1 if the root
+ *      is in C; n_b += |F|*M.
+ * Variants (flags, any combination):
+ *   TG_POOL_NEWONLY: step 1 uses C = {v : new_from[b] <= v < n_b} (the root
+ *      when new_from[b] == -1); new_from [B] int32 device, read only with
+ *      this flag (BAD_NODE when outside [-1, n_b], then clamped).
+ *   TG_GRAFT_OVERWRITE: between steps 3 and 4 every node with a strict
+ *      ancestor in F is removed (a frontier node inside a removed subtree
+ *      leaves F) and the survivors are renumbered densely in id order, all
+ *      their fields moved; F and the new children use the new ids; the
+ *      children of surviving slot f are n_b' + f*M + j.
+ *   TG_GRAFT_DEDUP: a (slot, rank) whose token an existing child of F[f]
+ *      carries is not attached; the attached children take dense ids in
+ *      (slot, rank) order.  (After an overwrite a frontier node has no
+ *      children, so nothing is skipped.)
+ *   The capacity check is the upper bound n_b + |F|*M in every variant.
  * row_lse[b, r] is written for the rows the step reads: v+1 and parent(v)+1
  * for v in C (other rows untouched).  graft_frontier[b] = F (ids, -1 = root),
  * padded with TG_NO_NODE; n_graft[b] = |F|.
@@ -208,7 +232,10 @@ tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
  * n_graft        [B] int32 out
  * next_frontier  [B, N] int32 out or NULL;  n_next [B] int32 out (NULL iff
  *                next_frontier is NULL);  N >= 1 when next_frontier is used
- * 1 <= M <= min(V, TG_MAX_TOPK); 1 <= W; cap <= TG_MAX_CAP; flags = 0.
+ * 1 <= M <= min(V, TG_MAX_TOPK); 1 <= W; cap <= TG_MAX_CAP; flags within
+ * the three bits above (TG_ERR_UNSUPPORTED otherwise, or when the step's LDS
+ * layout for this cap, M and flags exceeds 160 KiB: the graft variants need
+ * 20 bytes per slot more, so they stop at cap 2048 for small M).
  * Device errors: NONFINITE; BAD_NODE (R too small) or CAPACITY
  * (n_b + |F|*M > cap) leave tree b unchanged with n_graft[b] = 0 and
  * n_next[b] = 0.
@@ -217,7 +244,7 @@ size_t tg_rescore_graft_workspace(int B, int R, int V, int W, int M, int cap);
 
 tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 int B, int R, int V, int W, int M,
-                                uint32_t flags, float *row_lse,
+                                uint32_t flags, const int32_t *new_from, float *row_lse,
                                 int32_t *graft_frontier, int32_t *n_graft,
                                 int32_t *next_frontier, int32_t *n_next, int N,
                                 void *workspace, size_t ws_bytes,
@@ -246,6 +273,23 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
                          int cap, int max_depth, int32_t *accept_len,
                          int32_t *accept_path, int32_t *bonus, uint32_t *d_err,
                          void *stream);
+
+/*
+ * tg_tree_accept_logits: the same acceptance straight from the target's
+ * logits.  greedy[b, r] = arg-max of logits[b, r] (ties to the smallest
+ * token id; NaN and +inf read as -inf, NONFINITE) for r <= n_nodes[b], -1
+ * for the other rows; then tg_tree_accept on that greedy array.
+ *
+ * logits  [B, R, V] fp32 (row 0 = after the prefix, 1+i = after node i);
+ *         R >= n_nodes[b] + 1, else BAD_NODE and the missing rows read -1
+ *         (nothing below them is acceptable)
+ * greedy  [B, cap + 1] int32 out; the other arguments as tg_tree_accept.
+ */
+tg_status tg_tree_accept_logits(const int32_t *parent, const int32_t *token,
+                                const int32_t *n_nodes, const float *logits, int B, int cap,
+                                int R, int V, int max_depth, int32_t *greedy,
+                                int32_t *accept_len, int32_t *accept_path, int32_t *bonus,
+                                uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Final pruning and the verification buffers (Alg. 3, global score-based

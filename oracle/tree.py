@@ -414,11 +414,14 @@ def greedy_argmax(logits: np.ndarray, n_nodes: np.ndarray):
     """The target's greedy tokens (temperature 0, App. E) from its logits
     [B, R, V]: greedy[b, r] = arg-max of row r for r <= n_nodes[b] (ties to
     the smallest token id; NaN and +inf read as -inf, NONFINITE bit), -1 for
-    rows past the tree.  Returns (greedy [B, R], err)."""
+    rows past the tree (BAD_NODE when the tree needs a row past R).  Returns
+    (greedy [B, R], err)."""
     B, R, V = logits.shape
     g = np.full((B, R), -1, np.int32)
     err = 0
     for b in range(B):
+        if int(n_nodes[b]) + 1 > R:
+            err |= DERR_BAD_NODE
         for r in range(min(R, int(n_nodes[b]) + 1)):
             x, bad = clean_logits(logits[b, r])
             if bad:
@@ -429,10 +432,15 @@ def greedy_argmax(logits: np.ndarray, n_nodes: np.ndarray):
 
 def accept_logits(parent, token, n_nodes, logits, max_depth: int):
     """Acceptance straight from the target's logits: greedy_argmax, then
-    accept.  Returns (greedy, accept_len, accept_path, bonus, err)."""
+    accept.  Returns (greedy [B, cap + 1] with -1 past the rows computed,
+    accept_len, accept_path, bonus, err)."""
     g, e1 = greedy_argmax(logits, n_nodes)
-    A, paths, bonus, e2 = accept(parent, token, n_nodes, g, max_depth)
-    return g, A, paths, bonus, e1 | e2
+    B, cap = parent.shape
+    full = np.full((B, cap + 1), -1, np.int32)
+    w = min(g.shape[1], cap + 1)
+    full[:, :w] = g[:, :w]
+    A, paths, bonus, e2 = accept(parent, token, n_nodes, full, max_depth)
+    return full, A, paths, bonus, e1 | e2
 
 
 # -------------------------------------------------------------- global prune

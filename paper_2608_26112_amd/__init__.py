@@ -30,6 +30,10 @@ DERR_NONFINITE = 4
 DERR_BAD_PREFIX = 8
 DERR_BAD_NODE = 16
 NO_NODE = -2
+# variant flags of rescore_graft (see include/treegraft.h)
+POOL_NEWONLY = 1
+GRAFT_OVERWRITE = 2
+GRAFT_DEDUP = 4
 MAX_TOPK = 64
 MAX_CAP = 4096
 MAX_EXPAND_CHILDREN = 8192
@@ -47,6 +51,7 @@ EXPORTED = (
     "tg_tree_expand_topk",
     "tg_rescore_graft_workspace",
     "tg_tree_rescore_graft",
+    "tg_tree_accept_logits",
     "tg_tree_accept",
     "tg_tree_global_prune",
     "tg_kv_compact",
@@ -109,9 +114,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_rescore_graft_workspace.argtypes = [_i32] * 6
     lib.tg_tree_rescore_graft.restype = _i32
     lib.tg_tree_rescore_graft.argtypes = ([ctypes.POINTER(TgTree), _vp] + [_i32] * 5 + [_u32] +
-                                          [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp])
+                                          [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp,
+                                           _vp])
     lib.tg_tree_accept.restype = _i32
     lib.tg_tree_accept.argtypes = [_vp] * 4 + [_i32] * 3 + [_vp] * 5
+    lib.tg_tree_accept_logits.restype = _i32
+    lib.tg_tree_accept_logits.argtypes = [_vp] * 4 + [_i32] * 5 + [_vp] * 6
     lib.tg_tree_reset.restype = _i32
     lib.tg_tree_reset.argtypes = [ctypes.POINTER(TgTree), _i32, _vp]
     lib.tg_tree_global_prune.restype = _i32
@@ -283,12 +291,16 @@ def rescore_graft_workspace(B, R, V, W, M, cap) -> int:
 
 def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
                   graft_frontier=None, n_graft=None, N=0, next_frontier=None, n_next=None,
-                  workspace=None, d_err=None, stream=None):
+                  workspace=None, d_err=None, stream=None, new_from=None):
     """One middle-drafter step.  strong_logits [B,R,V] fp32 (row 0 = root,
-    1+i = node i).  Returns (row_lse, graft_frontier, n_graft), plus
-    (next_frontier, n_next) -- the best N grafted children -- when N > 0."""
+    1+i = node i).  flags: POOL_NEWONLY (needs new_from [B] int32),
+    GRAFT_OVERWRITE, GRAFT_DEDUP.  Returns (row_lse, graft_frontier,
+    n_graft), plus (next_frontier, n_next) -- the best N grafted children --
+    when N > 0."""
     lib = load()
     _dev(strong_logits, "strong_logits", torch.float32)
+    if new_from is not None:
+        _dev(new_from, "new_from", torch.int32)
     B, R, V = strong_logits.shape
     dev = strong_logits.device
     row_lse = (torch.full((B, R), float("nan"), dtype=torch.float32, device=dev)
@@ -304,7 +316,8 @@ def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
                          workspace)
     ts = tree.struct()
     st = lib.tg_tree_rescore_graft(ctypes.byref(ts), _ptr(strong_logits), B, R, V, W, M,
-                                   int(flags), _ptr(row_lse), _ptr(graft_frontier),
+                                   int(flags), _ptr(new_from), _ptr(row_lse),
+                                   _ptr(graft_frontier),
                                    _ptr(n_graft), _ptr(next_frontier if N > 0 else None),
                                    _ptr(n_next if N > 0 else None), int(N), _ptr(ws), wsb,
                                    _ptr(d_err), _stream(stream))
@@ -335,6 +348,32 @@ def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_pa
                             _ptr(d_err), _stream(stream))
     _check("tg_tree_accept", st)
     return accept_len, accept_path, bonus
+
+
+def accept_logits(parent, token, n_nodes, logits, max_depth, greedy=None, accept_len=None,
+                  accept_path=None, bonus=None, d_err=None, stream=None):
+    """Greedy acceptance from the target's logits [B,R,V] fp32 (row 0 = after
+    the prefix, 1+i = after node i).  Returns (greedy [B,cap+1], accept_len,
+    accept_path, bonus)."""
+    lib = load()
+    for t, n in ((parent, "parent"), (token, "token"), (n_nodes, "n_nodes")):
+        _dev(t, n, torch.int32)
+    _dev(logits, "logits", torch.float32)
+    B, cap = parent.shape
+    R, V = logits.shape[1], logits.shape[2]
+    if logits.shape[0] != B:
+        raise ValueError("logits must be [B, R, V]")
+    dev = parent.device
+    greedy = torch.empty((B, cap + 1), dtype=torch.int32, device=dev) if greedy is None else greedy
+    accept_len = torch.empty((B,), dtype=torch.int32, device=dev) if accept_len is None else accept_len
+    accept_path = (torch.empty((B, max_depth), dtype=torch.int32, device=dev)
+                   if accept_path is None else accept_path)
+    bonus = torch.empty((B,), dtype=torch.int32, device=dev) if bonus is None else bonus
+    st = lib.tg_tree_accept_logits(_ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(logits), B,
+                                   cap, R, V, max_depth, _ptr(greedy), _ptr(accept_len),
+                                   _ptr(accept_path), _ptr(bonus), _ptr(d_err), _stream(stream))
+    _check("tg_tree_accept_logits", st)
+    return greedy, accept_len, accept_path, bonus
 
 
 def global_prune(tree: TreeState, B_ver: int, max_path: int | None = None, d_err=None,

@@ -7,6 +7,9 @@
 // path matches" and the depth are computed by pointer jumping over the parent
 // links in LDS (log2(n) rounds), so adversarial chains cost O(n log n), not
 // O(n * depth).  The winner is the block-wide maximum of (depth, -id).
+//
+// argmax_rows_kernel: the target's greedy tokens straight from its logits,
+// for the accept-from-logits entry point.
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -108,7 +111,67 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(
   }
 }
 
+// The target's greedy token of every row a tree uses (temperature 0):
+// greedy[b, r] = arg-max of logits[b, r] for r <= n_nodes[b] (ties to the
+// smallest token: the max of (logit, -token) keys; NaN and +inf read as
+// -inf), -1 for the other rows.  One workgroup per (tree, row) of the
+// greedy array; rows past the logits (r >= R) are -1 and raise BAD_NODE
+// when the tree needs them.
+__global__ __launch_bounds__(kThreads) void argmax_rows_kernel(
+    const float *__restrict__ logits, const int32_t *__restrict__ n_nodes, int cap, int R,
+    int V, int32_t *__restrict__ greedy, uint32_t *d_err) {
+  __shared__ uint64_t red[kThreads / kWave];
+  const int rows = cap + 1;
+  const int b = blockIdx.x / rows, r = blockIdx.x - b * rows;
+  const int tid = threadIdx.x;
+  int nb = n_nodes[b];
+  nb = nb < 0 ? 0 : (nb > cap ? cap : nb);
+  int32_t *out = greedy + (size_t)b * rows + r;
+  if (r > nb || r >= R) {
+    if (tid == 0) {
+      *out = -1;
+      if (r <= nb) report(d_err, TG_DERR_BAD_NODE);
+    }
+    return;
+  }
+  const float *x = logits + ((size_t)b * R + r) * V;
+  uint64_t best = 0;
+  bool bad = false;
+  if ((V & 3) == 0) {
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    for (int i = tid; i < V / 4; i += kThreads) {
+      const float4 q = x4[i];
+      const uint32_t t0 = 4u * (uint32_t)i;
+      uint64_t k = token_key(clean_logit(q.x, bad), t0);
+      k = max(k, token_key(clean_logit(q.y, bad), t0 + 1));
+      k = max(k, token_key(clean_logit(q.z, bad), t0 + 2));
+      k = max(k, token_key(clean_logit(q.w, bad), t0 + 3));
+      best = max(best, k);
+    }
+  } else {
+    for (int i = tid; i < V; i += kThreads)
+      best = max(best, token_key(clean_logit(x[i], bad), (uint32_t)i));
+  }
+  if (bad) report(d_err, TG_DERR_NONFINITE);
+  best = wave_max_u64(best);
+  if ((tid & (kWave - 1)) == 0) red[tid / kWave] = best;
+  __syncthreads();
+  if (tid == 0) {
+    for (int i = 1; i < kThreads / kWave; ++i) best = max(best, red[i]);
+    best = max(best, red[0]);
+    *out = (int32_t)key_token(best);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_argmax_rows(const float *logits, const int32_t *n_nodes, int B, int cap,
+                              int R, int V, int32_t *greedy, uint32_t *d_err,
+                              hipStream_t stream) {
+  launch("argmax_rows", argmax_rows_kernel, dim3((unsigned)((long long)B * (cap + 1))),
+         dim3(kThreads), 0, stream, logits, n_nodes, cap, R, V, greedy, d_err);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept(const int32_t *parent, const int32_t *token,
                          const int32_t *n_nodes, const int32_t *greedy, int B,

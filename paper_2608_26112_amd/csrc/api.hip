@@ -133,7 +133,7 @@ size_t tg_rescore_graft_workspace(int B, int R, int V, int W, int M, int cap) {
 
 tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 int B, int R, int V, int W, int M,
-                                uint32_t flags, float *row_lse,
+                                uint32_t flags, const int32_t *new_from, float *row_lse,
                                 int32_t *graft_frontier, int32_t *n_graft,
                                 int32_t *next_frontier, int32_t *n_next, int N,
                                 void *workspace, size_t ws_bytes,
@@ -144,18 +144,25 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   if (next_frontier && N <= 0) return TG_ERR_INVALID_ARG;
   if (B <= 0 || R <= 0 || V <= 0 || W <= 0 || M <= 0) return TG_ERR_INVALID_ARG;
   if (M > V) return TG_ERR_INVALID_ARG;
-  if (flags != 0) return TG_ERR_UNSUPPORTED;
+  if (flags & ~(TG_POOL_NEWONLY | TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP))
+    return TG_ERR_UNSUPPORTED;
+  if ((flags & TG_POOL_NEWONLY) && !new_from) return TG_ERR_INVALID_ARG;
   if (M > TG_MAX_TOPK || tree->cap > TG_MAX_CAP)
     return TG_ERR_UNSUPPORTED;
   RowWs w = row_ws((long long)B * R, V, M, (size_t)B * R);
   if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
   tg::RowPlan plan = tg::plan_rows((long long)B * R, V);
+  {
+    int so = 0, vo = 0;
+    if (tg::rescore_tree_lds(tree->cap, M, plan, flags, &so, &vo) > 160 * 1024)
+      return TG_ERR_UNSUPPORTED;
+  }
   char *ws = static_cast<char *>(workspace);
   float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
   uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
   uint8_t *needed = reinterpret_cast<uint8_t *>(ws + w.extra_off);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = tg::launch_rescore_pool(*tree, B, R, needed, st);
+  hipError_t e = tg::launch_rescore_pool(*tree, B, R, needed, flags, new_from, st);
   if (e != hipSuccess) return TG_ERR_HIP;
   e = tg::launch_row_partials(strong_logits, B, R, V, M, plan, nullptr, needed, ms, keys,
                               d_err, st);
@@ -163,7 +170,7 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan, needed,
                                           ms, keys, row_lse, graft_frontier, n_graft,
                                           next_frontier, n_next, next_frontier ? N : 0,
-                                          d_err, st));
+                                          flags, new_from, d_err, st));
 }
 
 // ------------------------------------------------------------------- accept
@@ -180,6 +187,24 @@ tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
   return from_hip(tg::launch_accept(parent, token, n_nodes, greedy, B, cap, max_depth,
                                     accept_len, accept_path, bonus, d_err,
                                     reinterpret_cast<hipStream_t>(stream)));
+}
+
+tg_status tg_tree_accept_logits(const int32_t *parent, const int32_t *token,
+                                const int32_t *n_nodes, const float *logits, int B, int cap,
+                                int R, int V, int max_depth, int32_t *greedy,
+                                int32_t *accept_len, int32_t *accept_path, int32_t *bonus,
+                                uint32_t *d_err, void *stream) {
+  if (!logits || !greedy) return TG_ERR_INVALID_ARG;
+  if (R <= 0 || V <= 0) return TG_ERR_INVALID_ARG;
+  if (!parent || !token || !n_nodes || !accept_len || !bonus) return TG_ERR_INVALID_ARG;
+  if (B <= 0 || cap <= 0 || max_depth < 0) return TG_ERR_INVALID_ARG;
+  if (max_depth > 0 && !accept_path) return TG_ERR_INVALID_ARG;
+  if (cap > TG_MAX_CAP) return TG_ERR_UNSUPPORTED;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = tg::launch_argmax_rows(logits, n_nodes, B, cap, R, V, greedy, d_err, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(tg::launch_accept(parent, token, n_nodes, greedy, B, cap, max_depth,
+                                    accept_len, accept_path, bonus, d_err, st));
 }
 
 tg_status tg_tree_global_prune(const tg_tree *tree, int B, int B_ver, int max_path,

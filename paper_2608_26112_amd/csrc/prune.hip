@@ -27,29 +27,6 @@ constexpr int kThreads = 256;
 
 constexpr int kRankCountMax = kRankPerThread * kThreads;  // rank by counting up to here
 
-// Exclusive prefix of one int per thread in thread order (waves by shuffles,
-// then the wave totals); `slots` holds kThreads / kWave ints.  Ends
-// synchronised.
-__device__ int block_exclusive_scan(int v, int *slots, int &total) {
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  int incl = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
-  if (lane == kWave - 1) slots[wv] = incl;
-  __syncthreads();
-  int before = 0;
-  total = 0;
-  for (int i = 0; i < kThreads / kWave; ++i) {
-    before += i < wv ? slots[i] : 0;
-    total += slots[i];
-  }
-  __syncthreads();
-  return before + incl - v;
-}
-
 __global__ __launch_bounds__(kThreads) void prune_kernel(
     tg_tree tree, int B_ver, int max_path, int32_t *__restrict__ kept,
     int32_t *__restrict__ vparent, int32_t *__restrict__ vtoken,
@@ -168,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   int mine_k = 0;
   for (int v = c_lo; v < c_hi; ++v) mine_k += flag[v];
   int nk_total = 0;
-  int pos = block_exclusive_scan(mine_k, cnt, nk_total);
+  int pos = block_exclusive_scan<kThreads>(mine_k, cnt, nk_total);
   for (int v = c_lo; v < c_hi; ++v)
     if (flag[v]) key[pos++] = ~(((uint64_t)depth[v] << 32) | (uint64_t)v);
   for (int v = tid; v < nn; v += kThreads) newid[v] = 0;
@@ -259,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   }
   if (deep) deep_s = 1;
   int total = 0;
-  const int first_rank = block_exclusive_scan(mine, cnt, total);
+  const int first_rank = block_exclusive_scan<kThreads>(mine, cnt, total);
   if (tid == 0) {
     nl_s = total;
     if (deep_s) report(d_err, TG_DERR_CAPACITY);

@@ -116,6 +116,30 @@ __device__ inline void block_bitonic_desc(uint64_t *a, int n) {
   }
 }
 
+// Exclusive prefix sum of one int per thread in thread order (waves by
+// shuffles, then the wave totals); `slots` holds kBlock / kWave ints of LDS.
+// Called by the whole block; ends synchronised.
+template <int kBlock>
+__device__ int block_exclusive_scan(int v, int *slots, int &total) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) slots[wv] = incl;
+  __syncthreads();
+  int before = 0;
+  total = 0;
+  for (int i = 0; i < kBlock / kWave; ++i) {
+    before += i < wv ? slots[i] : 0;
+    total += slots[i];
+  }
+  __syncthreads();
+  return before + incl - v;
+}
+
 // ---------------------------------------------------- ranks by counting
 // A key's exact rank among a small set is the number of larger keys: one pass
 // over LDS broadcasts with no barrier, where a bitonic sort of the same set

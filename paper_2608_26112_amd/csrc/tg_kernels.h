@@ -58,8 +58,12 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
 
 hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream);
 
-hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
-                               uint8_t *needed, hipStream_t stream);
+hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *needed,
+                               uint32_t flags, const int32_t *new_from,
+                               hipStream_t stream);
+// dynamic LDS of rescore_tree_kernel (and the offsets of its regions)
+size_t rescore_tree_lds(int cap, int M, RowPlan plan, uint32_t flags, int *stage_off,
+                        int *var_off);
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                int R, int V, int W, int M, RowPlan plan,
@@ -67,9 +71,13 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                const uint64_t *part_keys, float *row_lse,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
+                               uint32_t flags, const int32_t *new_from,
                                uint32_t *d_err, hipStream_t stream);
 
 // ----------------------------------------------------------------- accept
+hipError_t launch_argmax_rows(const float *logits, const int32_t *n_nodes, int B, int cap,
+                              int R, int V, int32_t *greedy, uint32_t *d_err,
+                              hipStream_t stream);
 hipError_t launch_accept(const int32_t *parent, const int32_t *token,
                          const int32_t *n_nodes, const int32_t *greedy, int B,
                          int cap, int max_depth, int32_t *accept_len,

@@ -182,11 +182,34 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
 }
 
 // ------------------------------------------------------- middle-step pool
+// The candidate pool C of a middle step (Sec. 3.2): the unvisited nodes and
+// the root while unvisited; with TG_POOL_NEWONLY (the w/o EG ablation, Sec.
+// 4.4) the previous step's new nodes, ids new_from[b] .. n_b - 1, the root
+// when new_from[b] == -1 (read clamped to [-1, n_b]).
+struct PoolRule {
+  bool newonly;
+  int lo;
+  __device__ bool in(const tg_tree &t, size_t base, int v) const {
+    return newonly ? v >= lo : !t.visited[base + v];
+  }
+  __device__ bool root_in(const tg_tree &t, int b) const {
+    return newonly ? lo <= -1 : !t.root_visited[b];
+  }
+};
+__device__ inline PoolRule pool_rule(const tg_tree &t, int b, int nb, uint32_t flags,
+                                     const int32_t *new_from) {
+  PoolRule r{(flags & TG_POOL_NEWONLY) != 0, 0};
+  if (r.newonly) r.lo = min(max(new_from[b], -1), max(nb, 0));
+  return r;
+}
+
+
 // needed[b, r] = 1 iff logits row r is read by this middle step: the row of
 // each pool node (its children) and the row of each pool node's parent (its
 // edge score).  Rows of trees that cannot be processed are all 0.
 __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
-    tg_tree tree, int R, uint8_t *__restrict__ needed) {
+    tg_tree tree, int R, uint8_t *__restrict__ needed, uint32_t flags,
+    const int32_t *__restrict__ new_from) {
   __shared__ uint8_t flag[TG_MAX_CAP + 1];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int nb = tree.n_nodes[b];
@@ -195,11 +218,12 @@ __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
   for (int r = tid; r < rows; r += kThreads) flag[r] = 0;
   __syncthreads();
   const size_t base = (size_t)b * tree.cap;
+  const PoolRule pool = pool_rule(tree, b, nb, flags, new_from);
   if (ok) {
-    if (tid == 0 && !tree.root_visited[b]) flag[0] = 1;
+    if (tid == 0 && pool.root_in(tree, b)) flag[0] = 1;
     bool dummy = false;
     for (int v = tid; v < nb; v += kThreads) {
-      if (!tree.visited[base + v]) {
+      if (pool.in(tree, base, v)) {
         flag[v + 1] = 1;
         flag[sane_parent(tree.parent[base + v], v, dummy) + 1] = 1;
       }
@@ -210,6 +234,199 @@ __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
     needed[(size_t)b * R + r] = r < rows ? flag[r] : 0;
 }
 
+// ------------------------------------------------------- graft variants
+// The middle step's graft under TG_GRAFT_OVERWRITE (w/o ND, Sec. 4.4: the
+// frontier nodes' existing subtrees are removed and the tree compacted
+// before the new children are attached) and TG_GRAFT_DEDUP (a child whose
+// token an existing child of the same parent carries is skipped; kept
+// children take dense ids in (slot, rank) order).  Entered after the
+// reselection (F = skey[0, nF)) and the P <- P u C write-back.  LDS:
+//   vmap, rrow, rpid, rdep, rcum  [cap] each (the variant region);
+//   stage = the logp scratch, flags = inC / done, candidates = skey.
+__device__ void graft_variant(const tg_tree &tree, int b, int nb, int nF, int M, int W,
+                              int N, int R, int chunks, uint32_t flags,
+                              const uint64_t *__restrict__ part_keys, const float *lse_s,
+                              const float *cum_s, const int *par_s, int *stage,
+                              uint8_t *flag_a, uint8_t *flag_b, uint64_t *skey, int *var,
+                              uint64_t *wstage, int *red, int32_t *graft_frontier,
+                              int32_t *n_graft, int32_t *next_frontier, int32_t *n_next) {
+  __shared__ int rootF_s, nF2_s, rootslot_s;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int cap = tree.cap;
+  const size_t base = (size_t)b * cap;
+  int *vmap = var, *rrow = var + cap, *rpid = var + 2 * cap, *rdep = var + 3 * cap;
+  float *rcum = reinterpret_cast<float *>(var + 4 * cap);
+
+  // frontier records (logits row, id, depth, cum) from the old ids
+  for (int f = tid; f < nF; f += kThreads) {
+    const int v = node_key_id(skey[f]);
+    rrow[f] = v + 1;
+    rpid[f] = v;
+    rdep[f] = v < 0 ? 0 : tree.depth[base + v];
+    rcum[f] = v < 0 ? 0.0f : cum_s[v];
+  }
+  if (tid == 0) {
+    rootF_s = 0;
+    nF2_s = nF;
+    rootslot_s = -1;
+  }
+  __syncthreads();
+  int nb2 = nb;
+
+  if (flags & TG_GRAFT_OVERWRITE) {
+    uint8_t *inF = flag_a, *dead = flag_b;
+    for (int v = tid; v < nb; v += kThreads) {
+      inF[v] = 0;
+      dead[v] = 0;
+    }
+    __syncthreads();
+    for (int f = tid; f < nF; f += kThreads) {
+      if (rpid[f] < 0) rootF_s = 1;
+      else inF[rpid[f]] = 1;
+    }
+    __syncthreads();
+    const bool rootF = rootF_s != 0;
+    // dead = a strict ancestor is in F; one more level settles per round
+    for (;;) {
+      int changed = 0;
+      for (int v = tid; v < nb; v += kThreads) {
+        if (dead[v]) continue;
+        const int p = par_s[v];
+        if (rootF || (p >= 0 && (inF[p] || dead[p]))) {
+          dead[v] = 1;
+          changed = 1;
+        }
+      }
+      if (!__syncthreads_or(changed)) break;
+    }
+    // survivors get dense ids in id order
+    const int per = (nb + kThreads - 1) / kThreads;
+    const int lo = min(nb, tid * per), hi = min(nb, lo + per);
+    int mine = 0;
+    for (int v = lo; v < hi; ++v) mine += dead[v] ? 0 : 1;
+    int total = 0;
+    int pos = block_exclusive_scan<kThreads>(mine, red, total);
+    for (int v = lo; v < hi; ++v) vmap[v] = dead[v] ? -1 : pos++;
+    nb2 = total;
+    __syncthreads();
+    // move the survivors down (every read lands in LDS before any write)
+    auto move = [&](int32_t *field, int which) {
+      for (int v = tid; v < nb; v += kThreads) {
+        if (dead[v]) continue;
+        int x;
+        if (which == 0) x = par_s[v] < 0 ? -1 : vmap[par_s[v]];
+        else if (which == 1) x = tree.visited[base + v];
+        else x = field[base + v];
+        stage[v] = x;
+      }
+      __syncthreads();
+      for (int v = tid; v < nb; v += kThreads) {
+        if (dead[v]) continue;
+        if (which == 1) tree.visited[base + vmap[v]] = (uint8_t)stage[v];
+        else field[base + vmap[v]] = stage[v];
+      }
+      __syncthreads();
+    };
+    move(tree.parent, 0);
+    move(nullptr, 1);
+    move(tree.token, 2);
+    move(tree.depth, 2);
+    move(reinterpret_cast<int32_t *>(tree.logp), 2);
+    for (int v = tid; v < nb; v += kThreads)
+      if (!dead[v]) tree.cum[base + vmap[v]] = cum_s[v];
+    // surviving frontier slots, in order, with their new ids
+    if (tid == 0) {
+      int k = 0;
+      for (int f = 0; f < nF; ++f) {
+        const int v = rpid[f];
+        if (v >= 0 && dead[v]) continue;
+        rrow[k] = rrow[f];
+        rdep[k] = rdep[f];
+        rcum[k] = rcum[f];
+        rpid[k] = v < 0 ? -1 : vmap[v];
+        ++k;
+      }
+      nF2_s = k;
+    }
+    __syncthreads();
+  }
+  const int nF2 = nF2_s;
+
+  // candidates of every (slot, rank) in skey: a wave per slot
+  for (int f = w; f < nF2; f += kWaves) {
+    const size_t slot = (size_t)b * R + rrow[f];
+    const uint64_t key = wave_finish_topk(part_keys + slot * chunks * M, chunks, M, wstage);
+    if (lane < M) skey[f * M + lane] = key;
+  }
+  __syncthreads();
+  const int total_c = nF2 * M;
+  uint8_t *dup = flag_a;
+  for (int i = tid; i < total_c; i += kThreads) dup[i] = 0;
+  if ((flags & TG_GRAFT_DEDUP) && !(flags & TG_GRAFT_OVERWRITE)) {
+    for (int v = tid; v < nb; v += kThreads) vmap[v] = -1;
+    __syncthreads();
+    for (int f = tid; f < nF2; f += kThreads) {
+      if (rpid[f] < 0) rootslot_s = f;
+      else vmap[rpid[f]] = f;
+    }
+    __syncthreads();
+    for (int u = tid; u < nb; u += kThreads) {
+      const int p = par_s[u];
+      const int f = p < 0 ? rootslot_s : vmap[p];
+      if (f < 0) continue;
+      const uint32_t tok = (uint32_t)tree.token[base + u];
+      for (int j = 0; j < M; ++j)
+        if (key_token(skey[f * M + j]) == tok) dup[f * M + j] = 1;
+    }
+  }
+  __syncthreads();
+
+  // kept candidates get dense ids nb2 + rank in (slot, rank) order
+  const int per2 = (total_c + kThreads - 1) / kThreads;
+  const int lo2 = min(total_c, tid * per2), hi2 = min(total_c, lo2 + per2);
+  int mine2 = 0;
+  for (int i = lo2; i < hi2; ++i) mine2 += dup[i] ? 0 : 1;
+  int total_k = 0;
+  const int first = block_exclusive_scan<kThreads>(mine2, red, total_k);
+  int pos2 = first;
+  for (int i = lo2; i < hi2; ++i) {
+    if (dup[i]) continue;
+    const int f = i / M;
+    const uint64_t key = skey[i];
+    const int id = nb2 + pos2++;
+    const float lp = edge_logp(key_logit(key), lse_s[rrow[f]]);
+    tree.parent[base + id] = rpid[f];
+    tree.token[base + id] = (int)key_token(key);
+    tree.depth[base + id] = rdep[f] + 1;
+    tree.logp[base + id] = lp;
+    tree.cum[base + id] = __fadd_rn(rcum[f], lp);
+    tree.visited[base + id] = 0;
+  }
+  for (int f = tid; f < W; f += kThreads)
+    graft_frontier[(size_t)b * W + f] = f < nF2 ? rpid[f] : TG_NO_NODE;
+  if (tid == 0) {
+    tree.n_nodes[b] = nb2 + total_k;
+    n_graft[b] = nF2;
+  }
+  if (N <= 0) return;
+  __syncthreads();  // every candidate key has been read
+  // Top_N of the new children
+  pos2 = first;
+  for (int i = lo2; i < hi2; ++i) {
+    if (dup[i]) continue;
+    const int id = nb2 + pos2++;
+    skey[id - nb2] = node_key(tree.cum[base + id], tree.depth[base + id], id);
+  }
+  const int P2c = pow2_at_least(total_k > 0 ? total_k : 1);
+  for (int c = total_k + tid; c < P2c; c += kThreads) skey[c] = 0;
+  __syncthreads();
+  const int nn = min(N, total_k);
+  block_top_keys<kThreads>(skey, total_k, P2c, nn);
+  for (int j = tid; j < N; j += kThreads)
+    next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
+  if (tid == 0) n_next[b] = nn;
+}
+
 // ------------------------------------------------ rescore + reselect + graft
 __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     tg_tree tree, const float *__restrict__ strong, int R, int V, int W, int M,
@@ -217,7 +434,8 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
     float *__restrict__ row_lse, int32_t *__restrict__ graft_frontier,
     int32_t *__restrict__ n_graft, int32_t *__restrict__ next_frontier,
-    int32_t *__restrict__ n_next, int N, uint32_t *d_err, int stage_off) {
+    int32_t *__restrict__ n_next, int N, uint32_t *d_err, int stage_off, uint32_t flags,
+    const int32_t *__restrict__ new_from, int var_off) {
   extern __shared__ uint64_t smem[];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & (kWave - 1), w = tid / kWave;
@@ -250,17 +468,20 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   uint8_t *done = inC + cap;                               // [cap]
 
   // ---- pool C and parents
+  const PoolRule pool = pool_rule(tree, b, nb, flags, new_from);
+  if (tid == 0 && pool.newonly && (new_from[b] < -1 || new_from[b] > nb))
+    report(d_err, TG_DERR_BAD_NODE);
   bool badp = false;
   int cnt = 0;
   for (int v = tid; v < nb; v += kThreads) {
-    uint8_t in = tree.visited[base + v] ? 0 : 1;
+    uint8_t in = pool.in(tree, base, v) ? 1 : 0;
     inC[v] = in;
     done[v] = in ? 0 : 1;
     cum_s[v] = tree.cum[base + v];
     par_s[v] = sane_parent(tree.parent[base + v], v, badp);
     cnt += in;
   }
-  const int root_in = tree.root_visited[b] ? 0 : 1;
+  const int root_in = pool.root_in(tree, b) ? 1 : 0;
   if (badp) report(d_err, TG_DERR_BAD_PARENT);
   __shared__ int red[kWaves];
   int wsum = wave_sum_i32(cnt);
@@ -343,10 +564,23 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   // ---- P <- P u C; write back rescored path scores (before the graft,
   // whose staging reuses the per-node scratch)
   for (int v = tid; v < nb; v += kThreads) {
-    if (inC[v]) tree.cum[base + v] = cum_s[v];
-    tree.visited[base + v] = 1;
+    if (inC[v]) {
+      tree.cum[base + v] = cum_s[v];
+      tree.visited[base + v] = 1;
+    }
   }
+  if (tid == 0 && root_in) tree.root_visited[b] = 1;
   __syncthreads();
+
+  if (flags & (TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP)) {
+    graft_variant(tree, b, nb, nF, M, W, N, R, chunks, flags, part_keys, lse_s, cum_s,
+                  par_s, reinterpret_cast<int *>(lp_s), inC, done, skey,
+                  reinterpret_cast<int *>(reinterpret_cast<char *>(smem) + var_off),
+                  reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(smem) + stage_off) +
+                      (size_t)w * (chunks * M),
+                  red, graft_frontier, n_graft, next_frontier, n_next);
+    return;
+  }
 
   // ---- non-destructive graft: new children only, ids nb + f*M + j
   // (wave-private LDS for finishing each graft point's top-M; the region of
@@ -376,7 +610,6 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   for (int f = tid; f < W; f += kThreads)
     graft_frontier[(size_t)b * W + f] = f < nF ? node_key_id(skey[f]) : TG_NO_NODE;
   if (tid == 0) {
-    tree.root_visited[b] = 1;
     tree.n_nodes[b] = nb + nF * M;
     n_graft[b] = nF;
   }
@@ -444,11 +677,39 @@ hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
   return hipGetLastError();
 }
 
-hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R,
-                               uint8_t *needed, hipStream_t stream) {
+hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *needed,
+                               uint32_t flags, const int32_t *new_from,
+                               hipStream_t stream) {
   launch("rescore_pool", rescore_pool_kernel, dim3(B), dim3(kThreads), 0, stream,
-                     tree, R, needed);
+                     tree, R, needed, flags, new_from);
   return hipGetLastError();
+}
+
+size_t rescore_tree_lds(int cap, int M, RowPlan plan, uint32_t flags, int *stage_off,
+                        int *var_off) {
+  // layout sized by cap (the kernel uses it up to the live node count):
+  // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent [cap] | inC, done [cap]
+  // (| variant records [5 cap] ints when a graft variant is on)
+  const int n = cap;
+  const size_t keys_b = (size_t)pow2_at_least(n + 1) * 8;
+  const size_t head_b = keys_b + (size_t)(n + 1) * 4 + (size_t)n * 4;  // up to logp
+  const size_t scratch_b = (size_t)n * (4 + 4 + 1 + 1);                // logp..done
+  size_t lds = head_b + scratch_b;
+  // per-wave top-M staging reuses logp..done when they are large enough
+  const size_t stage_b = (size_t)(kThreads / kWave) * plan.chunks * M * 8;
+  size_t so = (head_b + 7) / 8 * 8;
+  if (plan.chunks > 1 && so + stage_b > head_b + scratch_b) {
+    so = (lds + 7) / 8 * 8;
+    lds = so + stage_b;
+  }
+  size_t vo = 0;
+  if (flags & (TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP)) {
+    vo = (lds + 15) / 16 * 16;
+    lds = vo + (size_t)5 * n * 4;
+  }
+  *stage_off = (int)so;
+  *var_off = (int)vo;
+  return lds;
 }
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
@@ -457,28 +718,18 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                const uint64_t *part_keys, float *row_lse,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
+                               uint32_t flags, const int32_t *new_from,
                                uint32_t *d_err, hipStream_t stream) {
-  // layout sized by cap (the kernel uses it up to the live node count):
-  // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent [cap] | inC, done [cap]
-  const int n = tree.cap;
-  const size_t keys_b = (size_t)pow2_at_least(n + 1) * 8;
-  const size_t head_b = keys_b + (size_t)(n + 1) * 4 + (size_t)n * 4;  // up to logp
-  const size_t scratch_b = (size_t)n * (4 + 4 + 1 + 1);                // logp..done
-  size_t lds = head_b + scratch_b;
-  // per-wave top-M staging reuses logp..done when they are large enough
-  const size_t stage_b = (size_t)(kThreads / kWave) * plan.chunks * M * 8;
-  size_t stage_off = (head_b + 7) / 8 * 8;
-  if (plan.chunks > 1 && stage_off + stage_b > head_b + scratch_b) {
-    stage_off = (lds + 7) / 8 * 8;
-    lds = stage_off + stage_b;
-  }
+  int stage_off = 0, var_off = 0;
+  const size_t lds = rescore_tree_lds(tree.cap, M, plan, flags, &stage_off, &var_off);
   hipError_t e = hipFuncSetAttribute((const void *)rescore_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
   launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
          strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms, part_keys,
-         row_lse, graft_frontier, n_graft, next_frontier, n_next, N, d_err, (int)stage_off);
+         row_lse, graft_frontier, n_graft, next_frontier, n_next, N, d_err, stage_off, flags,
+         new_from, var_off);
   return hipGetLastError();
 }
 

@@ -136,7 +136,8 @@ def _rescore(lib, tree=None, **kw):
     a.update(kw)
     t = _tree() if tree is None else tree
     return lib.tg_tree_rescore_graft(ctypes.byref(t), a["strong"], a["B"], a["R"], a["V"],
-                                     a["W"], a["M"], a["flags"], a["lse"], a["gf"], a["ng"],
+                                     a["W"], a["M"], a["flags"], a.get("nf", NULL), a["lse"],
+                                     a["gf"], a["ng"],
                                      a.get("nx", NULL), a.get("nn", NULL), a.get("N", 0),
                                      a["ws"], a["wsb"], NULL, NULL)
 
@@ -146,13 +147,34 @@ def test_rescore_host_checks(lib):
     assert _rescore(lib, strong=NULL) == tg.ERR_INVALID_ARG
     assert _rescore(lib, W=0) == tg.ERR_INVALID_ARG
     assert _rescore(lib, M=2000) == tg.ERR_INVALID_ARG
-    assert _rescore(lib, flags=1) == tg.ERR_UNSUPPORTED
+    assert _rescore(lib, flags=8) == tg.ERR_UNSUPPORTED             # unknown variant bit
+    assert _rescore(lib, flags=tg.POOL_NEWONLY) == tg.ERR_INVALID_ARG  # new_from missing
+    big = _tree()
+    big.cap = 4096                                                  # variant LDS > 160 KiB
+    assert _rescore(lib, tree=big, flags=tg.GRAFT_OVERWRITE) == tg.ERR_UNSUPPORTED
     assert _rescore(lib, nx=P) == tg.ERR_INVALID_ARG              # n_next missing
     assert _rescore(lib, nx=P, nn=P, N=0) == tg.ERR_INVALID_ARG   # N must be >= 1
     assert _rescore(lib, M=100, V=5000) == tg.ERR_UNSUPPORTED
     assert _rescore(lib, ws=NULL) == tg.ERR_WORKSPACE
     need = lib.tg_rescore_graft_workspace(1, 17, 1000, 8, 4, 64)
     assert _rescore(lib, wsb=need - 1) == tg.ERR_WORKSPACE
+
+
+def test_accept_logits_host_checks(lib):
+    import paper_2608_26112_amd as tg
+
+    def acc(**kw):
+        a = dict(parent=P, token=P, n=P, logits=P, B=1, cap=16, R=17, V=100, md=16, g=P, A=P,
+                 path=P, bonus=P)
+        a.update(kw)
+        return lib.tg_tree_accept_logits(a["parent"], a["token"], a["n"], a["logits"], a["B"],
+                                         a["cap"], a["R"], a["V"], a["md"], a["g"], a["A"],
+                                         a["path"], a["bonus"], NULL, NULL)
+    assert acc(logits=NULL) == tg.ERR_INVALID_ARG
+    assert acc(g=NULL) == tg.ERR_INVALID_ARG
+    assert acc(V=0) == tg.ERR_INVALID_ARG
+    assert acc(R=0) == tg.ERR_INVALID_ARG
+    assert acc(cap=5000) == tg.ERR_UNSUPPORTED
 
 
 def test_accept_host_checks(lib):
