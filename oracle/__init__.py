@@ -20,6 +20,12 @@ Grafting for Tree-Based Speculative Decoding):
     buffers (mask, position ids, retrieval paths).
   * ``attention.kv_compact`` - the cache update after acceptance: the accepted
     chain's K/V rows become the continuation of the prefix.
+  * ``tree.rescore_graft`` variants (flags) - the Sec. 4.4 ablations (pool =
+    the previous step's new nodes; overwriting graft) and a duplicate-sibling
+    filter; ``tree.accept_logits`` - acceptance from the target's arg-max.
+  * ``ngram.ngram_cache`` / ``ngram.expand_ngram`` - the n-gram small drafter
+    (appendix on the n-gram small drafter): the prefill top-m cache and the
+    suffix-match expansion with back-off and the most-frequent-token fallback.
   * ``signals.tree_signals`` / ``signals.margin`` - the ten candidate tree
     signals with the reselection preview frontier, and the scheduler's
     margin predictor forward pass (App. online observations; value system
@@ -35,4 +41,4 @@ attention), brute-force enumeration on tiny inputs, hand-derived golden cases
 under ``tests/golden/`` and invariants the paper's definitions fix.  No function
 here is "parity unpinned".
 """
-from . import attention, signals, tree  # noqa: F401
+from . import attention, ngram, signals, tree  # noqa: F401
