@@ -89,6 +89,8 @@ typedef enum { TG_F32 = 0, TG_BF16 = 1 } tg_dtype;
 #define TG_MAX_CAP 4096        /* tree capacity (nodes per tree, root excluded) */
 #define TG_MAX_EXPAND_CHILDREN 8192 /* F * K of one expand call                */
 #define TG_MAX_VERIFY_NODES 1024    /* N of one verify call                    */
+#define TG_MAX_NGRAM 16             /* n_max of the n-gram drafter             */
+#define TG_MAX_NGRAM_FRONTIER 1024  /* F of one n-gram expansion               */
 
 /*
  * Caller-owned draft tree, structure of arrays, one row of `cap` slots per
@@ -249,6 +251,53 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 int32_t *next_frontier, int32_t *n_next, int N,
                                 void *workspace, size_t ws_bytes,
                                 uint32_t *d_err, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* The n-gram small drafter (appendix on the n-gram small drafter): a
+ * training-free lookup that proposes children from the target's prefill.  */
+/*
+ * tg_ngram_cache builds the prefill cache of B sequences:
+ *   cand_tok[b, i, :], cand_logp[b, i, :] = the top-m tokens of logits row
+ *     (b, i) (the target's logits after x_<=i) by (logit desc, token asc) and
+ *     their log-probabilities fl(x - lse), lse as in tg_tree_expand_topk;
+ *     every row 0 <= i < L is cached;
+ *   fallback_pos[b] = the last position i < ctx_len[b] of the most frequent
+ *     token of context[b, :ctx_len[b]] (ties to the smallest token id), -1
+ *     for an empty context.
+ * logits [B, L, V] fp32; context [B, L] int32 (tokens in [0, V), others are
+ * skipped and raise BAD_NODE); ctx_len [B] int32 device; cand_tok [B, L, m]
+ * int32 out; cand_logp [B, L, m] fp32 out; fallback_pos [B] int32 out.
+ * 1 <= m <= min(V, TG_MAX_TOPK).  Device errors: NONFINITE, BAD_NODE.
+ *
+ * tg_tree_expand_ngram is one small-drafter step (Alg. 1 with the n-gram
+ * drafter).  For frontier node v (slot f) of tree b the prefix is
+ * context[b, :ctx_len[b]] followed by the tokens on v's root path; its
+ * matched position j is the latest end position in the context of its
+ * longest suffix of length n_max, n_max - 1, ..., 1 found there (the root's
+ * own prefix matches at ctx_len - 1), else fallback_pos[b] (BAD_NODE and
+ * ctx_len - 1 when that is not a context position).  v gets the K children
+ * (ids n_b + f*K + k) token = cand_tok[b, j, k], logp = cand_logp[b, j, k],
+ * cum = fl(cum(v) + logp), depth(v) + 1, visited 0; next_frontier / n_next
+ * as in tg_tree_expand_topk; match_pos[b, f] = j (-1 padded; may be NULL).
+ * 1 <= K <= m; 1 <= n_max <= TG_MAX_NGRAM; F <= TG_MAX_NGRAM_FRONTIER;
+ * F*K <= TG_MAX_EXPAND_CHILDREN; cap <= TG_MAX_CAP.
+ * Device errors: BAD_NODE (frontier id out of range: tree b unchanged);
+ * BAD_PREFIX (ctx_len outside [1, L]: unchanged); CAPACITY (unchanged).
+ */
+size_t tg_ngram_cache_workspace(int B, int L, int V, int m);
+
+tg_status tg_ngram_cache(const float *logits, const int32_t *context, const int32_t *ctx_len,
+                         int B, int L, int V, int m, int32_t *cand_tok, float *cand_logp,
+                         int32_t *fallback_pos, void *workspace, size_t ws_bytes,
+                         uint32_t *d_err, void *stream);
+
+tg_status tg_tree_expand_ngram(const tg_tree *tree, const int32_t *frontier,
+                               const int32_t *n_frontier, const int32_t *context,
+                               const int32_t *ctx_len, const int32_t *cand_tok,
+                               const float *cand_logp, const int32_t *fallback_pos, int B,
+                               int F, int L, int m, int K, int N, int n_max,
+                               int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
+                               uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Greedy acceptance (temperature 0; Sec. 3.2; App. E).                     */

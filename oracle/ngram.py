@@ -24,7 +24,8 @@ Readings where the appendix is silent (applied identically in the library):
   * "most frequent token": highest count in x_<ctx_len, ties to the smallest
     token id; its position = its last occurrence;
   * an empty context (ctx_len = 0) has nothing to propose: BAD_PREFIX, the
-    tree is left unchanged.
+    tree is left unchanged; a fallback position outside the context raises
+    BAD_NODE and the last context position is used.
 Every node ranking uses (cum desc, depth asc, id asc), as in expand.
 """
 from __future__ import annotations
@@ -44,7 +45,6 @@ def ngram_cache(logits: np.ndarray, context: np.ndarray, ctx_len: np.ndarray, m:
     B, L, V = logits.shape
     tok = np.zeros((B, L, m), np.int32)
     lp = np.zeros((B, L, m), np.float32)
-    fb = np.full(B, -1, np.int32)
     err = 0
     for b in range(B):
         for i in range(L):
@@ -55,6 +55,18 @@ def ngram_cache(logits: np.ndarray, context: np.ndarray, ctx_len: np.ndarray, m:
             t, x = T.row_topk(logits[b, i], m)
             tok[b, i] = t
             lp[b, i] = [T.edge_logp(v, lse) for v in x]
+    fb, e2 = fallback_position(context, ctx_len, V)
+    return tok, lp, fb, err | e2
+
+
+def fallback_position(context: np.ndarray, ctx_len: np.ndarray, V: int):
+    """Last position of the most frequent context token (ties to the smallest
+    token id; tokens outside [0, V) are skipped with BAD_NODE); -1 for an empty
+    context.  Returns (fallback_pos [B], err)."""
+    B = context.shape[0]
+    fb = np.full(B, -1, np.int32)
+    err = 0
+    for b in range(B):
         n = int(ctx_len[b])
         ctx = [int(x) for x in context[b, :n]]
         if any(x < 0 or x >= V for x in ctx):
@@ -66,7 +78,7 @@ def ngram_cache(logits: np.ndarray, context: np.ndarray, ctx_len: np.ndarray, m:
                 counts[x] = counts.get(x, 0) + 1
             best = min(counts, key=lambda x: (-counts[x], x))
             fb[b] = max(i for i in range(n) if int(context[b, i]) == best)
-    return tok, lp, fb, err
+    return fb, err
 
 
 def match_position(ctx, prefix, n_max: int):
@@ -117,6 +129,9 @@ def expand_ngram(tree: T.Tree, frontier: np.ndarray, n_frontier, context: np.nda
             j = match_position(ctx, ctx + path, n_max)
             if j < 0:
                 j = int(fallback_pos[b])
+                if not 0 <= j < Lb:          # not a context position
+                    err |= T.DERR_BAD_NODE
+                    j = Lb - 1
             pos_out[b, f] = j
             cum_v = F32(0.0) if v == -1 else t.cum[b, v]
             d_v = 0 if v == -1 else int(t.depth[b, v])

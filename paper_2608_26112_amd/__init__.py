@@ -51,6 +51,9 @@ EXPORTED = (
     "tg_tree_expand_topk",
     "tg_rescore_graft_workspace",
     "tg_tree_rescore_graft",
+    "tg_ngram_cache_workspace",
+    "tg_ngram_cache",
+    "tg_tree_expand_ngram",
     "tg_tree_accept_logits",
     "tg_tree_accept",
     "tg_tree_global_prune",
@@ -118,6 +121,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                            _vp])
     lib.tg_tree_accept.restype = _i32
     lib.tg_tree_accept.argtypes = [_vp] * 4 + [_i32] * 3 + [_vp] * 5
+    lib.tg_ngram_cache_workspace.restype = _sz
+    lib.tg_ngram_cache_workspace.argtypes = [_i32] * 4
+    lib.tg_ngram_cache.restype = _i32
+    lib.tg_ngram_cache.argtypes = [_vp] * 3 + [_i32] * 4 + [_vp] * 4 + [_sz, _vp, _vp]
+    lib.tg_tree_expand_ngram.restype = _i32
+    lib.tg_tree_expand_ngram.argtypes = ([ctypes.POINTER(TgTree)] + [_vp] * 7 + [_i32] * 7 +
+                                         [_vp] * 5)
     lib.tg_tree_accept_logits.restype = _i32
     lib.tg_tree_accept_logits.argtypes = [_vp] * 4 + [_i32] * 5 + [_vp] * 6
     lib.tg_tree_reset.restype = _i32
@@ -283,6 +293,66 @@ def expand_topk(tree: TreeState, logits, frontier, n_frontier, K, N, row_lse=Non
                                  _ptr(d_err), _stream(stream))
     _check("tg_tree_expand_topk", st)
     return row_lse, next_frontier, n_next
+
+
+def ngram_cache(logits, context, ctx_len, m, cand_tok=None, cand_logp=None,
+                fallback_pos=None, workspace=None, d_err=None, stream=None):
+    """n-gram drafter prefill cache.  logits [B,L,V] fp32 (row i = after
+    x_<=i), context [B,L] int32, ctx_len [B] int32.  Returns (cand_tok
+    [B,L,m], cand_logp [B,L,m], fallback_pos [B])."""
+    lib = load()
+    _dev(logits, "logits", torch.float32)
+    _dev(context, "context", torch.int32)
+    _dev(ctx_len, "ctx_len", torch.int32)
+    B, L, V = logits.shape
+    if tuple(context.shape) != (B, L):
+        raise ValueError("context must be [B, L]")
+    dev = logits.device
+    cand_tok = (torch.empty((B, L, m), dtype=torch.int32, device=dev)
+                if cand_tok is None else cand_tok)
+    cand_logp = (torch.empty((B, L, m), dtype=torch.float32, device=dev)
+                 if cand_logp is None else cand_logp)
+    fallback_pos = (torch.empty((B,), dtype=torch.int32, device=dev)
+                    if fallback_pos is None else fallback_pos)
+    ws, wsb = _workspace(lib.tg_ngram_cache_workspace(B, L, V, m), dev, workspace)
+    st = lib.tg_ngram_cache(_ptr(logits), _ptr(context), _ptr(ctx_len), B, L, V, m,
+                            _ptr(cand_tok), _ptr(cand_logp), _ptr(fallback_pos), _ptr(ws), wsb,
+                            _ptr(d_err), _stream(stream))
+    _check("tg_ngram_cache", st)
+    return cand_tok, cand_logp, fallback_pos
+
+
+def expand_ngram(tree: TreeState, frontier, n_frontier, context, ctx_len, cand_tok, cand_logp,
+                 fallback_pos, K, N, n_max, match_pos=None, next_frontier=None, n_next=None,
+                 d_err=None, stream=None):
+    """One small-drafter step with the n-gram drafter (see
+    tg_tree_expand_ngram).  Returns (next_frontier, n_next, match_pos)."""
+    lib = load()
+    for t, n in ((frontier, "frontier"), (context, "context"), (ctx_len, "ctx_len"),
+                 (cand_tok, "cand_tok"), (fallback_pos, "fallback_pos")):
+        _dev(t, n, torch.int32)
+    _dev(cand_logp, "cand_logp", torch.float32)
+    if n_frontier is not None:
+        _dev(n_frontier, "n_frontier", torch.int32)
+    B, F = frontier.shape
+    L = context.shape[1]
+    m = cand_tok.shape[2]
+    if tuple(cand_tok.shape) != (B, L, m) or tuple(cand_logp.shape) != (B, L, m):
+        raise ValueError("cand_tok / cand_logp must be [B, L, m]")
+    dev = frontier.device
+    match_pos = (torch.empty((B, F), dtype=torch.int32, device=dev)
+                 if match_pos is None else match_pos)
+    next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
+                     if next_frontier is None else next_frontier)
+    n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
+    ts = tree.struct()
+    st = lib.tg_tree_expand_ngram(ctypes.byref(ts), _ptr(frontier), _ptr(n_frontier),
+                                  _ptr(context), _ptr(ctx_len), _ptr(cand_tok), _ptr(cand_logp),
+                                  _ptr(fallback_pos), B, F, L, m, K, N, n_max, _ptr(match_pos),
+                                  _ptr(next_frontier), _ptr(n_next), _ptr(d_err),
+                                  _stream(stream))
+    _check("tg_tree_expand_ngram", st)
+    return next_frontier, n_next, match_pos
 
 
 def rescore_graft_workspace(B, R, V, W, M, cap) -> int:

@@ -173,6 +173,58 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                           flags, new_from, d_err, st));
 }
 
+// ------------------------------------------------------------ n-gram drafter
+size_t tg_ngram_cache_workspace(int B, int L, int V, int m) {
+  if (B <= 0 || L <= 0 || V <= 0 || m <= 0) return 0;
+  return row_ws((long long)B * L, V, m, (size_t)B * V * sizeof(int32_t)).bytes;
+}
+
+tg_status tg_ngram_cache(const float *logits, const int32_t *context, const int32_t *ctx_len,
+                         int B, int L, int V, int m, int32_t *cand_tok, float *cand_logp,
+                         int32_t *fallback_pos, void *workspace, size_t ws_bytes,
+                         uint32_t *d_err, void *stream) {
+  if (!logits || !context || !ctx_len || !cand_tok || !cand_logp || !fallback_pos)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || L <= 0 || V <= 0 || m <= 0 || m > V) return TG_ERR_INVALID_ARG;
+  if (m > TG_MAX_TOPK) return TG_ERR_UNSUPPORTED;
+  RowWs w = row_ws((long long)B * L, V, m, (size_t)B * V * sizeof(int32_t));
+  if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
+  tg::RowPlan plan = tg::plan_rows((long long)B * L, V);
+  char *ws = static_cast<char *>(workspace);
+  float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
+  uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
+  int32_t *counts = reinterpret_cast<int32_t *>(ws + w.extra_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = tg::launch_row_partials(logits, B, L, V, m, plan, nullptr, nullptr, ms, keys,
+                                         d_err, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  e = tg::launch_ngram_cache((long long)B * L, m, plan, ms, keys, cand_tok, cand_logp, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(
+      tg::launch_ngram_fallback(context, ctx_len, B, L, V, counts, fallback_pos, d_err, st));
+}
+
+tg_status tg_tree_expand_ngram(const tg_tree *tree, const int32_t *frontier,
+                               const int32_t *n_frontier, const int32_t *context,
+                               const int32_t *ctx_len, const int32_t *cand_tok,
+                               const float *cand_logp, const int32_t *fallback_pos, int B,
+                               int F, int L, int m, int K, int N, int n_max,
+                               int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
+                               uint32_t *d_err, void *stream) {
+  if (!tree_ok(tree) || !frontier || !context || !ctx_len || !cand_tok || !cand_logp ||
+      !fallback_pos || !next_frontier || !n_next)
+    return TG_ERR_INVALID_ARG;
+  if (B <= 0 || F <= 0 || L <= 0 || m <= 0 || K <= 0 || K > m || N <= 0 || n_max <= 0)
+    return TG_ERR_INVALID_ARG;
+  if (n_max > TG_MAX_NGRAM || F > TG_MAX_NGRAM_FRONTIER ||
+      (long long)F * K > TG_MAX_EXPAND_CHILDREN || tree->cap > TG_MAX_CAP)
+    return TG_ERR_UNSUPPORTED;
+  return from_hip(tg::launch_ngram_expand(*tree, frontier, n_frontier, B, F, context, ctx_len,
+                                          L, cand_tok, cand_logp, fallback_pos, m, K, N, n_max,
+                                          match_pos, next_frontier, n_next, d_err,
+                                          reinterpret_cast<hipStream_t>(stream)));
+}
+
 // ------------------------------------------------------------------- accept
 tg_status tg_tree_accept(const int32_t *parent, const int32_t *token,
                          const int32_t *n_nodes, const int32_t *greedy, int B,

@@ -1,0 +1,252 @@
+// The n-gram small drafter (the paper's appendix on the n-gram small
+// drafter): a prefill cache of the target's top-m next tokens per context
+// position, and the small-step expansion that matches each frontier node's
+// prefix suffix against the context (longest n-gram first, shorter on a miss,
+// the most frequent context token's position as the last resort) and grows
+// the node's children from the matched position's cache row.
+//
+// ngram_cache_kernel: one wave per context position; the position's logits
+//   row was already reduced by row_partial_kernel (lse partials and top-m
+//   chunk lists), the wave merges them: cand_logp = fl(x - lse).
+// ngram_fallback_kernel: one workgroup per sequence; token counts by global
+//   atomics into a zeroed [V] slice, then the (count desc, token asc) best
+//   token and its last position, both as block maxima of packed keys.
+// ngram_expand_kernel: one workgroup per tree.  Per frontier node the whole
+//   block scans the context: end position j scores the length l(j) of the
+//   longest common suffix of x[..j] and the node's prefix (capped at n_max);
+//   the block maximum of (l, j) with l >= 1 is the latest longest match, which
+//   is what "longest n-gram first, shorter on a miss, latest occurrence"
+//   selects.  Children take ids n_b + f*K + k, then Top_N of them by
+//   (cum desc, depth asc, id asc).
+#include "tg_device.h"
+#include "tg_kernels.h"
+
+namespace tg {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+
+__global__ __launch_bounds__(kThreads) void ngram_cache_kernel(
+    long long rows, int m, int chunks, int n_ms, const float2 *__restrict__ part_ms,
+    const uint64_t *__restrict__ part_keys, int32_t *__restrict__ cand_tok,
+    float *__restrict__ cand_logp) {
+  extern __shared__ uint64_t wsmem[];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const long long r = (long long)blockIdx.x * kWaves + w;
+  if (r >= rows) return;  // wave-uniform
+  float lse = 0.0f;
+  if (lane == 0) lse = finish_lse(part_ms + r * n_ms, n_ms);
+  lse = __shfl(lse, 0, kWave);
+  const uint64_t key =
+      wave_finish_topk(part_keys + r * chunks * m, chunks, m, wsmem + (size_t)w * chunks * m);
+  if (lane < m) {
+    cand_tok[r * m + lane] = (int32_t)key_token(key);
+    cand_logp[r * m + lane] = edge_logp(key_logit(key), lse);
+  }
+}
+
+__device__ uint64_t block_max_u64(uint64_t v, uint64_t *red) {
+  v = wave_max_u64(v);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+  __syncthreads();
+  uint64_t r = red[0];
+  for (int i = 1; i < kWaves; ++i) r = red[i] > r ? red[i] : r;
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kThreads) void ngram_fallback_kernel(
+    const int32_t *__restrict__ context, const int32_t *__restrict__ ctx_len, int L, int V,
+    int32_t *__restrict__ counts, int32_t *__restrict__ fallback_pos, uint32_t *d_err) {
+  __shared__ uint64_t red[kWaves];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  int n = ctx_len[b];
+  n = n < 0 ? 0 : (n > L ? L : n);
+  int32_t *cnt = counts + (size_t)b * V;
+  const int32_t *ctx = context + (size_t)b * L;
+  for (int t = tid; t < V; t += kThreads) cnt[t] = 0;
+  __syncthreads();
+  bool bad = false;
+  for (int i = tid; i < n; i += kThreads) {
+    const int t = ctx[i];
+    if (t < 0 || t >= V) bad = true;
+    else atomicAdd(cnt + t, 1);
+  }
+  if (bad) report(d_err, TG_DERR_BAD_NODE);
+  __syncthreads();
+  // best token: count desc, token asc
+  uint64_t best = 0;
+  for (int t = tid; t < V; t += kThreads) {
+    const uint32_t c = (uint32_t)cnt[t];
+    if (c == 0) continue;
+    const uint64_t k = ((uint64_t)c << 32) | (uint64_t)(0xffffffffu - (uint32_t)t);
+    best = k > best ? k : best;
+  }
+  best = block_max_u64(best, red);
+  const int tok = best ? (int)(0xffffffffu - (uint32_t)best) : -1;
+  // its last position
+  uint64_t last = 0;
+  for (int i = tid; i < n; i += kThreads)
+    if (ctx[i] == tok) last = (uint64_t)(i + 1) > last ? (uint64_t)(i + 1) : last;
+  last = block_max_u64(last, red);
+  if (tid == 0) fallback_pos[b] = (int32_t)last - 1;
+}
+
+__global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
+    tg_tree tree, const int32_t *__restrict__ frontier, const int32_t *__restrict__ n_frontier,
+    int F, const int32_t *__restrict__ context, const int32_t *__restrict__ ctx_len, int L,
+    const int32_t *__restrict__ cand_tok, const float *__restrict__ cand_logp,
+    const int32_t *__restrict__ fallback_pos, int m, int K, int N, int n_max,
+    int32_t *__restrict__ match_pos, int32_t *__restrict__ next_frontier,
+    int32_t *__restrict__ n_next, uint32_t *d_err) {
+  extern __shared__ uint64_t skey[];  // [pow2(F*K)]
+  __shared__ uint64_t red[kWaves];
+  __shared__ int32_t suf[TG_MAX_NGRAM];
+  __shared__ int plen_s;
+  __shared__ int32_t posf[TG_MAX_NGRAM_FRONTIER];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int cap = tree.cap;
+  const size_t base = (size_t)b * cap;
+  int Fb = n_frontier ? n_frontier[b] : F;
+  Fb = Fb < 0 ? 0 : (Fb > F ? F : Fb);
+  const int nb = tree.n_nodes[b];
+  int Lb = ctx_len[b];
+  const int total = Fb * K;
+  const int32_t *ctx = context + (size_t)b * L;
+
+  bool bad = nb < 0 || nb > cap;
+  for (int f = tid; f < Fb; f += kThreads) {
+    const int v = frontier[(size_t)b * F + f];
+    bad |= v < -1 || v >= nb;
+  }
+  bad = __syncthreads_or(bad);
+  const bool no_ctx = !bad && (Lb <= 0 || Lb > L);
+  const bool full = !bad && !no_ctx && nb + total > cap;
+  for (int f = tid; f < F; f += kThreads)
+    if (match_pos) match_pos[(size_t)b * F + f] = -1;
+  if (bad || no_ctx || full) {
+    if (tid == 0) {
+      report(d_err, bad ? TG_DERR_BAD_NODE : (no_ctx ? TG_DERR_BAD_PREFIX : TG_DERR_CAPACITY));
+      n_next[b] = 0;
+    }
+    for (int j = tid; j < N; j += kThreads) next_frontier[(size_t)b * N + j] = TG_NO_NODE;
+    return;
+  }
+  int fb = fallback_pos[b];
+  if (fb < 0 || fb >= Lb) {
+    if (tid == 0) report(d_err, TG_DERR_BAD_NODE);
+    fb = Lb - 1;
+  }
+
+  // ---- matched position of every frontier node
+  for (int f = 0; f < Fb; ++f) {
+    if (tid == 0) {
+      // the prefix's last n_max tokens, newest first: the node's path, then
+      // the context's tail
+      int k = 0;
+      for (int u = frontier[(size_t)b * F + f]; u >= 0 && k < n_max; ++k) {
+        suf[k] = tree.token[base + u];
+        const int p = tree.parent[base + u];
+        u = (p < -1 || p >= u) ? -1 : p;
+      }
+      for (int i = Lb - 1; i >= 0 && k < n_max; --i, ++k) suf[k] = ctx[i];
+      plen_s = k;
+    }
+    __syncthreads();
+    const int plen = plen_s;
+    uint64_t best = 0;
+    for (int j = tid; j < Lb; j += kThreads) {
+      int l = 0;
+      const int lim = min(plen, j + 1);
+      while (l < lim && ctx[j - l] == suf[l]) ++l;
+      if (l > 0) {
+        const uint64_t key = ((uint64_t)l << 32) | (uint64_t)j;
+        best = key > best ? key : best;
+      }
+    }
+    best = block_max_u64(best, red);
+    if (tid == 0) {
+      const int pos = best ? (int)(uint32_t)best : fb;
+      posf[f] = pos;
+      if (match_pos) match_pos[(size_t)b * F + f] = pos;
+    }
+  }
+  __syncthreads();
+
+  // ---- children from the cache rows, then Top_N
+  const int P2 = pow2_at_least(total > 0 ? total : 1);
+  for (int c = tid; c < P2; c += kThreads) {
+    if (c >= total) {
+      skey[c] = 0;
+      continue;
+    }
+    const int f = c / K, k = c - f * K;
+    const int v = frontier[(size_t)b * F + f];
+    const size_t row = ((size_t)b * L + posf[f]) * m + k;
+    const float cv = v < 0 ? 0.0f : tree.cum[base + v];
+    const int dv = v < 0 ? 0 : tree.depth[base + v];
+    const float lp = cand_logp[row];
+    const float cum = __fadd_rn(cv, lp);
+    const int id = nb + c;
+    tree.parent[base + id] = v;
+    tree.token[base + id] = cand_tok[row];
+    tree.depth[base + id] = dv + 1;
+    tree.logp[base + id] = lp;
+    tree.cum[base + id] = cum;
+    tree.visited[base + id] = 0;
+    skey[c] = node_key(cum, dv + 1, id);
+  }
+  __syncthreads();
+  const int nn = min(N, total);
+  block_top_keys<kThreads>(skey, total, P2, nn);
+  for (int j = tid; j < N; j += kThreads)
+    next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
+  if (tid == 0) {
+    n_next[b] = nn;
+    tree.n_nodes[b] = nb + total;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_ngram_cache(long long rows, int m, RowPlan plan, const float2 *part_ms,
+                              const uint64_t *part_keys, int32_t *cand_tok, float *cand_logp,
+                              hipStream_t stream) {
+  const size_t lds = (size_t)kWaves * plan.chunks * m * sizeof(uint64_t);
+  hipError_t e = hipFuncSetAttribute((const void *)ngram_cache_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const long long grid = (rows + kWaves - 1) / kWaves;
+  launch("ngram_cache", ngram_cache_kernel, dim3((unsigned)grid), dim3(kThreads), lds, stream,
+         rows, m, plan.chunks, plan.ms_per_row, part_ms, part_keys, cand_tok, cand_logp);
+  return hipGetLastError();
+}
+
+hipError_t launch_ngram_fallback(const int32_t *context, const int32_t *ctx_len, int B, int L,
+                                 int V, int32_t *counts, int32_t *fallback_pos, uint32_t *d_err,
+                                 hipStream_t stream) {
+  launch("ngram_fallback", ngram_fallback_kernel, dim3(B), dim3(kThreads), 0, stream, context,
+         ctx_len, L, V, counts, fallback_pos, d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_ngram_expand(const tg_tree &tree, const int32_t *frontier,
+                               const int32_t *n_frontier, int B, int F,
+                               const int32_t *context, const int32_t *ctx_len, int L,
+                               const int32_t *cand_tok, const float *cand_logp,
+                               const int32_t *fallback_pos, int m, int K, int N, int n_max,
+                               int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
+                               uint32_t *d_err, hipStream_t stream) {
+  const size_t lds = (size_t)pow2_at_least(F * K > 0 ? F * K : 1) * sizeof(uint64_t);
+  hipError_t e = hipFuncSetAttribute((const void *)ngram_expand_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  launch("ngram_expand", ngram_expand_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
+         frontier, n_frontier, F, context, ctx_len, L, cand_tok, cand_logp, fallback_pos, m, K,
+         N, n_max, match_pos, next_frontier, n_next, d_err);
+  return hipGetLastError();
+}
+
+}  // namespace tg

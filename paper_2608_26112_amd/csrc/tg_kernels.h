@@ -75,6 +75,20 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                uint32_t *d_err, hipStream_t stream);
 
 // ----------------------------------------------------------------- accept
+// n-gram small drafter
+hipError_t launch_ngram_cache(long long rows, int m, RowPlan plan, const float2 *part_ms,
+                              const uint64_t *part_keys, int32_t *cand_tok, float *cand_logp,
+                              hipStream_t stream);
+hipError_t launch_ngram_fallback(const int32_t *context, const int32_t *ctx_len, int B, int L,
+                                 int V, int32_t *counts, int32_t *fallback_pos, uint32_t *d_err,
+                                 hipStream_t stream);
+hipError_t launch_ngram_expand(const tg_tree &tree, const int32_t *frontier,
+                               const int32_t *n_frontier, int B, int F,
+                               const int32_t *context, const int32_t *ctx_len, int L,
+                               const int32_t *cand_tok, const float *cand_logp,
+                               const int32_t *fallback_pos, int m, int K, int N, int n_max,
+                               int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
+                               uint32_t *d_err, hipStream_t stream);
 hipError_t launch_argmax_rows(const float *logits, const int32_t *n_nodes, int B, int cap,
                               int R, int V, int32_t *greedy, uint32_t *d_err,
                               hipStream_t stream);

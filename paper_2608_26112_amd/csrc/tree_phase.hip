@@ -21,38 +21,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
-// ------------------------------------------------------- finishing rows
-// log-sum-exp of one row from its per-grain (max, sum-exp) partials, folded
-// in grain order (the same bits whatever the call's chunking).
-__device__ float finish_lse(const float2 *__restrict__ ms, int n) {
-  float m = -__builtin_inff(), s = 0.0f;
-#pragma unroll 8
-  for (int i = 0; i < n; ++i) {
-    const float2 p = ms[i];
-    merge_ms(m, s, p.x, p.y);
-  }
-  return m == -__builtin_inff() ? -__builtin_inff() : m + logf(s);
-}
-
-// K-round merge of one row's `chunks` sorted lists (each K keys, best
-// first) staged in LDS at `lists`: lane c holds list c's head, the wave takes
-// the largest head, that list advances.  Lane j < K returns the j-th best key.
-__device__ uint64_t wave_merge_lists(const uint64_t *lists, int chunks, int K) {
-  const int lane = threadIdx.x & (kWave - 1);
-  int idx = 0;
-  uint64_t head = lane < chunks ? lists[lane * K] : 0;
-  uint64_t mine = 0;
-  for (int j = 0; j < K; ++j) {
-    const uint64_t best = wave_max_u64(head);
-    if (head == best && best != 0) {
-      ++idx;
-      head = idx < K ? lists[lane * K + idx] : 0;
-    }
-    if (lane == j) mine = best;
-  }
-  return mine;
-}
-
 // Top-K of nr consecutive rows (row r's `chunks` lists of K keys at
 // lists + r * chunks * K) into out[r * K + j], best first.  The lists are
 // staged in LDS (`stage`, room for stage_cap >= chunks * K keys) with one
@@ -78,22 +46,6 @@ __device__ void block_finish_topk(const uint64_t *__restrict__ lists, int chunks
     }
     __syncthreads();
   }
-}
-
-// One wave finishes one row's top-K: lane j < K returns the j-th best key.
-// `ws` is this wave's LDS scratch (chunks * K keys).  chunks <= 64.
-__device__ uint64_t wave_finish_topk(const uint64_t *__restrict__ lists, int chunks, int K,
-                                     uint64_t *ws) {
-  const int lane = threadIdx.x & (kWave - 1);
-  if (chunks == 1) return lane < K ? lists[lane] : 0;
-  const int nk = chunks * K;
-  for (int i = lane; i < nk; i += kWave) ws[i] = lists[i];
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const uint64_t r = wave_merge_lists(ws, chunks, K);
-  __builtin_amdgcn_wave_barrier();   // ws is reused by the wave's next row
-  return r;
 }
 
 __device__ __forceinline__ int sane_parent(int p, int v, bool &bad) {

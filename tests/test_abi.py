@@ -160,6 +160,38 @@ def test_rescore_host_checks(lib):
     assert _rescore(lib, wsb=need - 1) == tg.ERR_WORKSPACE
 
 
+def test_ngram_host_checks(lib):
+    import paper_2608_26112_amd as tg
+
+    def cache(**kw):
+        a = dict(logits=P, ctx=P, clen=P, B=1, L=32, V=100, m=4, tok=P, lp=P, fb=P, ws=P,
+                 wsb=1 << 30)
+        a.update(kw)
+        return lib.tg_ngram_cache(a["logits"], a["ctx"], a["clen"], a["B"], a["L"], a["V"],
+                                  a["m"], a["tok"], a["lp"], a["fb"], a["ws"], a["wsb"], NULL,
+                                  NULL)
+    assert cache(logits=NULL) == tg.ERR_INVALID_ARG
+    assert cache(m=101) == tg.ERR_INVALID_ARG
+    assert cache(m=65, V=1000) == tg.ERR_UNSUPPORTED
+    assert cache(ws=NULL) == tg.ERR_WORKSPACE
+    assert cache(wsb=lib.tg_ngram_cache_workspace(1, 32, 100, 4) - 1) == tg.ERR_WORKSPACE
+
+    def expand(**kw):
+        a = dict(fr=P, nf=NULL, ctx=P, clen=P, tok=P, lp=P, fb=P, B=1, F=4, L=32, m=4, K=2,
+                 N=4, n=3, mp=NULL, nx=P, nn=P)
+        a.update(kw)
+        t = _tree()
+        return lib.tg_tree_expand_ngram(ctypes.byref(t), a["fr"], a["nf"], a["ctx"], a["clen"],
+                                        a["tok"], a["lp"], a["fb"], a["B"], a["F"], a["L"],
+                                        a["m"], a["K"], a["N"], a["n"], a["mp"], a["nx"],
+                                        a["nn"], NULL, NULL)
+    assert expand(ctx=NULL) == tg.ERR_INVALID_ARG
+    assert expand(K=5) == tg.ERR_INVALID_ARG                      # K > m
+    assert expand(n=0) == tg.ERR_INVALID_ARG
+    assert expand(n=17) == tg.ERR_UNSUPPORTED
+    assert expand(F=2000) == tg.ERR_UNSUPPORTED
+
+
 def test_accept_logits_host_checks(lib):
     import paper_2608_26112_amd as tg
 

@@ -31,6 +31,7 @@ __all__ = [
     "greedy_match_random_child",
     "greedy_match_first_child",
     "verify_layout_with_root",
+    "token_stream",
     "CONFIGS",
 ]
 
@@ -218,6 +219,22 @@ def verify_layout_with_root(parent: np.ndarray) -> np.ndarray:
     vp[0] = -1
     vp[1:] = parent + 1
     return vp
+
+
+def token_stream(g: np.random.Generator, length: int, vocab: int, n_phrases: int = 32,
+                 phrase_len=(2, 8), p_phrase: float = 0.6) -> np.ndarray:
+    """Synthetic prompt: a bank of random phrases (lengths in phrase_len) that
+    recur through the stream, interleaved with single random tokens, so that
+    n-grams of every length repeat as in real prompts.  int32 [length]."""
+    lo, hi = phrase_len
+    bank = [g.integers(0, vocab, int(g.integers(lo, hi + 1))) for _ in range(n_phrases)]
+    out = []
+    while len(out) < length:
+        if g.random() < p_phrase:
+            out.extend(int(x) for x in bank[int(g.integers(0, n_phrases))])
+        else:
+            out.append(int(g.integers(0, vocab)))
+    return np.asarray(out[:length], dtype=np.int32)
 
 
 # Shapes of the five workloads (the sizes the paper's setting implies; see the
