@@ -6,11 +6,18 @@ Llama-3-8B-shaped workload (batch 1, vocabulary 128256, frontier W = 10,
 m = 8 children per node, 32/8 heads, head_dim 128, prefix 2048, bf16):
 
   reset          the shared tree becomes the lone root (T_1 = {r}, P_1 = {})
+  every step     tg_tree_signals        the scheduler's ten tree signals and
+                                        its margin predictor (the action it
+                                        returns is overridden by the fixed
+                                        schedule below, so the tree is the same
+                                        every turn)
   k=1  middle    tg_tree_rescore_graft  pool {root}: graft its top-8 children
-  k=2  small     tg_tree_expand_topk    expand Top_W of the grafted children
+  k=2  small     tg_tree_expand_ngram   the n-gram drafter expands Top_W of
+                                        the grafted children from the prefill
+                                        cache (8 candidates per position)
   k=3  middle    tg_tree_rescore_graft  pool = 72 unvisited nodes, rescore,
                                         reselect 10 graft points, +80 nodes
-  k=4  small     tg_tree_expand_topk    expand Top_W of those 80
+  k=4  small     tg_tree_expand_ngram   expand Top_W of those 80
   k=5  middle    tg_tree_rescore_graft  pool = 160 nodes, rescore, +80 nodes
   prune          tg_tree_global_prune   the 312-node tree -> 64 nodes (Alg. 3)
                                         + verification buffers
@@ -20,9 +27,13 @@ m = 8 children per node, 32/8 heads, head_dim 128, prefix 2048, bf16):
   accept         tg_tree_accept         greedy acceptance on the pruned tree
   cache          tg_kv_compact          the accepted rows extend the prefix
 
-The schedule [1,0,1,0,1] is the paper's fixed ablation schedule (Sec. 5.3).
+The schedule [1,0,1,0,1] is the paper's fixed ablation schedule (Sec. 5.3);
+the small drafter is the paper's n-gram drafter, whose cache (the target's
+top-8 next tokens at each of the 2048 prompt positions) is built once per
+input copy at set-up, as at prefill.
 Drafter and target logits, Q/K/V and tokens are seeded synthetic data of the
-workload's shapes and distributions (logits N(0,3) fp32; Q/K/V N(0,1)/sqrt(128)
+workload's shapes and distributions (logits N(0,3) fp32; the prompt a token
+stream of recurring phrases; Q/K/V N(0,1)/sqrt(128)
 bf16; the target's greedy token at each pruned-tree node is its first child's
 token with p = 0.7, fixed once per input copy from the tree the turn builds).  Inputs rotate over several resident copies (> the 256 MB MALL) so no
 timed read is served from the last-level cache.
@@ -62,6 +73,7 @@ B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64     # N_VER = B_ver pruned nod
 CAP = 512
 MAX_DEPTH = 8            # accept path width (the turn's trees are at most 5 deep)
 R_ROWS = 313             # strong-logits rows (root + up to 312 nodes)
+NG_NMAX = 4              # n-gram drafter: longest n-gram matched
 
 
 def parse():
@@ -120,13 +132,32 @@ def make_inputs(c, dev):
     for r0 in range(0, R_ROWS, 32):        # chunks keep host memory small
         r1 = min(R_ROWS, r0 + 32)
         strong[0, r0:r1] = torch.from_numpy(W.normal(g, (r1 - r0, V), 3.0)).to(dev)
-    weak = [torch.from_numpy(W.normal(g, (B, W_FR, V), 3.0)).to(dev) for _ in range(2)]
     s = np.float32(1.0 / np.sqrt(128.0))
     S = L + N_VER
     q = torch.from_numpy(W.normal(g, (B, N_VER, HQ, D)) * s).to(dev).bfloat16()
     k = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
     v = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
-    return dict(strong=strong, weak=weak, q=q, k=k, v=v)
+    # the prompt and the target's prefill logits over it (row i = after x_<=i)
+    ctx = W.token_stream(g, L, V, n_phrases=64)[None]
+    prefill = torch.empty((B, L, V), dtype=torch.float32, device=dev)
+    for r0 in range(0, L, 64):
+        prefill[0, r0:r0 + 64] = torch.from_numpy(W.normal(W.rng([1002, c, 9, r0]), (64, V),
+                                                           3.0)).to(dev)
+    # the scheduler's inputs: predictor weights and each step's runtime
+    # context + history encoding (11 values)
+    params = torch.from_numpy(W.normal(g, (3265,), 0.1)).to(dev)
+    sched_ctx = torch.from_numpy(W.normal(g, (len(SCHEDULE), B, 11), 1.0)).to(dev)
+    return dict(strong=strong, q=q, k=k, v=v, ctx=torch.from_numpy(ctx).to(dev),
+                prefill=prefill, params=params, sched_ctx=sched_ctx)
+
+
+def prefill_host(c):
+    """Host copy of input copy c's prefill logits (the same seeded draws)."""
+    import workloads as W
+    out = np.empty((B, L, V), np.float32)
+    for r0 in range(0, L, 64):
+        out[0, r0:r0 + 64] = W.normal(W.rng([1002, c, 9, r0]), (64, V), 3.0)
+    return out
 
 
 def greedy_for(tree_host):
@@ -150,14 +181,25 @@ class Step:
         # zero-filled once (the library's row counters start at zero)
         self.ws_r = torch.zeros(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
                                 dtype=torch.uint8, device=dev)
-        self.ws_e = torch.zeros(tg.expand_topk_workspace(B, W_FR, V, M_CH, W_FR),
-                                dtype=torch.uint8, device=dev)
+        # n-gram drafter: the prefill cache (built once, untimed)
+        self.clen = torch.full((B,), L, **i32)
+        ws_c = torch.zeros(tg.ngram_cache_workspace(B, L, V, M_CH), dtype=torch.uint8,
+                           device=dev)
+        self.c_tok, self.c_lp, self.c_fb = tg.ngram_cache(inp["prefill"], inp["ctx"], self.clen,
+                                                          M_CH, workspace=ws_c)
+        torch.cuda.synchronize()
+        del ws_c
+        self.mpos = [torch.empty((B, W_FR), **i32) for _ in range(2)]
+        self.root_fr = torch.full((B, 1), -1, **i32)
+        self.sig = [torch.empty((B, 10), dtype=torch.float32, device=dev)
+                    for _ in SCHEDULE]
+        self.margin = [torch.empty((B,), dtype=torch.float32, device=dev) for _ in SCHEDULE]
+        self.action = [torch.empty((B,), **i32) for _ in SCHEDULE]
         nv = tg.verify_attention_workspace(B, N_VER, HQ, HKV, D, L + N_VER, tg.BF16)
         self.ws_v = torch.zeros(max(nv, 1), dtype=torch.uint8, device=dev)
         self.r_lse = [torch.empty((B, R_ROWS), dtype=torch.float32, device=dev) for _ in range(3)]
         self.gf = [torch.empty((B, W_FR), **i32) for _ in range(3)]
         self.ng = [torch.empty((B,), **i32) for _ in range(3)]
-        self.e_lse = [torch.empty((B, W_FR), dtype=torch.float32, device=dev) for _ in range(2)]
         self.fr = [torch.empty((B, W_FR), **i32) for _ in range(5)]
         self.nn = [torch.empty((B,), **i32) for _ in range(5)]
         M = N_VER + 1
@@ -180,16 +222,22 @@ class Step:
         tg.tree_reset(t)
         mid, small = 0, 0
         for k, a in enumerate(SCHEDULE):
+            # the scheduler's pre-action state (its action is not used)
+            fr_k, nf_k = (self.root_fr, None) if k == 0 else (self.fr[k - 1], self.nn[k - 1])
+            tg.tree_signals(t, fr_k, nf_k, W_FR, 5, context=x["sched_ctx"][k],
+                            params=x["params"], signals=self.sig[k], margin=self.margin[k],
+                            action=self.action[k])
             if a == 1:       # middle-drafter step
                 tg.rescore_graft(t, x["strong"], W_FR, M_CH, row_lse=self.r_lse[mid],
                                  graft_frontier=self.gf[mid], n_graft=self.ng[mid], N=W_FR,
                                  next_frontier=self.fr[k], n_next=self.nn[k],
                                  workspace=self.ws_r)
                 mid += 1
-            else:            # small-drafter step over the previous step's new nodes
-                tg.expand_topk(t, x["weak"][small], self.fr[k - 1], self.nn[k - 1], M_CH, W_FR,
-                               row_lse=self.e_lse[small], next_frontier=self.fr[k],
-                               n_next=self.nn[k], workspace=self.ws_e)
+            else:            # small (n-gram) step over the previous step's new nodes
+                tg.expand_ngram(t, self.fr[k - 1], self.nn[k - 1], x["ctx"], self.clen,
+                                self.c_tok, self.c_lp, self.c_fb, M_CH, W_FR, NG_NMAX,
+                                match_pos=self.mpos[small], next_frontier=self.fr[k],
+                                n_next=self.nn[k])
                 small += 1
         p = tg.global_prune(t, N_VER, MAX_DEPTH + 1, out=self.pr)
         tg.verify_attention(x["q"], x["k"], x["v"], p["vparent"], self.plen, D ** -0.5,
@@ -203,14 +251,19 @@ class Step:
 # ------------------------------------------------------------ accounting
 
 def rows_read_per_step():
-    """Logits rows one step reads (structural: independent of the values).
-    k=1 pool {root}: row 0.  k=2: the 8 frontier rows.  k=3 pool = 72
-    unvisited nodes: their 72 rows + the root row (parent of 8 of them).
-    k=4: 10 rows.  k=5 pool = 160 nodes: their rows + the rows of the 10
-    graft points of k=3 (parents of 80 of them, already visited)."""
-    rescore = [1, 73, 170]
-    expand = [8, 10]
-    return rescore, expand
+    """Middle-drafter logits rows one turn reads (structural: independent of
+    the values).  k=1 pool {root}: row 0.  k=3 pool = 72 unvisited nodes:
+    their 72 rows + the root row (parent of 8 of them).  k=5 pool = 160
+    nodes: their rows + the rows of the 10 graft points of k=3 (parents of 80
+    of them, already visited)."""
+    return [1, 73, 170]
+
+
+def ngram_bytes_per_step():
+    """Bytes the two n-gram steps read: the prompt once per step (4 B a
+    token) and the matched cache rows of their 8 and 10 frontier nodes (8
+    candidates of 8 B: token + log-probability)."""
+    return sum(L * 4 + f * M_CH * 8 for f in (8, 10))
 
 
 def path_len_sum(vpar):
@@ -247,8 +300,15 @@ def cpu_baseline(inp, greedy0, budget_s):
         blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         blas = 1
+    from oracle import ngram as NG
+    from oracle import signals as OS
     strong = inp["strong"].cpu().numpy()
-    weak = [w.cpu().numpy() for w in inp["weak"]]
+    ctx = inp["ctx"].cpu().numpy()
+    clen = np.array([L], np.int32)
+    # the prefill cache (set-up, untimed, as on the GPU side)
+    c_tok, c_lp, c_fb, _ = NG.ngram_cache(prefill_host(0), ctx, clen, M_CH)
+    params = inp["params"].cpu().numpy()
+    sched_ctx = inp["sched_ctx"].cpu().numpy()
     q = inp["q"].float().cpu().numpy()
     k = inp["k"].float().cpu().numpy()
     v = inp["v"].float().cpu().numpy()
@@ -256,13 +316,16 @@ def cpu_baseline(inp, greedy0, budget_s):
     while True:
         t = OT.Tree.empty(B, CAP)
         fr = nn = None
-        small = 0
-        for a in SCHEDULE:
+        for step, a in enumerate(SCHEDULE):
+            F_k = [-1] if step == 0 else [int(x) for x in fr[0, :int(nn[0])]]
+            n = int(t.n_nodes[0])
+            sig, _ = OS.tree_signals(t.parent[0], t.depth[0], t.cum[0], n, F_k, W_FR, 5)
+            OS.margin(sched_ctx[step, 0], sig, params)
             if a == 1:
                 t, _, _, _, _, fr, nn = OT.rescore_graft(t, strong, W_FR, M_CH, N=W_FR)
             else:
-                t, _, fr, nn, _ = OT.expand(t, weak[small], fr, nn, M_CH, W_FR)
-                small += 1
+                t, _, fr, nn, _ = NG.expand_ngram(t, fr, nn, ctx, clen, c_tok, c_lp, c_fb, M_CH,
+                                                  W_FR, NG_NMAX)
         n = int(t.n_nodes[0])
         pr = OT.global_prune(t.parent[0, :n], t.cum[0, :n], n, N_VER)
         par = pr["parent"][None]
@@ -585,20 +648,24 @@ def main():
     timeline = [[name, round(1e3 * ms, 2)] for name, ms in recs[-per_step:]]
 
     # ---- accounting
-    rows_r, rows_e = rows_read_per_step()
+    rows_r = rows_read_per_step()
     row_bytes = V * 4
     works = [verify_work(par) for par, _ in trees["host"]["pruned"]]
     v_bytes = sum(w[0] for w in works) / len(works)
     v_flops = sum(w[1] for w in works) / len(works)
-    step_bytes = (sum(rows_r) + sum(rows_e)) * row_bytes + v_bytes
+    step_bytes = sum(rows_r) * row_bytes + ngram_bytes_per_step() + v_bytes
     nodes = 8 + 64 + 80 + 80 + 80            # created per turn
     rescored = 72 + 160                       # non-root pool nodes rescored
     value = step_bytes / (ms_step * 1e-3) / 1e12
 
-    # dominant kernel (largest device time per step) and its roofline
-    dom = max(kernels, key=lambda k: kernels[k]["us_per_step"])
-    if dom == "row_partial":
-        dom_bytes = (sum(rows_r) + sum(rows_e)) * row_bytes
+    # roofline of the turn's bandwidth kernel: row_partial streams every
+    # logits row the turn reads (the other kernels are single-workgroup,
+    # latency-bound tree phases with a few KB of traffic; the largest of all
+    # by time is reported beside it)
+    slowest = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    dom = "row_partial"
+    if dom in kernels:
+        dom_bytes = sum(rows_r) * row_bytes
         launches = kern[dom][0]
         achieved = dom_bytes * args.steps / (kern[dom][1] * 1e-3)
         roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
@@ -607,9 +674,8 @@ def main():
                 "bytes_per_launch": dom_bytes * args.steps / launches,
                 "avg_launch_us": 1e3 * kern[dom][1] / launches}
     else:
-        t_us = kernels[dom]["us_per_step"]
         roof = {"bound": "hbm", "kernel": dom, "achieved": None, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": None, "traffic": None, "avg_launch_us": t_us}
+                "unit": "GB/s", "frac": None, "traffic": None, "avg_launch_us": None}
     attn_us = sum(kernels[k]["us_per_step"] for k in ATTN_MAIN + ("attn_combine",) if k in kernels)
     verify = {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
               "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
@@ -626,8 +692,11 @@ def main():
                                "verify layer", "batch": B, "vocab": V, "frontier_W": W_FR,
                    "children_m": M_CH, "q_heads": HQ, "kv_heads": HKV, "head_dim": D,
                    "prefix": L, "verify_nodes": N_VER, "input_copies": args.copies,
+                   "small_drafter": f"n-gram (cache m = {M_CH}, n_max = {NG_NMAX})",
+                   "scheduler": "signals + margin predictor every step, fixed schedule",
                    "timing": timing},
         "roofline": roof,
+        "largest_kernel": {"name": slowest, "us_per_step": kernels[slowest]["us_per_step"]},
         "draft_nodes_per_s": (nodes + rescored) / (ms_step * 1e-3),
         "verify_attention": verify,
         "step_bytes": step_bytes,
@@ -642,7 +711,8 @@ def main():
                                "cores": blas, "kind": "oracle",
                                "sample": f"{turns} full turns of the same workload on input "
                                          f"copy 0 in {el:.1f} s (tree steps single-threaded "
-                                         f"NumPy; attention matmuls on {blas} BLAS threads)"}
+                                         f"NumPy; attention matmuls on {blas} BLAS threads; "
+                                         f"the n-gram prefill cache built untimed first)"}
     print(json.dumps(out), flush=True)
 
 

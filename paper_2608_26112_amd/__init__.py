@@ -295,6 +295,10 @@ def expand_topk(tree: TreeState, logits, frontier, n_frontier, K, N, row_lse=Non
     return row_lse, next_frontier, n_next
 
 
+def ngram_cache_workspace(B, L, V, m) -> int:
+    return load().tg_ngram_cache_workspace(B, L, V, m)
+
+
 def ngram_cache(logits, context, ctx_len, m, cand_tok=None, cand_logp=None,
                 fallback_pos=None, workspace=None, d_err=None, stream=None):
     """n-gram drafter prefill cache.  logits [B,L,V] fp32 (row i = after
@@ -501,7 +505,8 @@ def kv_compact(k_cache, v_cache, prefix_len, path, n_path, new_prefix_len=None, 
 
 
 def tree_signals(tree: TreeState, frontier, n_frontier, W: int, lookback: int = 5,
-                 context=None, params=None, d_err=None, stream=None):
+                 context=None, params=None, d_err=None, stream=None, signals=None,
+                 margin=None, action=None):
     """The ten pre-action tree signals per tree (see tg_tree_signals), and
     with `params` (3265 fp32 predictor weights) and `context` [B, 11] the
     margin [B] and action [B].  frontier [B, F] int32 (-1 = root);
@@ -512,15 +517,16 @@ def tree_signals(tree: TreeState, frontier, n_frontier, W: int, lookback: int = 
         _dev(n_frontier, "n_frontier", torch.int32)
     B, F = frontier.shape
     dev = frontier.device
-    sig = torch.empty((B, 10), dtype=torch.float32, device=dev)
-    margin = action = None
+    sig = torch.empty((B, 10), dtype=torch.float32, device=dev) if signals is None else signals
     if params is not None:
         _dev(params, "params", torch.float32)
         _dev(context, "context", torch.float32)
         if params.numel() != 3265 or tuple(context.shape) != (B, 11):
             raise ValueError("params must hold 3265 values and context be [B, 11]")
-        margin = torch.empty((B,), dtype=torch.float32, device=dev)
-        action = torch.empty((B,), dtype=torch.int32, device=dev)
+        margin = torch.empty((B,), dtype=torch.float32, device=dev) if margin is None else margin
+        action = torch.empty((B,), dtype=torch.int32, device=dev) if action is None else action
+    else:
+        margin = action = None
     ts = tree.struct()
     st = lib.tg_tree_signals(ctypes.byref(ts), _ptr(frontier), _ptr(n_frontier), B, F, int(W),
                              int(lookback), _ptr(context), _ptr(params), _ptr(sig),

@@ -11,13 +11,14 @@
 // ngram_fallback_kernel: one workgroup per sequence; token counts by global
 //   atomics into a zeroed [V] slice, then the (count desc, token asc) best
 //   token and its last position, both as block maxima of packed keys.
-// ngram_expand_kernel: one workgroup per tree.  Per frontier node the whole
-//   block scans the context: end position j scores the length l(j) of the
-//   longest common suffix of x[..j] and the node's prefix (capped at n_max);
-//   the block maximum of (l, j) with l >= 1 is the latest longest match, which
-//   is what "longest n-gram first, shorter on a miss, latest occurrence"
-//   selects.  Children take ids n_b + f*K + k, then Top_N of them by
-//   (cum desc, depth asc, id asc).
+// ngram_expand_kernel: one workgroup per tree.  The prompt is staged in LDS
+//   (up to 4096 tokens) and every frontier node's suffix built at once; then
+//   for each node the block scans the prompt: end position j scores the
+//   length l(j) of the longest common suffix of x[..j] and the node's prefix
+//   (capped at n_max), and the maximum of (l, j) with l >= 1 is the latest
+//   longest match, which is what "longest n-gram first, shorter on a miss,
+//   latest occurrence" selects.  Children take ids n_b + f*K + k, then
+//   Top_N of them by (cum desc, depth asc, id asc).
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -94,6 +95,8 @@ __global__ __launch_bounds__(kThreads) void ngram_fallback_kernel(
   if (tid == 0) fallback_pos[b] = (int32_t)last - 1;
 }
 
+constexpr int kCtxLds = 4096;  // prompts up to this many tokens are scanned from LDS
+
 __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     tg_tree tree, const int32_t *__restrict__ frontier, const int32_t *__restrict__ n_frontier,
     int F, const int32_t *__restrict__ context, const int32_t *__restrict__ ctx_len, int L,
@@ -101,20 +104,22 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     const int32_t *__restrict__ fallback_pos, int m, int K, int N, int n_max,
     int32_t *__restrict__ match_pos, int32_t *__restrict__ next_frontier,
     int32_t *__restrict__ n_next, uint32_t *d_err) {
-  extern __shared__ uint64_t skey[];  // [pow2(F*K)]
-  __shared__ uint64_t red[kWaves];
-  __shared__ int32_t suf[TG_MAX_NGRAM];
-  __shared__ int plen_s;
-  __shared__ int32_t posf[TG_MAX_NGRAM_FRONTIER];
+  // dynamic LDS: keys [pow2(F*K)] | best [F] u64 | suffixes [F * n_max] | plen [F]
+  extern __shared__ uint64_t skey[];
+  __shared__ int32_t ctx_s[kCtxLds];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int cap = tree.cap;
   const size_t base = (size_t)b * cap;
   int Fb = n_frontier ? n_frontier[b] : F;
   Fb = Fb < 0 ? 0 : (Fb > F ? F : Fb);
   const int nb = tree.n_nodes[b];
-  int Lb = ctx_len[b];
+  const int Lb = ctx_len[b];
   const int total = Fb * K;
-  const int32_t *ctx = context + (size_t)b * L;
+  const int P2 = pow2_at_least(F * K > 0 ? F * K : 1);
+  uint64_t *best = skey + P2;
+  int32_t *suf = reinterpret_cast<int32_t *>(best + F);
+  int32_t *plen = suf + F * n_max;
+  const int32_t *ctx_g = context + (size_t)b * L;
 
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
@@ -124,8 +129,8 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   bad = __syncthreads_or(bad);
   const bool no_ctx = !bad && (Lb <= 0 || Lb > L);
   const bool full = !bad && !no_ctx && nb + total > cap;
-  for (int f = tid; f < F; f += kThreads)
-    if (match_pos) match_pos[(size_t)b * F + f] = -1;
+  if (match_pos)
+    for (int f = tid; f < F; f += kThreads) match_pos[(size_t)b * F + f] = -1;
   if (bad || no_ctx || full) {
     if (tid == 0) {
       report(d_err, bad ? TG_DERR_BAD_NODE : (no_ctx ? TG_DERR_BAD_PREFIX : TG_DERR_CAPACITY));
@@ -140,43 +145,62 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     fb = Lb - 1;
   }
 
-  // ---- matched position of every frontier node
-  for (int f = 0; f < Fb; ++f) {
-    if (tid == 0) {
-      // the prefix's last n_max tokens, newest first: the node's path, then
-      // the context's tail
-      int k = 0;
-      for (int u = frontier[(size_t)b * F + f]; u >= 0 && k < n_max; ++k) {
-        suf[k] = tree.token[base + u];
-        const int p = tree.parent[base + u];
-        u = (p < -1 || p >= u) ? -1 : p;
-      }
-      for (int i = Lb - 1; i >= 0 && k < n_max; --i, ++k) suf[k] = ctx[i];
-      plen_s = k;
+  // ---- the prompt in LDS (when it fits), every frontier node's suffix
+  const bool in_lds = Lb <= kCtxLds;
+  if (in_lds)
+    for (int i = tid; i < Lb; i += kThreads) ctx_s[i] = ctx_g[i];
+  for (int f = tid; f < Fb; f += kThreads) {
+    // the prefix's last n_max tokens, newest first: the node's path, then
+    // the context's tail
+    int32_t *sf = suf + f * n_max;
+    int k = 0;
+    for (int u = frontier[(size_t)b * F + f]; u >= 0 && k < n_max; ++k) {
+      sf[k] = tree.token[base + u];
+      const int p = tree.parent[base + u];
+      u = (p < -1 || p >= u) ? -1 : p;
     }
-    __syncthreads();
-    const int plen = plen_s;
-    uint64_t best = 0;
-    for (int j = tid; j < Lb; j += kThreads) {
-      int l = 0;
-      const int lim = min(plen, j + 1);
-      while (l < lim && ctx[j - l] == suf[l]) ++l;
-      if (l > 0) {
+    for (int i = Lb - 1; i >= 0 && k < n_max; --i, ++k) sf[k] = ctx_g[i];
+    plen[f] = k;
+    best[f] = 0;
+  }
+  __syncthreads();
+
+  // ---- latest longest match of every node.  The first token decides almost
+  // every position, so it is compared for a thread's positions together and
+  // only the hits are extended.  (Called with the LDS copy or the global
+  // prompt, each with its own address space.)
+  auto scan = [&](const int32_t *cx) __attribute__((always_inline)) {
+    for (int f = 0; f < Fb; ++f) {
+      const int32_t *sf = suf + f * n_max;
+      const int pl = plen[f];
+      const int s0 = sf[0];
+      uint64_t mine = 0;
+      for (int j = tid; j < Lb; j += kThreads) {
+        if (cx[j] != s0) continue;
+        int l = 1;
+        const int lim = min(pl, j + 1);
+        while (l < lim && cx[j - l] == sf[l]) ++l;
         const uint64_t key = ((uint64_t)l << 32) | (uint64_t)j;
-        best = key > best ? key : best;
+        mine = key > mine ? key : mine;
       }
+      mine = wave_max_u64(mine);
+      if ((tid & (kWave - 1)) == 0 && mine)
+        atomicMax(reinterpret_cast<unsigned long long *>(best + f), (unsigned long long)mine);
     }
-    best = block_max_u64(best, red);
-    if (tid == 0) {
-      const int pos = best ? (int)(uint32_t)best : fb;
-      posf[f] = pos;
-      if (match_pos) match_pos[(size_t)b * F + f] = pos;
-    }
+  };
+  if (in_lds)
+    scan(ctx_s);
+  else
+    scan(ctx_g);
+  __syncthreads();
+  for (int f = tid; f < Fb; f += kThreads) {
+    const int pos = best[f] ? (int)(uint32_t)best[f] : fb;
+    plen[f] = pos;  // reused: the matched position
+    if (match_pos) match_pos[(size_t)b * F + f] = pos;
   }
   __syncthreads();
 
   // ---- children from the cache rows, then Top_N
-  const int P2 = pow2_at_least(total > 0 ? total : 1);
   for (int c = tid; c < P2; c += kThreads) {
     if (c >= total) {
       skey[c] = 0;
@@ -184,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     }
     const int f = c / K, k = c - f * K;
     const int v = frontier[(size_t)b * F + f];
-    const size_t row = ((size_t)b * L + posf[f]) * m + k;
+    const size_t row = ((size_t)b * L + plen[f]) * m + k;
     const float cv = v < 0 ? 0.0f : tree.cum[base + v];
     const int dv = v < 0 ? 0 : tree.depth[base + v];
     const float lp = cand_logp[row];
@@ -200,7 +224,7 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   }
   __syncthreads();
   const int nn = min(N, total);
-  block_top_keys<kThreads>(skey, total, P2, nn);
+  block_top_keys<kThreads>(skey, total, pow2_at_least(total > 0 ? total : 1), nn);
   for (int j = tid; j < N; j += kThreads)
     next_frontier[(size_t)b * N + j] = j < nn ? node_key_id(skey[j]) : TG_NO_NODE;
   if (tid == 0) {
@@ -239,7 +263,8 @@ hipError_t launch_ngram_expand(const tg_tree &tree, const int32_t *frontier,
                                const int32_t *fallback_pos, int m, int K, int N, int n_max,
                                int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
                                uint32_t *d_err, hipStream_t stream) {
-  const size_t lds = (size_t)pow2_at_least(F * K > 0 ? F * K : 1) * sizeof(uint64_t);
+  const size_t lds = (size_t)pow2_at_least(F * K > 0 ? F * K : 1) * sizeof(uint64_t) +
+                    (size_t)F * sizeof(uint64_t) + (size_t)F * (n_max + 1) * sizeof(int32_t);
   hipError_t e = hipFuncSetAttribute((const void *)ngram_expand_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

@@ -5,8 +5,9 @@
 // One workgroup per tree, all in LDS: child counts, the frontier's depth set
 // D_F and its lookback closure D_C as bitsets over depth, the candidate set R
 // (root included) as node keys, ranked by counting (a sort past 1024 keys)
-// for the preview Top_W(R, s), block reductions for the ten signals, then the 3,265-parameter MLP with one
-// thread per hidden unit (fp32, fixed summation order).
+// for the preview Top_W(R, s), block reductions for the ten signals, then the
+// 3,265-parameter MLP (weights prefetched into LDS at the start) with four
+// lanes per hidden unit (fp32, fixed summation order).
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -18,6 +19,7 @@ constexpr int kThreads = 256;
 constexpr int kSigs = 10;
 constexpr int kCtx = 11;
 constexpr int kIn = 17;
+constexpr int kParams = 64 * kIn + 64 + 32 * 64 + 32 + 32 + 1;  // 3265
 constexpr int kMaxKeys = 2 * TG_MAX_CAP;  // pow2 >= cap + 1 (root)
 
 // block sums of up to four floats (fixed order: waves by shuffle tree, then
@@ -50,6 +52,9 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   __shared__ uint32_t dF[(TG_MAX_CAP + 1 + 31) / 32], dC[(TG_MAX_CAP + 1 + 31) / 32];
   __shared__ float red[4][kThreads / kWave];
   __shared__ float x_s[kIn], h1_s[64], h2_s[32];
+  __shared__ float par_s[kParams];   // the predictor's weights, prefetched
+  __shared__ int dep_s[TG_MAX_CAP];
+  __shared__ float cum_s[TG_MAX_CAP];
   __shared__ int bad_s;
 
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -59,17 +64,26 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   int n = tree.n_nodes[b];
   int Fb = n_frontier ? n_frontier[b] : F;
   Fb = Fb < 0 ? 0 : (Fb > F ? F : Fb);
-  if (tid == 0) bad_s = (n < 0 || n > cap) ? 1 : 0;
-  for (int i = tid; i <= TG_MAX_CAP; i += kThreads) {
+  const bool bad_n = n < 0 || n > cap;
+  if (bad_n) n = 0;
+  if (tid == 0) bad_s = bad_n ? 1 : 0;
+  // the weights stream into LDS while the tree is read
+  if (params)
+    for (int i = tid; i < kParams; i += kThreads) par_s[i] = params[i];
+  for (int i = tid; i <= n; i += kThreads) {
     childcnt[i] = 0;
     inF[i] = 0;
   }
   for (int i = tid; i < DW; i += kThreads) dF[i] = dC[i] = 0;
+  // node depths and scores, read once
+  for (int v = tid; v < n; v += kThreads) {
+    dep_s[v] = tree.depth[base + v];
+    cum_s[v] = tree.cum[base + v];
+  }
   __syncthreads();
-  if (bad_s) n = 0;
   const int32_t *fr = frontier + (size_t)b * F;
-  auto depth_of = [&](int v) { return v < 0 ? 0 : tree.depth[base + v]; };
-  auto cum_of = [&](int v) { return v < 0 ? 0.0f : tree.cum[base + v]; };
+  auto depth_of = [&](int v) { return v < 0 ? 0 : dep_s[v]; };
+  auto cum_of = [&](int v) { return v < 0 ? 0.0f : cum_s[v]; };
 
   // ---- children, frontier membership, D_F, D_C
   for (int v = tid; v < n; v += kThreads) {
@@ -194,25 +208,36 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   if (!params) return;
   __syncthreads();
   // ---- margin predictor: W1[64,17] b1[64] W2[32,64] b2[32] W3[1,32] b3[1]
-  const float *W1 = params, *b1 = W1 + 64 * kIn, *W2 = b1 + 64, *b2 = W2 + 32 * 64;
+  // (weights from LDS; four lanes per hidden unit, partial sums in fixed
+  // order, combined by lane shuffles)
+  const float *W1 = par_s, *b1 = W1 + 64 * kIn, *W2 = b1 + 64, *b2 = W2 + 32 * 64;
   const float *W3 = b2 + 32, *b3 = W3 + 32;
-  if (tid < 64) {
-    float a = b1[tid];
-    for (int i = 0; i < kIn; ++i) a = fmaf(W1[tid * kIn + i], x_s[i], a);
-    h1_s[tid] = fmaxf(a, 0.0f);
+  {
+    const int u = tid >> 2, q = tid & 3;   // 64 units x 4 lanes
+    float a = 0.0f;
+    for (int i = q; i < kIn; i += 4) a = fmaf(W1[u * kIn + i], x_s[i], a);
+    a += __shfl_xor(a, 1, kWave);
+    a += __shfl_xor(a, 2, kWave);
+    if (q == 0) h1_s[u] = fmaxf(a + b1[u], 0.0f);
   }
   __syncthreads();
-  if (tid < 32) {
-    float a = b2[tid];
-    for (int i = 0; i < 64; ++i) a = fmaf(W2[tid * 64 + i], h1_s[i], a);
-    h2_s[tid] = fmaxf(a, 0.0f);
+  if (tid < 128) {
+    const int u = tid >> 2, q = tid & 3;   // 32 units x 4 lanes
+    float a = 0.0f;
+    for (int i = q; i < 64; i += 4) a = fmaf(W2[u * 64 + i], h1_s[i], a);
+    a += __shfl_xor(a, 1, kWave);
+    a += __shfl_xor(a, 2, kWave);
+    if (q == 0) h2_s[u] = fmaxf(a + b2[u], 0.0f);
   }
   __syncthreads();
-  if (tid == 0) {
-    float y = b3[0];
-    for (int i = 0; i < 32; ++i) y = fmaf(W3[i], h2_s[i], y);
-    margin[b] = y;
-    action[b] = y > 0.0f ? 1 : 0;
+  if (tid < kWave) {
+    float y = tid < 32 ? W3[tid] * h2_s[tid] : 0.0f;
+    y = wave_sum_f32(y);
+    if (tid == 0) {
+      y += b3[0];
+      margin[b] = y;
+      action[b] = y > 0.0f ? 1 : 0;
+    }
   }
 }
 

@@ -174,25 +174,52 @@ __device__ __forceinline__ void count_larger(const uint64_t *key, int n,
 
 // Moves the k largest of key[0..n) (distinct; 0 = no key) to key[0..k), best
 // first, 0 in the places past the last present key; what lies past
-// min(k, n) is undefined afterwards.  Sets larger than kRankPerThread * kBlock
-// are sorted whole: then key[n..P2) must hold 0, P2 a power of two >= n.
-// Callers synchronise before; ends synchronised.
-template <int kBlock>
-__device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
-  if (n > kRankPerThread * kBlock) {
-    block_bitonic_desc(key, P2);
-    return;
+// min(k, n) is undefined afterwards.  Sets up to kRankPerThread * kBlock are
+// ranked by counting (each thread compares as many keys as the set needs),
+// larger ones sorted whole: then key[n..P2) must hold 0, P2 a power of two
+// >= n.  Callers synchronise before; ends synchronised.
+template <int kBlock, int R>
+__device__ void block_top_keys_r(uint64_t *key, int n, int k) {
+  uint64_t mk[R];
+  int r[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int i = threadIdx.x + j * kBlock;
+    mk[j] = i < n ? key[i] : ~0ull;
+    r[j] = 0;
   }
-  uint64_t mk[kRankPerThread];
-  int r[kRankPerThread];
-  count_larger<kBlock>(key, n, mk, r);
+  int u = 0;
+#pragma unroll 4
+  for (; u + 1 < n; u += 2) {
+    const uint64_t a = key[u], c = key[u + 1];
+#pragma unroll
+    for (int j = 0; j < R; ++j) r[j] += (int)(a > mk[j]) + (int)(c > mk[j]);
+  }
+  if (u < n) {
+    const uint64_t a = key[u];
+#pragma unroll
+    for (int j = 0; j < R; ++j) r[j] += (int)(a > mk[j]);
+  }
   __syncthreads();
   for (int j = threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kRankPerThread; ++j)
+  for (int j = 0; j < R; ++j)
     if (threadIdx.x + j * kBlock < n && mk[j] != 0 && r[j] < k) key[r[j]] = mk[j];
   __syncthreads();
+}
+
+template <int kBlock>
+__device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
+  if (n > kRankPerThread * kBlock) {
+    block_bitonic_desc(key, P2);
+  } else if (n > 2 * kBlock) {
+    block_top_keys_r<kBlock, 4>(key, n, k);
+  } else if (n > kBlock) {
+    block_top_keys_r<kBlock, 2>(key, n, k);
+  } else {
+    block_top_keys_r<kBlock, 1>(key, n, k);
+  }
 }
 
 // ------------------------------------------------------- finishing rows

@@ -76,11 +76,14 @@ def run_expand(tg, tree_h, fr, nf, ctx, clen, tok, lp, fb, K, N, n_max):
     return got, nx.cpu().numpy(), nn.cpu().numpy(), mp.cpu().numpy()
 
 
-@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("seed", range(5))
 def test_expand_chain_small(tg, seed):
-    """Four small steps from the root with the GPU's own cache."""
+    """Four small steps from the root with the GPU's own cache (seed 4: a
+    6000-token prompt, past what the kernel stages in LDS)."""
     g = W.rng(920 + seed)
     B, L, V, m = int(g.integers(1, 4)), int(g.integers(8, 200)), 300, 6
+    if seed == 4:
+        B, L = 2, 6000
     K, N, n_max = int(g.integers(1, m + 1)), int(g.integers(1, 12)), int(g.integers(1, 6))
     ctx = np.stack([W.token_stream(g, L, 20) for _ in range(B)])
     clen = g.integers(1, L + 1, B).astype(np.int32)
