@@ -76,7 +76,7 @@ typedef enum { TG_F32 = 0, TG_BF16 = 1 } tg_dtype;
 #define TG_NO_NODE (-2)        /* padding of frontier outputs (-1 is the root) */
 
 /* Variant flags of tg_tree_rescore_graft (0 = the method of Sec. 3.2).  The
- * first two are the Sec. 4.4 ablations. */
+ * first two are the Sec. 5.3 ablations. */
 #define TG_POOL_NEWONLY 1u     /* w/o EG: pool C = N_k, the previous step's
                                   new nodes (ids >= new_from[b]; -1 = root) */
 #define TG_GRAFT_OVERWRITE 2u  /* w/o ND: grafting under a frontier node
@@ -253,7 +253,7 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
                                 uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
-/* The n-gram small drafter (appendix on the n-gram small drafter): a
+/* The n-gram small drafter (App. C.1, the small drafter's implementation): a
  * training-free lookup that proposes children from the target's prefill.  */
 /*
  * tg_ngram_cache builds the prefill cache of B sequences:
@@ -403,9 +403,9 @@ tg_status tg_kv_compact(void *k_cache, void *v_cache, const int32_t *prefix_len,
                         uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
-/* Scheduler observations and margin predictor (appendix on online
- * observations: the candidate tree signals and the reselection preview
- * frontier; appendix on the value system: the margin predictor).           */
+/* Scheduler observations and margin predictor (App. B.2: the candidate tree
+ * signals and the reselection preview frontier; App. B.4: the margin
+ * predictor; Sec. 4.3 runtime scheduling).                                 */
 /*
  * tg_tree_signals computes, for each tree b with current frontier
  * frontier[b, 0:Fb] (node ids, -1 = root; Fb = n_frontier[b], or F when

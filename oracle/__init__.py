@@ -20,16 +20,16 @@ Grafting for Tree-Based Speculative Decoding):
     buffers (mask, position ids, retrieval paths).
   * ``attention.kv_compact`` - the cache update after acceptance: the accepted
     chain's K/V rows become the continuation of the prefix.
-  * ``tree.rescore_graft`` variants (flags) - the Sec. 4.4 ablations (pool =
+  * ``tree.rescore_graft`` variants (flags) - the Sec. 5.3 ablations (pool =
     the previous step's new nodes; overwriting graft) and a duplicate-sibling
     filter; ``tree.accept_logits`` - acceptance from the target's arg-max.
   * ``ngram.ngram_cache`` / ``ngram.expand_ngram`` - the n-gram small drafter
-    (appendix on the n-gram small drafter): the prefill top-m cache and the
+    (App. C.1, the small drafter's implementation): the prefill top-m cache and the
     suffix-match expansion with back-off and the most-frequent-token fallback.
   * ``signals.tree_signals`` / ``signals.margin`` - the ten candidate tree
     signals with the reselection preview frontier, and the scheduler's
-    margin predictor forward pass (App. online observations; value system
-    architecture).
+    margin predictor forward pass (App. B.2 candidate tree signals; App. B.4
+    margin predictor).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library

@@ -1,7 +1,7 @@
 """Oracle for the n-gram small drafter (test infrastructure only).
 
 The small drafter of the paper's main experiments is a training-free lookup
-(appendix on the n-gram small drafter):
+(App. C.1, the small drafter's implementation):
   * at prefill, every context position i caches the target's top-m next
     tokens after x_<=i with their target probabilities;
   * at a small step, the suffix of each frontier node's prefix (context, then

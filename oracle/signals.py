@@ -1,8 +1,8 @@
 """Oracle for the scheduler's tree signals and margin predictor (test
 infrastructure only).
 
-Definitions followed (App. "online observations", table of candidate tree
-signals; App. "value system architecture", margin predictor):
+Definitions followed (App. B.2, the table of candidate tree signals; App.
+B.4, the margin predictor):
 
   F      the current frontier (node ids, -1 = root; taken as given)
   d(v)   depth (root 0), s(v) cumulative path score, child(v) children

@@ -44,7 +44,7 @@ DERR_BAD_NODE = 16
 
 NO_NODE = -2  # padding for frontier outputs (-1 is the root)
 
-# Variant flags of the middle step (the two ablations of Sec. 4.4 and a
+# Variant flags of the middle step (the two ablations of Sec. 5.3 and a
 # duplicate-sibling filter); 0 = TreeGraft as described in Sec. 3.2.
 POOL_NEWONLY = 1    # w/o EG: the pool is the previous step's new nodes
 GRAFT_OVERWRITE = 2  # w/o ND: grafting replaces the frontier nodes' subtrees
@@ -189,7 +189,7 @@ def expand(tree: Tree, logits: np.ndarray, frontier: np.ndarray,
 def pool_of(tree: Tree, b: int, flags: int = 0, new_from=None):
     """Middle-drafter candidate pool (Sec. 3.2): C = V(T) minus P, i.e. the
     unvisited ids plus the root (-1) while the root is unvisited.  With
-    POOL_NEWONLY (the w/o EG ablation, Sec. 4.4) C = N_k instead: the ids
+    POOL_NEWONLY (the w/o EG ablation, Sec. 5.3) C = N_k instead: the ids
     new_from[b] .. n_b - 1 made by the previous step, the root when
     new_from[b] == -1 (the first step, whose tree is the root alone)."""
     nb = int(tree.n_nodes[b])
@@ -214,7 +214,7 @@ def needed_rows(tree: Tree, b: int, flags: int = 0, new_from=None):
 
 
 def overwrite_compact(t: Tree, b: int, F):
-    """The w/o ND reading (Sec. 4.4): attaching under a frontier node
+    """The w/o ND reading (Sec. 5.3): attaching under a frontier node
     overwrites its existing children, so every node with a strict ancestor in
     F is removed.  Frontier nodes inside a removed subtree are removed with
     it.  The surviving nodes keep their order and are renumbered densely
@@ -263,7 +263,7 @@ def rescore_graft(tree: Tree, strong: np.ndarray, W: int, M: int,
     The grafted children are N_{k+1}, the pool of a following small step
     (Sec. 3.2: a small step's pool is the previous step's new nodes); with
     N > 0 their Top_N by (cum desc, depth asc, id asc) is also returned.
-    Variant flags (Sec. 4.4 ablations; 0 = the paper's method):
+    Variant flags (Sec. 5.3 ablations; 0 = the paper's method):
       POOL_NEWONLY   step 1 uses C = N_k (ids >= new_from[b]; see pool_of);
       GRAFT_OVERWRITE before step 4 the frontier nodes' existing subtrees are
                      removed and the tree compacted (overwrite_compact); F

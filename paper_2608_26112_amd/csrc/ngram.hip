@@ -1,5 +1,5 @@
-// The n-gram small drafter (the paper's appendix on the n-gram small
-// drafter): a prefill cache of the target's top-m next tokens per context
+// The n-gram small drafter (App. C.1, the small drafter's implementation):
+// a prefill cache of the target's top-m next tokens per context
 // position, and the small-step expansion that matches each frontier node's
 // prefix suffix against the context (longest n-gram first, shorter on a miss,
 // the most frequent context token's position as the last resort) and grows

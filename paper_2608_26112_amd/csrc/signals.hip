@@ -1,6 +1,7 @@
-// The scheduler's pre-action tree signals and its margin predictor (the
-// candidate-signal table and the reselection preview frontier; the margin
-// predictor Linear(17,64)-ReLU-Linear(64,32)-ReLU-Linear(32,1)).
+// The scheduler's pre-action tree signals and its margin predictor (App.
+// B.2: the candidate tree signals and the reselection preview frontier;
+// App. B.4: the margin predictor Linear(17,64)-ReLU-Linear(64,32)-ReLU-
+// Linear(32,1)).
 //
 // One workgroup per tree, all in LDS: child counts, the frontier's depth set
 // D_F and its lookback closure D_C as bitsets over depth, the candidate set R

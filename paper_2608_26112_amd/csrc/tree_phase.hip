@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
 }
 
 // ------------------------------------------------------- graft variants
-// The middle step's graft under TG_GRAFT_OVERWRITE (w/o ND, Sec. 4.4: the
+// The middle step's graft under TG_GRAFT_OVERWRITE (w/o ND, Sec. 5.3: the
 // frontier nodes' existing subtrees are removed and the tree compacted
 // before the new children are attached) and TG_GRAFT_DEDUP (a child whose
 // token an existing child of the same parent carries is skipped; kept

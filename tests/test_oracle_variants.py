@@ -1,4 +1,4 @@
-"""Pins for the oracle's middle-step variants (Sec. 4.4 ablations: w/o EG,
+"""Pins for the oracle's middle-step variants (Sec. 5.3 ablations: w/o EG,
 w/o ND; a duplicate-sibling filter) and the target arg-max (App. E,
 temperature 0).  CPU only.
 
@@ -7,7 +7,7 @@ What fixes them:
     non-destructive graft and is lost when the graft overwrites it;
   * overwrite removes exactly the nodes with a strict ancestor in F (checked
     by walking each node's root path), keeps the others in order;
-  * w/o EG never grafts at a historical position (Sec. 4.4 reports 0% for
+  * w/o EG never grafts at a historical position (Sec. 5.3 reports 0% for
     it); when N_k equals the unvisited set it is the paper's method;
   * dedup never adds a child whose token an existing sibling carries, and
     skips exactly those (brute force over siblings);
