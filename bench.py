@@ -89,6 +89,10 @@ def parse():
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="profiling aid: run one device copy of this many MiB first, so a "
                          "counter pass can scale FETCH_SIZE/WRITE_SIZE by a known size")
+    ap.add_argument("--rescore-flags", type=int, default=0,
+                    help="rescore-twodrafter only: middle-step variant flags (1 = pool of the "
+                         "previous step's new nodes, 2 = overwriting graft, 4 = skip "
+                         "duplicate siblings; the Sec. 5.3 ablations and a filter)")
     ap.add_argument("--workload", default="turn",
                     choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b",
                              "expand-twodrafter", "rescore-twodrafter"],
@@ -479,10 +483,17 @@ def tree_bench(args, tg, torch, dev):
         lse = torch.empty((Bt, R), dtype=torch.float32, device=dev)
         gf = torch.empty((Bt, Wd), dtype=torch.int32, device=dev)
         ng = torch.empty((Bt,), dtype=torch.int32, device=dev)
+        flags = args.rescore_flags
+        # w/o EG: the pool is the template's last expansion (ids 16..255)
+        new_from = torch.full((Bt,), 16, dtype=torch.int32, device=dev) if flags & 1 else None
         call = lambda i: tg.rescore_graft(trees[i], logits[i % copies], Wd, Mm, row_lse=lse,
-                                          graft_frontier=gf, n_graft=ng, workspace=ws)
-        nbytes = Bt * R * Vv * 4
-        nodes = Bt * (256 + Wd * Mm)
+                                          graft_frontier=gf, n_graft=ng, workspace=ws,
+                                          flags=flags, new_from=new_from)
+        # rows read: the pool's own rows and its parents' (w/o EG: nodes 16..255 and
+        # their parents 0..15, the root row is not read)
+        nbytes = Bt * (R - 1 if flags & 1 else R) * Vv * 4
+        # pool nodes rescored (root included) + graft slots
+        nodes = Bt * ((240 if flags & 1 else 257) + Wd * Mm)
     else:
         ws = torch.zeros(tg.expand_topk_workspace(Bt, F, Vv, K, Nn), dtype=torch.uint8,
                          device=dev)
@@ -518,7 +529,8 @@ def tree_bench(args, tg, torch, dev):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp32",
         "data": "synthetic",
         "config": {"workload": args.workload, "batch": Bt, "vocab": Vv, "rows_per_tree": rows,
-                   "K_or_m": Mm if rescore else K, "input_copies": copies},
+                   "K_or_m": Mm if rescore else K, "input_copies": copies,
+                   "rescore_flags": args.rescore_flags if rescore else None},
         "roofline": {"bound": "hbm", "kernel": "row_partial", "achieved": ach / 1e9,
                      "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": ach / PEAK_HBM,
                      "traffic": None if rescore else
