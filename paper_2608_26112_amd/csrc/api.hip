@@ -11,8 +11,10 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Workspace of the row-statistics pass: per (row, grain) (max, sum-exp)
 // partials, per (row, chunk) top-K keys, then `extra` bytes for the caller.
+// Workspace of a row pass: per grain (max, sum-exp) partials | per chunk
+// top-K keys | finished top-K keys per row | the caller's extra bytes.
 struct RowWs {
-  size_t ms_off, keys_off, extra_off, bytes;
+  size_t ms_off, keys_off, fin_off, extra_off, bytes;
 };
 RowWs row_ws(long long slots, int V, int K, size_t extra) {
   tg::RowPlan plan = tg::plan_rows(slots, V);
@@ -21,7 +23,8 @@ RowWs row_ws(long long slots, int V, int K, size_t extra) {
   RowWs w;
   w.ms_off = 0;
   w.keys_off = align_up(ms * sizeof(float2), 256);
-  w.extra_off = align_up(w.keys_off + parts * (size_t)K * sizeof(uint64_t), 256);
+  w.fin_off = align_up(w.keys_off + parts * (size_t)K * sizeof(uint64_t), 256);
+  w.extra_off = align_up(w.fin_off + (size_t)slots * K * sizeof(uint64_t), 256);
   w.bytes = align_up(w.extra_off + extra, 256);
   return w;
 }
@@ -115,12 +118,15 @@ tg_status tg_tree_expand_topk(const tg_tree *tree, const float *logits,
   char *ws = static_cast<char *>(workspace);
   float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
   uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
+  uint64_t *fin = reinterpret_cast<uint64_t *>(ws + w.fin_off);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = tg::launch_row_partials(logits, B, F, V, K, plan, n_frontier, nullptr, ms,
                                          keys, d_err, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  return from_hip(tg::launch_expand_tree(*tree, frontier, n_frontier, B, F, K, N, plan, ms,
-                                         keys, row_lse, next_frontier, n_next, d_err, st));
+  e = tg::launch_row_finish(B, F, K, plan, n_frontier, nullptr, ms, keys, row_lse, fin, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(tg::launch_expand_tree(*tree, frontier, n_frontier, B, F, K, N, row_lse,
+                                         fin, next_frontier, n_next, d_err, st));
 }
 
 // ------------------------------------------------------------ rescore + graft
@@ -153,13 +159,13 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   if (!workspace || ws_bytes < w.bytes) return TG_ERR_WORKSPACE;
   tg::RowPlan plan = tg::plan_rows((long long)B * R, V);
   {
-    int so = 0, vo = 0;
-    if (tg::rescore_tree_lds(tree->cap, M, plan, flags, &so, &vo) > 160 * 1024)
-      return TG_ERR_UNSUPPORTED;
+    int vo = 0;
+    if (tg::rescore_tree_lds(tree->cap, flags, &vo) > 160 * 1024) return TG_ERR_UNSUPPORTED;
   }
   char *ws = static_cast<char *>(workspace);
   float2 *ms = reinterpret_cast<float2 *>(ws + w.ms_off);
   uint64_t *keys = reinterpret_cast<uint64_t *>(ws + w.keys_off);
+  uint64_t *fin = reinterpret_cast<uint64_t *>(ws + w.fin_off);
   uint8_t *needed = reinterpret_cast<uint8_t *>(ws + w.extra_off);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = tg::launch_rescore_pool(*tree, B, R, needed, flags, new_from, st);
@@ -167,8 +173,10 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   e = tg::launch_row_partials(strong_logits, B, R, V, M, plan, nullptr, needed, ms, keys,
                               d_err, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, plan, needed,
-                                          ms, keys, row_lse, graft_frontier, n_graft,
+  e = tg::launch_row_finish(B, R, M, plan, nullptr, needed, ms, keys, row_lse, fin, st);
+  if (e != hipSuccess) return TG_ERR_HIP;
+  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, needed,
+                                          row_lse, fin, graft_frontier, n_graft,
                                           next_frontier, n_next, next_frontier ? N : 0,
                                           flags, new_from, d_err, st));
 }

@@ -73,16 +73,20 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     deep_s = 0;
   }
   __syncthreads();
+  // (until every chain has reached the root: depth+1 rounds at most)
   int cur = 0;
   for (int span = 1; span < nn; span <<= 1) {
     const int nxt = cur ^ 1;
+    bool more = false;
     for (int v = tid; v < nn; v += kThreads) {
       const int a = anc[cur][v];
-      anc[nxt][v] = a >= 0 ? anc[cur][a] : (int16_t)-1;
+      const int16_t na = a >= 0 ? anc[cur][a] : (int16_t)-1;
+      anc[nxt][v] = na;
       dep[nxt][v] = a >= 0 ? (int16_t)(dep[cur][v] + dep[cur][a]) : dep[cur][v];
+      more |= na >= 0;
     }
     cur = nxt;
-    __syncthreads();
+    if (!__syncthreads_or(more)) break;
   }
   const int16_t *depth = dep[cur];
 
@@ -94,12 +98,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     key[i] = i < nn ? node_key(tree.cum[base + i], depth[i], i) : 0;
   __syncthreads();
   if (nn <= kRankCountMax) {
-    uint64_t mk[kRankPerThread];
-    int r[kRankPerThread];
-    count_larger<kThreads>(key, nn, mk, r);
-#pragma unroll
-    for (int j = 0; j < kRankPerThread; ++j)
-      if (tid + j * kThreads < nn) rank[tid + j * kThreads] = (int16_t)r[j];
+    rank_each<kThreads>(key, nn, [&](int i, uint64_t, int r) { rank[i] = (int16_t)r; });
     __syncthreads();
     for (int v = tid; v < nn; v += kThreads) order[rank[v]] = (int16_t)v;  // ranked ids
   } else {
@@ -153,17 +152,11 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   __syncthreads();
   const int nk = nk_s;
   if (nk <= kRankCountMax) {
-    uint64_t mk[kRankPerThread];
-    int r[kRankPerThread];
-    count_larger<kThreads>(key, nk, mk, r);
-#pragma unroll
-    for (int j = 0; j < kRankPerThread; ++j) {
-      const int i = tid + j * kThreads;
-      if (i >= nk) continue;
-      const int v = (int)(uint32_t)~mk[j];
-      order[r[j]] = (int16_t)v;
-      newid[v] = (int16_t)(r[j] + 1);
-    }
+    rank_each<kThreads>(key, nk, [&](int, uint64_t k, int r) {
+      const int v = (int)(uint32_t)~k;
+      order[r] = (int16_t)v;
+      newid[v] = (int16_t)(r + 1);
+    });
   } else {
     const int P2k = pow2_at_least(nk);
     for (int i = nk + tid; i < P2k; i += kThreads) key[i] = 0;

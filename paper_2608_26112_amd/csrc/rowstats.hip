@@ -68,17 +68,32 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
   return v;
 }
 
-// Entries of a descending list that are >= v (or_equal) / > v.
-__device__ __forceinline__ int count_desc(const float *a, int n, float v, bool or_equal) {
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (or_equal ? a[mid] >= v : a[mid] > v)
-      lo = mid + 1;
-    else
-      hi = mid;
+// The K-th and the kq-th largest (kq <= K <= 64) of the wave's values, ties
+// counted: at least K (kq) lanes hold a value >= tK (tq); -inf when fewer
+// lanes hold finite values.  Small K: rounds of "take the wave maximum,
+// retire the lanes holding it"; larger K: a bitonic sort of the wave.
+__device__ __forceinline__ void wave_order_stats(float v, int K, int kq, int lane, float &tK,
+                                                 float &tq) {
+  const float ninf = -__builtin_inff();
+  tK = ninf;
+  tq = ninf;
+  if (K > 16) {
+    const float srt = wave_sort_desc(v, lane);
+    tK = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(srt), K - 1));
+    tq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(srt), kq - 1));
+    return;
   }
-  return lo;
+  int taken = 0;
+  for (int j = 0; j < K && taken < K; ++j) {
+    const float mx = wave_max_f32(v);
+    if (mx == ninf) return;
+    const bool hit = v == mx;
+    const int before = taken;
+    taken += __popcll(__ballot(hit));
+    if (before < kq && taken >= kq) tq = mx;
+    if (taken >= K) tK = mx;
+    v = hit ? ninf : v;
+  }
 }
 
 // Workgroup-wide sum of one int per thread (one barrier; slots alternate).
@@ -97,11 +112,14 @@ __device__ __forceinline__ int block_sum(int c, int *slots, int &par) {
 //  1. the grain sits in registers (32 elements per thread, one batch of
 //     loads); per thread max, then sum of exp (a NaN result flags NaN/+inf
 //     input, and only then are the values cleaned);
-//  2. one (max, sum-exp) partial per grain, waves by a fixed shuffle tree,
+//  2. one (max, sum-exp) partial per grain, waves by a fixed DPP tree,
 //     then the four waves in order: the same bits whatever the chunking;
-//  3. a lower bound T on the grain's K-th largest logit: the K-th largest of
-//     the 256 thread maxima (K threads each hold an element >= it), raised to
-//     the running chunk list's K-th entry;
+//  3. a lower bound T on the grain's K-th largest logit from the thread
+//     maxima, each wave on its own: the largest over waves of a wave's K-th
+//     largest maximum (K threads hold an element >= it), and the smallest
+//     over waves of a wave's ceil(K/4)-th largest (every wave then holds
+//     ceil(K/4) elements >= it); the larger of the two, raised to the
+//     running chunk list's K-th entry;
 //  4. elements >= T are compacted into LDS (about K of them for continuous
 //     logits); with more than kCandCap (heavy ties) the grain's exact K-th
 //     key is found by bisection over the key bits instead;
@@ -114,9 +132,8 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     uint64_t *__restrict__ part_keys, uint32_t *d_err) {
   __shared__ uint64_t cand[TG_MAX_TOPK + kCandCap];  // [0, K): running list
   __shared__ uint64_t run[TG_MAX_TOPK];
-  __shared__ float lmax[kWavesPerBlock][TG_MAX_TOPK];
+  __shared__ float lmax[kWavesPerBlock], lmaxq[kWavesPerBlock];
   __shared__ float gm[kWavesPerBlock], gs[kWavesPerBlock];
-  __shared__ float thr_s;
   __shared__ int cnt_s, cntf_s;
   __shared__ int red[2 * kWavesPerBlock];
 
@@ -191,15 +208,17 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
       s = lane_sumexp(x, m);
     }
 
-    // ---- 2. wave partials; 3. wave-sorted thread maxima
+    // ---- 2. wave partials; 3. the wave's bound on the K-th largest
     const float mw = wave_max_f32(m);
     const float sc = (m == ninf) ? 0.0f : s * __builtin_amdgcn_exp2f((m - mw) * kLog2e);
     const float sw = wave_sum_f32(sc);
-    const float ms = wave_sort_desc(m, lane);
-    if (lane < K) lmax[w][lane] = ms;
+    float tk, tq;
+    wave_order_stats(m, K, (K + kWavesPerBlock - 1) / kWavesPerBlock, lane, tk, tq);
     if (lane == 0) {
       gm[w] = mw;
       gs[w] = sw;
+      lmax[w] = tk;
+      lmaxq[w] = tq;
     }
     if (tid < K) cand[tid] = run[tid];
     if (tid == 0) {
@@ -213,20 +232,15 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
       for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[i], gs[i]);
       part_ms[(size_t)slot * n_grains + gr] = make_float2(M, S);
     }
-    if (tid < kWavesPerBlock * K) {
-      // rank of this entry in the four lists merged (value desc, list asc)
-      const int wl = tid / K, i = tid - wl * K;
-      const float v = lmax[wl][i];
-      int rank = i;
+    float T = key_threshold(cand[K - 1]), Tq = lmaxq[0];
 #pragma unroll
-      for (int o = 0; o < kWavesPerBlock; ++o)
-        if (o != wl) rank += count_desc(lmax[o], K, v, o < wl);
-      if (rank == K - 1) thr_s = v;
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      T = fmaxf(T, lmax[i]);
+      Tq = fminf(Tq, lmaxq[i]);
     }
-    __syncthreads();
+    T = fmaxf(T, Tq);
 
     // ---- 4. candidates
-    const float T = fmaxf(thr_s, key_threshold(cand[K - 1]));
     if (T > ninf) {
 #pragma unroll
       for (int j = 0; j < kPer; ++j) {
@@ -308,6 +322,43 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
   if (tid < K) part_keys[((size_t)slot * chunks + c) * K + tid] = run[tid];
 }
 
+// One wave per row slot, live by the row pass's rule: the row's
+// log-sum-exp from its grain partials, folded in grain order (the lanes load
+// them, the fold reads them lane by lane: the same bits as a serial pass),
+// and its top-K from the chunk lists (staged in LDS, K-round merge).
+// Writes lse[s] and out_keys[s * K + j], best first.
+__global__ __launch_bounds__(kThreads) void row_finish_kernel(
+    long long slots, int rows_per_batch, int K, int chunks, int n_ms,
+    const int32_t *__restrict__ n_live, const uint8_t *__restrict__ needed,
+    const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
+    float *__restrict__ lse, uint64_t *__restrict__ out_keys) {
+  extern __shared__ uint64_t stage[];  // [kWavesPerBlock][chunks * K]
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const long long s = (long long)blockIdx.x * kWavesPerBlock + w;
+  if (s >= slots) return;  // wave-uniform from here on
+  const int b = (int)(s / rows_per_batch);
+  const int r = (int)(s - (long long)b * rows_per_batch);
+  if (needed) {
+    if (!needed[s]) return;
+  } else if (r >= (n_live ? n_live[b] : rows_per_batch)) {
+    return;
+  }
+  const float2 *ms = part_ms + s * n_ms;
+  float2 p = lane < n_ms ? ms[lane] : make_float2(-__builtin_inff(), 0.0f);
+  const uint64_t key = wave_finish_topk(part_keys + s * chunks * K, chunks, K,
+                                        stage + (size_t)w * chunks * K);
+  float m = -__builtin_inff(), sum = 0.0f;
+  for (int i0 = 0; i0 < n_ms; i0 += kWave) {
+    if (i0 > 0) p = i0 + lane < n_ms ? ms[i0 + lane] : make_float2(-__builtin_inff(), 0.0f);
+    const int cnt = min(kWave, n_ms - i0);
+    for (int i = 0; i < cnt; ++i)
+      merge_ms(m, sum, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p.x), i)),
+               __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p.y), i)));
+  }
+  if (lane < K) out_keys[s * K + lane] = key;
+  if (lane == 0) lse[s] = m == -__builtin_inff() ? -__builtin_inff() : m + logf(sum);
+}
+
 }  // namespace
 
 RowPlan plan_rows(long long rows, int V) {
@@ -334,6 +385,25 @@ hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
   dim3 g((unsigned)grid), blk(kThreads);
 launch("row_partial", row_partial_kernel, g, blk, 0, stream, logits, rows_per_batch, V, K,
          plan.chunks, plan.grains_per_chunk, n_live, needed, part_ms, part_keys, d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_finish(int B, int rows_per_batch, int K, RowPlan plan,
+                             const int32_t *n_live, const uint8_t *needed,
+                             const float2 *part_ms, const uint64_t *part_keys, float *lse,
+                             uint64_t *out_keys, hipStream_t stream) {
+  const long long slots = (long long)B * rows_per_batch;
+  const long long grid = (slots + kWavesPerBlock - 1) / kWavesPerBlock;
+  if (grid <= 0) return hipSuccess;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  const size_t lds = (size_t)kWavesPerBlock * plan.chunks * K * sizeof(uint64_t);
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  hipError_t e = hipFuncSetAttribute((const void *)row_finish_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  launch("row_finish", row_finish_kernel, dim3((unsigned)grid), dim3(kThreads), lds, stream,
+         slots, rows_per_batch, K, plan.chunks, plan.ms_per_row, n_live, needed, part_ms,
+         part_keys, lse, out_keys);
   return hipGetLastError();
 }
 

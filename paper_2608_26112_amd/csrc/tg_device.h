@@ -63,28 +63,48 @@ __device__ __forceinline__ float edge_logp(float x, float lse) {
 }
 
 // ------------------------------------------------------------ wave helpers
+// Wave reductions by DPP lane moves (all VALU, no LDS round trips): two quad
+// swaps, row shifts by 4 and 8 (lane 15 of each row of 16 then holds the
+// row's result), row broadcasts of lanes 15 and 31 into the next rows; lane
+// 63 ends with the wave's result, returned to every lane.  Lanes a move
+// cannot source contribute the identity.  The combination order is fixed.
+// Every lane of the wave must be active.
+template <int kCtrl, int kRowMask, typename T>
+__device__ __forceinline__ T dpp_move(T v, T fill) {
+  static_assert(sizeof(T) == 4, "32-bit lanes");
+  return __builtin_bit_cast(
+      T, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill), __builtin_bit_cast(int, v),
+                                     kCtrl, kRowMask, 0xf, false));
+}
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, T id, Op op) {
+  v = op(v, dpp_move<0xb1, 0xf>(v, id));   // quad_perm [1,0,3,2]
+  v = op(v, dpp_move<0x4e, 0xf>(v, id));   // quad_perm [2,3,0,1]
+  v = op(v, dpp_move<0x114, 0xf>(v, id));  // row_shr:4
+  v = op(v, dpp_move<0x118, 0xf>(v, id));  // row_shr:8
+  v = op(v, dpp_move<0x142, 0xa>(v, id));  // row_bcast:15 into rows 1 and 3
+  v = op(v, dpp_move<0x143, 0xc>(v, id));  // row_bcast:31 into rows 2 and 3
+  return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), kWave - 1));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  return wave_reduce(v, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+// 64-bit keys: the high words first, then the low words of the lanes that
+// hold the high maximum.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t w = __shfl_xor(v, o, kWave);
-    v = w > v ? w : v;
-  }
-  return v;
+  const uint32_t hi = (uint32_t)(v >> 32);
+  const uint32_t mh = wave_max_u32(hi);
+  const uint32_t ml = wave_max_u32(hi == mh ? (uint32_t)v : 0u);
+  return ((uint64_t)mh << 32) | ml;
 }
 __device__ __forceinline__ float wave_max_f32(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  return wave_reduce(v, -__builtin_inff(), [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
 }
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return wave_reduce(v, 0, [](int a, int b) { return a + b; });
 }
 
 // Merge two (max, sum-of-exp relative to max) pairs in the log2 domain.
@@ -147,41 +167,10 @@ __device__ int block_exclusive_scan(int v, int *slots, int &total) {
 constexpr int kRankPerThread = 4;  // keys a thread ranks (sets up to 4 * block)
 
 // r[j] = how many of key[0..n) are larger than mk[j] = key[threadIdx.x +
-// j * kBlock] (~0, ranking nothing, past n).  n <= kRankPerThread * kBlock.
-template <int kBlock>
-__device__ __forceinline__ void count_larger(const uint64_t *key, int n,
-                                             uint64_t (&mk)[kRankPerThread],
-                                             int (&r)[kRankPerThread]) {
-#pragma unroll
-  for (int j = 0; j < kRankPerThread; ++j) {
-    const int i = threadIdx.x + j * kBlock;
-    mk[j] = i < n ? key[i] : ~0ull;
-    r[j] = 0;
-  }
-  int u = 0;
-#pragma unroll 4
-  for (; u + 1 < n; u += 2) {
-    const uint64_t a = key[u], c = key[u + 1];
-#pragma unroll
-    for (int j = 0; j < kRankPerThread; ++j) r[j] += (int)(a > mk[j]) + (int)(c > mk[j]);
-  }
-  if (u < n) {
-    const uint64_t a = key[u];
-#pragma unroll
-    for (int j = 0; j < kRankPerThread; ++j) r[j] += (int)(a > mk[j]);
-  }
-}
-
-// Moves the k largest of key[0..n) (distinct; 0 = no key) to key[0..k), best
-// first, 0 in the places past the last present key; what lies past
-// min(k, n) is undefined afterwards.  Sets up to kRankPerThread * kBlock are
-// ranked by counting (each thread compares as many keys as the set needs),
-// larger ones sorted whole: then key[n..P2) must hold 0, P2 a power of two
-// >= n.  Callers synchronise before; ends synchronised.
+// j * kBlock] (~0, ranking nothing, past n).  n <= R * kBlock.
 template <int kBlock, int R>
-__device__ void block_top_keys_r(uint64_t *key, int n, int k) {
-  uint64_t mk[R];
-  int r[R];
+__device__ __forceinline__ void count_larger(const uint64_t *key, int n, uint64_t (&mk)[R],
+                                             int (&r)[R]) {
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const int i = threadIdx.x + j * kBlock;
@@ -200,6 +189,42 @@ __device__ void block_top_keys_r(uint64_t *key, int n, int k) {
 #pragma unroll
     for (int j = 0; j < R; ++j) r[j] += (int)(a > mk[j]);
   }
+}
+
+// f(i, key[i], rank of key[i]) for every i < n (n <= kRankPerThread * kBlock),
+// each thread comparing as many keys as the set needs.  No synchronisation.
+template <int kBlock, int R, typename Fn>
+__device__ __forceinline__ void rank_each_r(const uint64_t *key, int n, Fn f) {
+  uint64_t mk[R];
+  int r[R];
+  count_larger<kBlock, R>(key, n, mk, r);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int i = threadIdx.x + j * kBlock;
+    if (i < n) f(i, mk[j], r[j]);
+  }
+}
+template <int kBlock, typename Fn>
+__device__ __forceinline__ void rank_each(const uint64_t *key, int n, Fn f) {
+  if (n > 2 * kBlock)
+    rank_each_r<kBlock, 4>(key, n, f);
+  else if (n > kBlock)
+    rank_each_r<kBlock, 2>(key, n, f);
+  else
+    rank_each_r<kBlock, 1>(key, n, f);
+}
+
+// Moves the k largest of key[0..n) (distinct; 0 = no key) to key[0..k), best
+// first, 0 in the places past the last present key; what lies past
+// min(k, n) is undefined afterwards.  Sets up to kRankPerThread * kBlock are
+// ranked by counting (each thread compares as many keys as the set needs),
+// larger ones sorted whole: then key[n..P2) must hold 0, P2 a power of two
+// >= n.  Callers synchronise before; ends synchronised.
+template <int kBlock, int R>
+__device__ void block_top_keys_r(uint64_t *key, int n, int k) {
+  uint64_t mk[R];
+  int r[R];
+  count_larger<kBlock, R>(key, n, mk, r);
   __syncthreads();
   for (int j = threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
   __syncthreads();
@@ -240,14 +265,19 @@ __device__ inline float finish_lse(const float2 *__restrict__ ms, int n) {
 // the largest head, that list advances.  Lane j < K returns the j-th best key.
 __device__ inline uint64_t wave_merge_lists(const uint64_t *lists, int chunks, int K) {
   const int lane = threadIdx.x & (kWave - 1);
-  int idx = 0;
-  uint64_t head = lane < chunks ? lists[lane * K] : 0;
+  const bool own = lane < chunks;
+  // the head and the entry after it sit in registers, so the LDS read that
+  // refills them overlaps the next round's reduction
+  uint64_t head = own ? lists[lane * K] : 0;
+  uint64_t next = own && K > 1 ? lists[lane * K + 1] : 0;
+  int idx = 1;
   uint64_t mine = 0;
   for (int j = 0; j < K; ++j) {
     const uint64_t best = wave_max_u64(head);
     if (head == best && best != 0) {
+      head = next;
       ++idx;
-      head = idx < K ? lists[lane * K + idx] : 0;
+      next = own && idx < K ? lists[lane * K + idx] : 0;
     }
     if (lane == j) mine = best;
   }
@@ -255,13 +285,26 @@ __device__ inline uint64_t wave_merge_lists(const uint64_t *lists, int chunks, i
 }
 
 // One wave finishes one row's top-K: lane j < K returns the j-th best key.
-// `ws` is this wave's LDS scratch (chunks * K keys).  chunks <= 64.
+// `ws` is this wave's LDS scratch (chunks * K keys).  chunks <= 64.  The
+// lists are staged four loads per lane at a time, one wait per batch.
 __device__ inline uint64_t wave_finish_topk(const uint64_t *__restrict__ lists, int chunks, int K,
                                      uint64_t *ws) {
   const int lane = threadIdx.x & (kWave - 1);
   if (chunks == 1) return lane < K ? lists[lane] : 0;
   const int nk = chunks * K;
-  for (int i = lane; i < nk; i += kWave) ws[i] = lists[i];
+  for (int i0 = 0; i0 < nk; i0 += 4 * kWave) {
+    uint64_t t[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kWave + lane;
+      t[u] = i < nk ? lists[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kWave + lane;
+      if (i < nk) ws[i] = t[u];
+    }
+  }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");

@@ -49,10 +49,18 @@ hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
                                float2 *part_ms, uint64_t *part_keys,
                                uint32_t *d_err, hipStream_t stream);
 
+// Finishes the same live rows: lse[s] (grain order) and the row's top-K keys
+// out_keys[s * K + j], best first (one wave per row over the whole chip).
+hipError_t launch_row_finish(int B, int rows_per_batch, int K, RowPlan plan,
+                             const int32_t *n_live, const uint8_t *needed,
+                             const float2 *part_ms, const uint64_t *part_keys, float *lse,
+                             uint64_t *out_keys, hipStream_t stream);
+
+// The tree kernels read finished rows: row_lse [B, rows] and row_keys
+// [B, rows, K] as written by launch_row_finish.
 hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
                               const int32_t *n_frontier, int B, int F, int K,
-                              int N, RowPlan plan, const float2 *part_ms,
-                              const uint64_t *part_keys, float *row_lse,
+                              int N, const float *row_lse, const uint64_t *row_keys,
                               int32_t *next_frontier, int32_t *n_next,
                               uint32_t *d_err, hipStream_t stream);
 
@@ -61,14 +69,12 @@ hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream);
 hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *needed,
                                uint32_t flags, const int32_t *new_from,
                                hipStream_t stream);
-// dynamic LDS of rescore_tree_kernel (and the offsets of its regions)
-size_t rescore_tree_lds(int cap, int M, RowPlan plan, uint32_t flags, int *stage_off,
-                        int *var_off);
+// dynamic LDS of rescore_tree_kernel (and the offset of its variant region)
+size_t rescore_tree_lds(int cap, uint32_t flags, int *var_off);
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
-                               int R, int V, int W, int M, RowPlan plan,
-                               const uint8_t *needed, const float2 *part_ms,
-                               const uint64_t *part_keys, float *row_lse,
+                               int R, int V, int W, int M, const uint8_t *needed,
+                               const float *row_lse, const uint64_t *row_keys,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t flags, const int32_t *new_from,

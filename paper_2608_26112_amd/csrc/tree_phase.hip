@@ -2,8 +2,9 @@
 // middle-drafter step (Sec. 3.2; Alg. 2, middle branch).
 //
 // One workgroup owns one tree.  The vocabulary-wide work already happened in
-// row_partial_kernel; here the chunk partials of each needed row are merged
-// into its log-sum-exp and top-K list, then the tree is edited in place:
+// the row pass and its finish (a wave per row across the chip): each needed
+// row's log-sum-exp and top-K list are read from there, then the tree is
+// edited in place:
 // children appended (expand), pool rescored, graft positions reselected and
 // new children grafted without touching existing nodes (rescore_graft).
 // Node selection (Top_W) ranks 64-bit keys in LDS ordered by (cum desc,
@@ -21,33 +22,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
-// Top-K of nr consecutive rows (row r's `chunks` lists of K keys at
-// lists + r * chunks * K) into out[r * K + j], best first.  The lists are
-// staged in LDS (`stage`, room for stage_cap >= chunks * K keys) with one
-// global round trip per batch, then a wave merges each row.  chunks <= 64.
-// Called by the whole block; ends synchronised.
-__device__ void block_finish_topk(const uint64_t *__restrict__ lists, int chunks, int K,
-                                  int nr, uint64_t *out, uint64_t *stage, int stage_cap) {
-  const int nk = chunks * K;
-  if (chunks == 1) {
-    for (int i = threadIdx.x; i < nr * K; i += blockDim.x) out[i] = lists[i];
-    __syncthreads();
-    return;
-  }
-  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
-  const int per = stage_cap / nk;
-  for (int r0 = 0; r0 < nr; r0 += per) {
-    const int rb = min(per, nr - r0);
-    for (int i = threadIdx.x; i < rb * nk; i += blockDim.x) stage[i] = lists[(size_t)r0 * nk + i];
-    __syncthreads();
-    for (int r = w; r < rb; r += kWaves) {
-      const uint64_t key = wave_merge_lists(stage + r * nk, chunks, K);
-      if (lane < K) out[(r0 + r) * K + lane] = key;
-    }
-    __syncthreads();
-  }
-}
-
 __device__ __forceinline__ int sane_parent(int p, int v, bool &bad) {
   bool b = p < -1 || p >= v;
   bad |= b;
@@ -57,11 +31,10 @@ __device__ __forceinline__ int sane_parent(int p, int v, bool &bad) {
 // --------------------------------------------------------------- expand
 __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
     tg_tree tree, const int32_t *__restrict__ frontier,
-    const int32_t *__restrict__ n_frontier, int F, int K, int N, int chunks,
-    int n_ms, const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
-    float *__restrict__ row_lse, int32_t *__restrict__ next_frontier,
-    int32_t *__restrict__ n_next, uint32_t *d_err, int skey_cap) {
-  extern __shared__ uint64_t smem[];
+    const int32_t *__restrict__ n_frontier, int F, int K, int N,
+    const float *__restrict__ row_lse, const uint64_t *__restrict__ row_keys,
+    int32_t *__restrict__ next_frontier, int32_t *__restrict__ n_next, uint32_t *d_err) {
+  extern __shared__ uint64_t skey[];  // [pow2(F * K)]
   const int b = blockIdx.x, tid = threadIdx.x;
   const int cap = tree.cap;
   int Fb = n_frontier ? n_frontier[b] : F;
@@ -69,9 +42,6 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
   const int nb = tree.n_nodes[b];
   const int total = Fb * K;
   const int P2 = pow2_at_least(total > 0 ? total : 1);
-  uint64_t *topk = smem;                       // [F*K]
-  uint64_t *skey = smem + (size_t)F * K;       // [skey_cap >= max(P2, chunks*K)]
-  float *lse_s = reinterpret_cast<float *>(skey + skey_cap);  // [F]
 
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
@@ -79,16 +49,6 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
     bad |= v < -1 || v >= nb;
   }
   bad = __syncthreads_or(bad);
-
-  // finish the live rows: lse (a thread per row) and top-K (skey as stage)
-  for (int f = tid; f < Fb; f += kThreads) {
-    const size_t slot = (size_t)b * F + f;
-    const float lse = finish_lse(part_ms + slot * n_ms, n_ms);
-    lse_s[f] = lse;
-    row_lse[slot] = lse;
-  }
-  block_finish_topk(part_keys + (size_t)b * F * chunks * K, chunks, K, Fb, topk, skey,
-                    skey_cap);
 
   const bool full = !bad && (nb + total > cap);
   if (bad || full) {
@@ -107,11 +67,11 @@ __global__ __launch_bounds__(kThreads) void expand_tree_kernel(
       continue;
     }
     const int f = c / K;
-    const uint64_t key = topk[c];
+    const uint64_t key = row_keys[(size_t)b * F * K + c];
     const int v = frontier[(size_t)b * F + f];
     const float cv = v < 0 ? 0.0f : tree.cum[base + v];
     const int dv = v < 0 ? 0 : tree.depth[base + v];
-    const float lp = edge_logp(key_logit(key), lse_s[f]);
+    const float lp = edge_logp(key_logit(key), row_lse[(size_t)b * F + f]);
     const float cum = __fadd_rn(cv, lp);
     const int id = nb + c;
     tree.parent[base + id] = v;
@@ -196,14 +156,14 @@ __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
 //   vmap, rrow, rpid, rdep, rcum  [cap] each (the variant region);
 //   stage = the logp scratch, flags = inC / done, candidates = skey.
 __device__ void graft_variant(const tg_tree &tree, int b, int nb, int nF, int M, int W,
-                              int N, int R, int chunks, uint32_t flags,
-                              const uint64_t *__restrict__ part_keys, const float *lse_s,
+                              int N, int R, uint32_t flags,
+                              const uint64_t *__restrict__ row_keys, const float *lse_s,
                               const float *cum_s, const int *par_s, int *stage,
                               uint8_t *flag_a, uint8_t *flag_b, uint64_t *skey, int *var,
-                              uint64_t *wstage, int *red, int32_t *graft_frontier,
+                              int *red, int32_t *graft_frontier,
                               int32_t *n_graft, int32_t *next_frontier, int32_t *n_next) {
   __shared__ int rootF_s, nF2_s, rootslot_s;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int tid = threadIdx.x;
   const int cap = tree.cap;
   const size_t base = (size_t)b * cap;
   int *vmap = var, *rrow = var + cap, *rpid = var + 2 * cap, *rdep = var + 3 * cap;
@@ -304,11 +264,10 @@ __device__ void graft_variant(const tg_tree &tree, int b, int nb, int nF, int M,
   }
   const int nF2 = nF2_s;
 
-  // candidates of every (slot, rank) in skey: a wave per slot
-  for (int f = w; f < nF2; f += kWaves) {
-    const size_t slot = (size_t)b * R + rrow[f];
-    const uint64_t key = wave_finish_topk(part_keys + slot * chunks * M, chunks, M, wstage);
-    if (lane < M) skey[f * M + lane] = key;
+  // candidates of every (slot, rank) in skey
+  for (int c = tid; c < nF2 * M; c += kThreads) {
+    const int f = c / M;
+    skey[c] = row_keys[((size_t)b * R + rrow[f]) * M + (c - f * M)];
   }
   __syncthreads();
   const int total_c = nF2 * M;
@@ -382,11 +341,10 @@ __device__ void graft_variant(const tg_tree &tree, int b, int nb, int nF, int M,
 // ------------------------------------------------ rescore + reselect + graft
 __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     tg_tree tree, const float *__restrict__ strong, int R, int V, int W, int M,
-    int chunks, int n_ms, const uint8_t *__restrict__ needed,
-    const float2 *__restrict__ part_ms, const uint64_t *__restrict__ part_keys,
-    float *__restrict__ row_lse, int32_t *__restrict__ graft_frontier,
+    const uint8_t *__restrict__ needed, const float *__restrict__ row_lse,
+    const uint64_t *__restrict__ row_keys, int32_t *__restrict__ graft_frontier,
     int32_t *__restrict__ n_graft, int32_t *__restrict__ next_frontier,
-    int32_t *__restrict__ n_next, int N, uint32_t *d_err, int stage_off, uint32_t flags,
+    int32_t *__restrict__ n_next, int N, uint32_t *d_err, uint32_t flags,
     const int32_t *__restrict__ new_from, int var_off) {
   extern __shared__ uint64_t smem[];
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -442,15 +400,10 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   int poolC = root_in;
   for (int i = 0; i < kWaves; ++i) poolC += red[i];
 
-  // ---- log-sum-exp of every needed row (a thread per row), exported
+  // ---- log-sum-exp of every needed row
   const uint8_t *need = needed + (size_t)b * R;
-  for (int r = tid; r <= nb; r += kThreads) {
-    if (!need[r]) continue;
-    const size_t slot = (size_t)b * R + r;
-    const float lse = finish_lse(part_ms + slot * n_ms, n_ms);
-    lse_s[r] = lse;
-    row_lse[slot] = lse;
-  }
+  for (int r = tid; r <= nb; r += kThreads)
+    if (need[r]) lse_s[r] = row_lse[(size_t)b * R + r];
   __syncthreads();
 
   const int nF = min(W, poolC);
@@ -525,39 +478,30 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   __syncthreads();
 
   if (flags & (TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP)) {
-    graft_variant(tree, b, nb, nF, M, W, N, R, chunks, flags, part_keys, lse_s, cum_s,
-                  par_s, reinterpret_cast<int *>(lp_s), inC, done, skey,
-                  reinterpret_cast<int *>(reinterpret_cast<char *>(smem) + var_off),
-                  reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(smem) + stage_off) +
-                      (size_t)w * (chunks * M),
-                  red, graft_frontier, n_graft, next_frontier, n_next);
+    graft_variant(tree, b, nb, nF, M, W, N, R, flags, row_keys, lse_s, cum_s, par_s,
+                  reinterpret_cast<int *>(lp_s), inC, done, skey,
+                  reinterpret_cast<int *>(reinterpret_cast<char *>(smem) + var_off), red,
+                  graft_frontier, n_graft, next_frontier, n_next);
     return;
   }
 
-  // ---- non-destructive graft: new children only, ids nb + f*M + j
-  // (wave-private LDS for finishing each graft point's top-M; the region of
-  // the per-node scratch, free by now, or extra room past it)
-  uint64_t *wstage = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(smem) + stage_off) +
-                     (size_t)w * (chunks * M);
-  for (int f = w; f < nF; f += kWaves) {
+  // ---- non-destructive graft: new children only, ids nb + f*M + j (a
+  // thread per child)
+  for (int c = tid; c < nF * M; c += kThreads) {
+    const int f = c / M;
     const int v = node_key_id(skey[f]);
     const int row = v + 1;
-    const size_t slot = (size_t)b * R + row;
-    const uint64_t key = wave_finish_topk(part_keys + slot * chunks * M, chunks, M, wstage);
+    const uint64_t key = row_keys[((size_t)b * R + row) * M + (c - f * M)];
     const float cv = v < 0 ? 0.0f : cum_s[v];
     const int dv = v < 0 ? 0 : tree.depth[base + v];
-    const float lse = lse_s[row];
-    if (lane < M) {
-      const int j = lane;
-      const float lp = edge_logp(key_logit(key), lse);
-      const int id = nb + f * M + j;
-      tree.parent[base + id] = v;
-      tree.token[base + id] = (int)key_token(key);
-      tree.depth[base + id] = dv + 1;
-      tree.logp[base + id] = lp;
-      tree.cum[base + id] = __fadd_rn(cv, lp);
-      tree.visited[base + id] = 0;
-    }
+    const float lp = edge_logp(key_logit(key), lse_s[row]);
+    const int id = nb + c;
+    tree.parent[base + id] = v;
+    tree.token[base + id] = (int)key_token(key);
+    tree.depth[base + id] = dv + 1;
+    tree.logp[base + id] = lp;
+    tree.cum[base + id] = __fadd_rn(cv, lp);
+    tree.visited[base + id] = 0;
   }
   for (int f = tid; f < W; f += kThreads)
     graft_frontier[(size_t)b * W + f] = f < nF ? node_key_id(skey[f]) : TG_NO_NODE;
@@ -603,29 +547,18 @@ hipError_t launch_tree_reset(const tg_tree &tree, int B, hipStream_t stream) {
   return hipGetLastError();
 }
 
-static int expand_skey_cap(int F, int K, int chunks) {
-  // the sort needs pow2(F*K) keys; finishing rows wants every row's chunk
-  // lists staged at once (one global round trip), up to 64 KiB of them
-  const int total = F * K;
-  const int stage_all = std::min(F * chunks * K, 8192);
-  return std::max({pow2_at_least(total > 0 ? total : 1), chunks * K, stage_all});
-}
-
 hipError_t launch_expand_tree(const tg_tree &tree, const int32_t *frontier,
                               const int32_t *n_frontier, int B, int F, int K,
-                              int N, RowPlan plan, const float2 *part_ms,
-                              const uint64_t *part_keys, float *row_lse,
+                              int N, const float *row_lse, const uint64_t *row_keys,
                               int32_t *next_frontier, int32_t *n_next,
                               uint32_t *d_err, hipStream_t stream) {
-  const int skey_cap = expand_skey_cap(F, K, plan.chunks);
-  const size_t lds = (size_t)F * K * 8 + (size_t)skey_cap * 8 + (size_t)F * 4;
+  const size_t lds = (size_t)pow2_at_least(F * K) * 8;
   hipError_t e = hipFuncSetAttribute((const void *)expand_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
   launch("expand_tree", expand_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
-         frontier, n_frontier, F, K, N, plan.chunks, plan.ms_per_row, part_ms, part_keys,
-         row_lse, next_frontier, n_next, d_err, skey_cap);
+         frontier, n_frontier, F, K, N, row_lse, row_keys, next_frontier, n_next, d_err);
   return hipGetLastError();
 }
 
@@ -637,51 +570,38 @@ hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *neede
   return hipGetLastError();
 }
 
-size_t rescore_tree_lds(int cap, int M, RowPlan plan, uint32_t flags, int *stage_off,
-                        int *var_off) {
+size_t rescore_tree_lds(int cap, uint32_t flags, int *var_off) {
   // layout sized by cap (the kernel uses it up to the live node count):
   // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent [cap] | inC, done [cap]
   // (| variant records [5 cap] ints when a graft variant is on)
   const int n = cap;
-  const size_t keys_b = (size_t)pow2_at_least(n + 1) * 8;
-  const size_t head_b = keys_b + (size_t)(n + 1) * 4 + (size_t)n * 4;  // up to logp
-  const size_t scratch_b = (size_t)n * (4 + 4 + 1 + 1);                // logp..done
-  size_t lds = head_b + scratch_b;
-  // per-wave top-M staging reuses logp..done when they are large enough
-  const size_t stage_b = (size_t)(kThreads / kWave) * plan.chunks * M * 8;
-  size_t so = (head_b + 7) / 8 * 8;
-  if (plan.chunks > 1 && so + stage_b > head_b + scratch_b) {
-    so = (lds + 7) / 8 * 8;
-    lds = so + stage_b;
-  }
+  size_t lds = (size_t)pow2_at_least(n + 1) * 8 + (size_t)(n + 1) * 4 +
+               (size_t)n * (4 + 4 + 4 + 1 + 1);
   size_t vo = 0;
   if (flags & (TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP)) {
     vo = (lds + 15) / 16 * 16;
     lds = vo + (size_t)5 * n * 4;
   }
-  *stage_off = (int)so;
   *var_off = (int)vo;
   return lds;
 }
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
-                               int R, int V, int W, int M, RowPlan plan,
-                               const uint8_t *needed, const float2 *part_ms,
-                               const uint64_t *part_keys, float *row_lse,
+                               int R, int V, int W, int M, const uint8_t *needed,
+                               const float *row_lse, const uint64_t *row_keys,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t flags, const int32_t *new_from,
                                uint32_t *d_err, hipStream_t stream) {
-  int stage_off = 0, var_off = 0;
-  const size_t lds = rescore_tree_lds(tree.cap, M, plan, flags, &stage_off, &var_off);
+  int var_off = 0;
+  const size_t lds = rescore_tree_lds(tree.cap, flags, &var_off);
   hipError_t e = hipFuncSetAttribute((const void *)rescore_tree_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
   launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
-         strong, R, V, W, M, plan.chunks, plan.ms_per_row, needed, part_ms, part_keys,
-         row_lse, graft_frontier, n_graft, next_frontier, n_next, N, d_err, stage_off, flags,
-         new_from, var_off);
+         strong, R, V, W, M, needed, row_lse, row_keys, graft_frontier, n_graft,
+         next_frontier, n_next, N, d_err, flags, new_from, var_off);
   return hipGetLastError();
 }
 
