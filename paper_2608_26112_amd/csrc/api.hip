@@ -175,8 +175,8 @@ tg_status tg_tree_rescore_graft(const tg_tree *tree, const float *strong_logits,
   if (e != hipSuccess) return TG_ERR_HIP;
   e = tg::launch_row_finish(B, R, M, plan, nullptr, needed, ms, keys, row_lse, fin, st);
   if (e != hipSuccess) return TG_ERR_HIP;
-  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, needed,
-                                          row_lse, fin, graft_frontier, n_graft,
+  return from_hip(tg::launch_rescore_tree(*tree, strong_logits, B, R, V, W, M, row_lse, fin,
+                                          graft_frontier, n_graft,
                                           next_frontier, n_next, next_frontier ? N : 0,
                                           flags, new_from, d_err, st));
 }

@@ -95,8 +95,16 @@ __global__ __launch_bounds__(kThreads) void ngram_fallback_kernel(
   if (tid == 0) fallback_pos[b] = (int32_t)last - 1;
 }
 
-constexpr int kCtxLds = 4096;  // prompts up to this many tokens are scanned from LDS
+constexpr int kCtxLds = 4096;             // prompts up to this many tokens are scanned from LDS
+constexpr int kCtxPer = kCtxLds / kThreads;  // prompt tokens a thread holds in registers
+constexpr int kTreeLds = 1024;            // nodes whose fields are staged in LDS
+constexpr int kTreePer = kTreeLds / kThreads;
 
+// One workgroup per tree.  Every global read the step can issue up front is
+// issued in one batch (bounded by the array sizes; the live sizes mask the
+// values afterwards): the prompt's first kCtxLds tokens (kept in registers
+// for the scan and copied to LDS for the match extension), the fields of the
+// first kTreeLds nodes, the frontier.
 __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     tg_tree tree, const int32_t *__restrict__ frontier, const int32_t *__restrict__ n_frontier,
     int F, const int32_t *__restrict__ context, const int32_t *__restrict__ ctx_len, int L,
@@ -107,7 +115,9 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   // dynamic LDS: keys [pow2(F*K)] | best [F] u64 | suffixes [F * n_max] | plen [F]
   extern __shared__ uint64_t skey[];
   __shared__ int32_t ctx_s[kCtxLds];
-  const int b = blockIdx.x, tid = threadIdx.x;
+  __shared__ int32_t par_s[kTreeLds], tok_s[kTreeLds], dep_s[kTreeLds];
+  __shared__ float cum_s[kTreeLds];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1);
   const int cap = tree.cap;
   const size_t base = (size_t)b * cap;
   int Fb = n_frontier ? n_frontier[b] : F;
@@ -120,11 +130,45 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   int32_t *suf = reinterpret_cast<int32_t *>(best + F);
   int32_t *plen = suf + F * n_max;
   const int32_t *ctx_g = context + (size_t)b * L;
+  const int32_t *fr = frontier + (size_t)b * F;
 
+  // ---- one batch of reads
+  const int Lr = min(L, kCtxLds), nt = min(cap, kTreeLds);
+  int32_t cr[kCtxPer];
+#pragma unroll
+  for (int i = 0; i < kCtxPer; ++i) {
+    const int j = tid + i * kThreads;
+    cr[i] = j < Lr ? ctx_g[j] : 0;
+  }
+  int32_t tp[kTreePer], tt[kTreePer], td[kTreePer];
+  float tc[kTreePer];
+#pragma unroll
+  for (int i = 0; i < kTreePer; ++i) {
+    const int v = tid + i * kThreads;
+    tp[i] = v < nt ? tree.parent[base + v] : -1;
+    tt[i] = v < nt ? tree.token[base + v] : 0;
+    td[i] = v < nt ? tree.depth[base + v] : 0;
+    tc[i] = v < nt ? tree.cum[base + v] : 0.0f;
+  }
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
-    const int v = frontier[(size_t)b * F + f];
+    const int v = fr[f];
     bad |= v < -1 || v >= nb;
+  }
+#pragma unroll
+  for (int i = 0; i < kCtxPer; ++i) {
+    const int j = tid + i * kThreads;
+    if (j < Lr) ctx_s[j] = cr[i];
+  }
+#pragma unroll
+  for (int i = 0; i < kTreePer; ++i) {
+    const int v = tid + i * kThreads;
+    if (v < nt) {
+      par_s[v] = tp[i];
+      tok_s[v] = tt[i];
+      dep_s[v] = td[i];
+      cum_s[v] = tc[i];
+    }
   }
   bad = __syncthreads_or(bad);
   const bool no_ctx = !bad && (Lb <= 0 || Lb > L);
@@ -144,54 +188,71 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     if (tid == 0) report(d_err, TG_DERR_BAD_NODE);
     fb = Lb - 1;
   }
-
-  // ---- the prompt in LDS (when it fits), every frontier node's suffix
   const bool in_lds = Lb <= kCtxLds;
-  if (in_lds)
-    for (int i = tid; i < Lb; i += kThreads) ctx_s[i] = ctx_g[i];
+  auto tok_of = [&](int u) { return u < nt ? tok_s[u] : tree.token[base + u]; };
+  auto par_of = [&](int u) { return u < nt ? par_s[u] : tree.parent[base + u]; };
+  auto ctx_at = [&](int i) { return in_lds ? ctx_s[i] : ctx_g[i]; };
+
+  // ---- every frontier node's suffix: the prefix's last n_max tokens, newest
+  // first (the node's path, then the prompt's tail)
   for (int f = tid; f < Fb; f += kThreads) {
-    // the prefix's last n_max tokens, newest first: the node's path, then
-    // the context's tail
     int32_t *sf = suf + f * n_max;
     int k = 0;
-    for (int u = frontier[(size_t)b * F + f]; u >= 0 && k < n_max; ++k) {
-      sf[k] = tree.token[base + u];
-      const int p = tree.parent[base + u];
+    for (int u = fr[f]; u >= 0 && k < n_max; ++k) {
+      sf[k] = tok_of(u);
+      const int p = par_of(u);
       u = (p < -1 || p >= u) ? -1 : p;
     }
-    for (int i = Lb - 1; i >= 0 && k < n_max; --i, ++k) sf[k] = ctx_g[i];
+    for (int i = Lb - 1; i >= 0 && k < n_max; --i, ++k) sf[k] = ctx_at(i);
     plen[f] = k;
     best[f] = 0;
   }
   __syncthreads();
 
   // ---- latest longest match of every node.  The first token decides almost
-  // every position, so it is compared for a thread's positions together and
-  // only the hits are extended.  (Called with the LDS copy or the global
-  // prompt, each with its own address space.)
-  auto scan = [&](const int32_t *cx) __attribute__((always_inline)) {
+  // every position: a thread compares its prompt tokens (registers) for every
+  // node and extends only the hits.  Key (length, position), larger is better.
+  if (in_lds) {
+    for (int f = 0; f < Fb; ++f) {
+      const int32_t *sf = suf + f * n_max;
+      const int pl = plen[f];
+      const int32_t s0 = sf[0];
+      uint32_t mine = 0;  // length << 27 | position (positions < kCtxLds)
+#pragma unroll
+      for (int i = 0; i < kCtxPer; ++i) {
+        const int j = tid + i * kThreads;
+        if (j < Lb && cr[i] == s0) {
+          int l = 1;
+          const int lim = min(pl, j + 1);
+          while (l < lim && ctx_s[j - l] == sf[l]) ++l;
+          const uint32_t key = ((uint32_t)l << 27) | (uint32_t)j;
+          mine = key > mine ? key : mine;
+        }
+      }
+      mine = wave_max_u32(mine);
+      if (lane == 0 && mine)
+        atomicMax(reinterpret_cast<unsigned long long *>(best + f),
+                  ((unsigned long long)(mine >> 27) << 32) | (mine & 0x7ffffffu));
+    }
+  } else {
     for (int f = 0; f < Fb; ++f) {
       const int32_t *sf = suf + f * n_max;
       const int pl = plen[f];
       const int s0 = sf[0];
       uint64_t mine = 0;
       for (int j = tid; j < Lb; j += kThreads) {
-        if (cx[j] != s0) continue;
+        if (ctx_g[j] != s0) continue;
         int l = 1;
         const int lim = min(pl, j + 1);
-        while (l < lim && cx[j - l] == sf[l]) ++l;
+        while (l < lim && ctx_g[j - l] == sf[l]) ++l;
         const uint64_t key = ((uint64_t)l << 32) | (uint64_t)j;
         mine = key > mine ? key : mine;
       }
       mine = wave_max_u64(mine);
-      if ((tid & (kWave - 1)) == 0 && mine)
+      if (lane == 0 && mine)
         atomicMax(reinterpret_cast<unsigned long long *>(best + f), (unsigned long long)mine);
     }
-  };
-  if (in_lds)
-    scan(ctx_s);
-  else
-    scan(ctx_g);
+  }
   __syncthreads();
   for (int f = tid; f < Fb; f += kThreads) {
     const int pos = best[f] ? (int)(uint32_t)best[f] : fb;
@@ -207,10 +268,10 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
       continue;
     }
     const int f = c / K, k = c - f * K;
-    const int v = frontier[(size_t)b * F + f];
+    const int v = fr[f];
     const size_t row = ((size_t)b * L + plen[f]) * m + k;
-    const float cv = v < 0 ? 0.0f : tree.cum[base + v];
-    const int dv = v < 0 ? 0 : tree.depth[base + v];
+    const float cv = v < 0 ? 0.0f : (v < nt ? cum_s[v] : tree.cum[base + v]);
+    const int dv = v < 0 ? 0 : (v < nt ? dep_s[v] : tree.depth[base + v]);
     const float lp = cand_logp[row];
     const float cum = __fadd_rn(cv, lp);
     const int id = nb + c;

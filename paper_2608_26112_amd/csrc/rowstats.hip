@@ -108,6 +108,66 @@ __device__ __forceinline__ int block_sum(int c, int *slots, int &par) {
   return t;
 }
 
+// Heavy ties (more than kCandCap elements reach the bound): the grain's
+// exact K-th key by bisection, first over the order image o (the largest o
+// with at least K elements >= o), then over the token bound among the
+// elements equal to o that completes K; the elements with a larger key go to
+// cand[K ..] (cntf_s counts them).  The grain is re-read from global memory
+// (values cleaned as in the row pass) in batches of eight, so the row pass
+// keeps no per-element state for this rare path.  Called by the whole block.
+__device__ __noinline__ void grain_bisect_topk(const float *__restrict__ row, int e0, int e1,
+                                               bool vec, int K, uint64_t *cand, int *cntf_s,
+                                               int *red) {
+  const int tid = threadIdx.x;
+  constexpr int kB = 8;
+  // f(j, order image) over the thread's valid elements
+  auto each = [&](auto f) {
+#pragma unroll 1
+    for (int j0 = 0; j0 < kPer; j0 += kB) {
+      float v[kB];
+#pragma unroll
+      for (int u = 0; u < kB; ++u) {
+        const int t = elem_token(vec, e0, tid, j0 + u);
+        v[u] = t < e1 ? row[t] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < kB; ++u) {
+        const int t = elem_token(vec, e0, tid, j0 + u);
+        bool b = false;
+        if (t < e1) f(t, float_order(clean_logit(v[u], b)));
+      }
+    }
+  };
+  int par = 0;
+  __syncthreads();  // the caller's block sums are done with red
+  uint32_t o = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cb = o | (1u << bit);
+    int q = 0;
+    each([&](int, uint32_t oj) { q += oj >= cb; });
+    if (block_sum(q, red, par) >= K) o = cb;
+  }
+  int q = 0;
+  each([&](int, uint32_t oj) { q += oj > o; });
+  const int need = K - block_sum(q, red, par);
+  int lo = e0, hi = e1 - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    int qq = 0;
+    each([&](int t, uint32_t oj) { qq += oj == o && t <= mid; });
+    if (block_sum(qq, red, par) >= need)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  each([&](int t, uint32_t oj) {
+    if (oj > o || (oj == o && t <= lo)) {
+      const int p = atomicAdd(cntf_s, 1);
+      cand[K + p] = ((uint64_t)oj << 32) | (uint64_t)(0xffffffffu - (uint32_t)t);
+    }
+  });
+}
+
 // One workgroup per chunk of a row; see the file comment.  Per grain:
 //  1. the grain sits in registers (32 elements per thread, one batch of
 //     loads); per thread max, then sum of exp (a NaN result flags NaN/+inf
@@ -122,7 +182,7 @@ __device__ __forceinline__ int block_sum(int c, int *slots, int &par) {
 //     running chunk list's K-th entry;
 //  4. elements >= T are compacted into LDS (about K of them for continuous
 //     logits); with more than kCandCap (heavy ties) the grain's exact K-th
-//     key is found by bisection over the key bits instead;
+//     key is found by bisection over the key bits instead (out of line);
 //  5. the running list and the candidates are ranked by (logit desc, token
 //     asc) and the best K kept.
 __global__ __launch_bounds__(kThreads) void row_partial_kernel(
@@ -262,45 +322,7 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     __syncthreads();
     int n = cnt_s;
     if (n > kCandCap) {
-      // Exact K-th key of the grain: the largest order image o with at least
-      // K elements >= o, then among the elements equal to o the smallest
-      // token bound that completes K.  (n > kCandCap >= K valid elements.)
-      uint32_t ord[kPer];
-#pragma unroll
-      for (int j = 0; j < kPer; ++j)
-        ord[j] = elem_token(vec, e0, tid, j) < e1 ? float_order(x[j]) : 0u;
-      uint32_t o = 0;
-      for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t cb = o | (1u << bit);
-        int q = 0;
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) q += ord[j] >= cb;
-        if (block_sum(q, red, rpar) >= K) o = cb;
-      }
-      int q = 0;
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) q += ord[j] > o;
-      const int need = K - block_sum(q, red, rpar);
-      int lo = e0, hi = e1 - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        int qq = 0;
-#pragma unroll
-        for (int j = 0; j < kPer; ++j)
-          qq += ord[j] == o && elem_token(vec, e0, tid, j) <= mid;
-        if (block_sum(qq, red, rpar) >= need)
-          hi = mid;
-        else
-          lo = mid + 1;
-      }
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) {
-        const int t = elem_token(vec, e0, tid, j);
-        if (ord[j] > o || (ord[j] == o && t <= lo)) {
-          const int p = atomicAdd(&cntf_s, 1);
-          cand[K + p] = ((uint64_t)ord[j] << 32) | (uint64_t)(0xffffffffu - (uint32_t)t);
-        }
-      }
+      grain_bisect_topk(row, e0, e1, vec, K, cand, &cntf_s, red);
       __syncthreads();
       n = cntf_s;
     }

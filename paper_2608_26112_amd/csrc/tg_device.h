@@ -97,8 +97,11 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   const uint32_t ml = wave_max_u32(hi == mh ? (uint32_t)v : 0u);
   return ((uint64_t)mh << 32) | ml;
 }
+// fp32 maximum through the order-preserving unsigned image (one integer DPP
+// max per step; fmaxf would quiet its operands first).  -0.0 comes back as
+// +0.0; a NaN with the sign bit clear orders above +inf.
 __device__ __forceinline__ float wave_max_f32(float v) {
-  return wave_reduce(v, -__builtin_inff(), [](float a, float b) { return fmaxf(a, b); });
+  return order_float(wave_max_u32(float_order(v)));
 }
 __device__ __forceinline__ float wave_sum_f32(float v) {
   return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
@@ -234,10 +237,102 @@ __device__ void block_top_keys_r(uint64_t *key, int n, int k) {
   __syncthreads();
 }
 
+// Descending bitonic sort of one 64-bit key per lane across the wave.
+__device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint64_t p = __shfl_xor(v, j, kWave);
+      const bool take_max = ((lane & j) == 0) == ((lane & k) == 0);
+      v = take_max ? (p > v ? p : v) : (p < v ? p : v);
+    }
+  }
+  return v;
+}
+
+// The k-th and kq-th largest (kq <= k <= 64) of the wave's keys, 0 when
+// fewer lanes hold a present (non-zero) key; keys are distinct.  Small k:
+// rounds of "take the wave maximum, retire its lane"; larger k: a wave sort.
+__device__ __forceinline__ void wave_key_order_stats(uint64_t v, int k, int kq, uint64_t &tk,
+                                                     uint64_t &tq) {
+  tk = 0;
+  tq = 0;
+  if (k > 16) {
+    const uint64_t srt = wave_sort_desc_u64(v);
+    const uint32_t lo = (uint32_t)srt, hi = (uint32_t)(srt >> 32);
+    tk = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, k - 1) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)lo, k - 1);
+    tq = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, kq - 1) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)lo, kq - 1);
+    return;
+  }
+  for (int j = 0; j < k; ++j) {
+    const uint64_t mx = wave_max_u64(v);
+    if (mx == 0) return;
+    if (j == kq - 1) tq = mx;
+    if (j == k - 1) tk = mx;
+    v = v == mx ? 0 : v;
+  }
+}
+
+// block_top_keys for a small k against a larger set (n <= kRankPerThread *
+// kBlock): a lower bound T on the k-th largest key from the thread maxima,
+// each wave on its own (the largest over waves of a wave's k-th largest
+// maximum; the smallest over waves of a wave's ceil(k / waves)-th largest),
+// then only the present keys >= T are compacted to the front and ranked by
+// counting.  Same contract as block_top_keys.  Kept out of line: the common
+// small sets take the inlined counting paths.
+template <int kBlock>
+__device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
+  constexpr int kW = kBlock / kWave;
+  __shared__ uint64_t bnd_s[2][kW];
+  __shared__ int cnt_s;
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  uint64_t mk[kRankPerThread];
+  uint64_t tmax = 0;
+#pragma unroll
+  for (int j = 0; j < kRankPerThread; ++j) {
+    const int i = threadIdx.x + j * kBlock;
+    mk[j] = i < n ? key[i] : 0;
+    tmax = mk[j] > tmax ? mk[j] : tmax;
+  }
+  uint64_t tk, tq;
+  wave_key_order_stats(tmax, k, (k + kW - 1) / kW, tk, tq);
+  if (lane == 0) {
+    bnd_s[0][w] = tk;
+    bnd_s[1][w] = tq;
+  }
+  if (threadIdx.x == 0) cnt_s = 0;
+  __syncthreads();
+  uint64_t T = 0, Tq = ~0ull;
+#pragma unroll
+  for (int i = 0; i < kW; ++i) {
+    T = bnd_s[0][i] > T ? bnd_s[0][i] : T;
+    Tq = bnd_s[1][i] < Tq ? bnd_s[1][i] : Tq;
+  }
+  T = Tq > T ? Tq : T;
+#pragma unroll
+  for (int j = 0; j < kRankPerThread; ++j)
+    if (mk[j] != 0 && mk[j] >= T) key[atomicAdd(&cnt_s, 1)] = mk[j];
+  __syncthreads();
+  const int c = cnt_s;
+  for (int j = c + threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
+  if (c > 2 * kBlock)
+    block_top_keys_r<kBlock, 4>(key, c, k);
+  else if (c > kBlock)
+    block_top_keys_r<kBlock, 2>(key, c, k);
+  else
+    block_top_keys_r<kBlock, 1>(key, c, k);
+}
+
 template <int kBlock>
 __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
   if (n > kRankPerThread * kBlock) {
     block_bitonic_desc(key, P2);
+  } else if ((k <= 16 && n > kBlock) || (k <= kWave && n > 2 * kBlock)) {
+    block_select_top<kBlock>(key, n, k);
   } else if (n > 2 * kBlock) {
     block_top_keys_r<kBlock, 4>(key, n, k);
   } else if (n > kBlock) {

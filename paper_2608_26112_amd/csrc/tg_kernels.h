@@ -73,8 +73,8 @@ hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *neede
 size_t rescore_tree_lds(int cap, uint32_t flags, int *var_off);
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
-                               int R, int V, int W, int M, const uint8_t *needed,
-                               const float *row_lse, const uint64_t *row_keys,
+                               int R, int V, int W, int M, const float *row_lse,
+                               const uint64_t *row_keys,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t flags, const int32_t *new_from,

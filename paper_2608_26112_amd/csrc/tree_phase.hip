@@ -341,7 +341,7 @@ __device__ void graft_variant(const tg_tree &tree, int b, int nb, int nF, int M,
 // ------------------------------------------------ rescore + reselect + graft
 __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
     tg_tree tree, const float *__restrict__ strong, int R, int V, int W, int M,
-    const uint8_t *__restrict__ needed, const float *__restrict__ row_lse,
+    const float *__restrict__ row_lse,
     const uint64_t *__restrict__ row_keys, int32_t *__restrict__ graft_frontier,
     int32_t *__restrict__ n_graft, int32_t *__restrict__ next_frontier,
     int32_t *__restrict__ n_next, int N, uint32_t *d_err, uint32_t flags,
@@ -374,22 +374,71 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   float *cum_s = lse_s + (cap + 1);                        // [cap]
   float *lp_s = cum_s + cap;                               // [cap]
   int *par_s = reinterpret_cast<int *>(lp_s + cap);        // [cap]
-  uint8_t *inC = reinterpret_cast<uint8_t *>(par_s + cap); // [cap]
+  int *dep_s = par_s + cap;                                // [cap]
+  uint8_t *inC = reinterpret_cast<uint8_t *>(dep_s + cap); // [cap]
   uint8_t *done = inC + cap;                               // [cap]
 
-  // ---- pool C and parents
+  // ---- pool C, node fields and the rescored edges
+  // logp[v] = fl(x[pa(v)+1][tok v] - lse[pa(v)+1]) for v in C.  Per batch of
+  // nodes: the fields and the row lse in one round of reads, then for the
+  // pool nodes the strong logit and the parent row's lse in a second.  Rows
+  // that are not needed hold whatever the buffer held and are never read.
   const PoolRule pool = pool_rule(tree, b, nb, flags, new_from);
   if (tid == 0 && pool.newonly && (new_from[b] < -1 || new_from[b] > nb))
     report(d_err, TG_DERR_BAD_NODE);
-  bool badp = false;
+  bool badp = false, badtok = false, nonfin = false;
   int cnt = 0;
-  for (int v = tid; v < nb; v += kThreads) {
-    uint8_t in = pool.in(tree, base, v) ? 1 : 0;
-    inC[v] = in;
-    done[v] = in ? 0 : 1;
-    cum_s[v] = tree.cum[base + v];
-    par_s[v] = sane_parent(tree.parent[base + v], v, badp);
-    cnt += in;
+  constexpr int kBatch = 4;
+  for (int v0 = 0; v0 <= nb; v0 += kBatch * kThreads) {
+    int pv[kBatch], tv[kBatch], dv[kBatch];
+    float cv[kBatch], rl[kBatch];
+    bool in[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int v = v0 + tid + k * kThreads;
+      const bool ok = v < nb;
+      pv[k] = ok ? tree.parent[base + v] : -1;
+      tv[k] = ok ? tree.token[base + v] : 0;
+      dv[k] = ok ? tree.depth[base + v] : 0;
+      cv[k] = ok ? tree.cum[base + v] : 0.0f;
+      in[k] = ok && pool.in(tree, base, v);
+      rl[k] = v <= nb ? row_lse[(size_t)b * R + v] : 0.0f;
+    }
+    float xv[kBatch], lv[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int v = v0 + tid + k * kThreads;
+      xv[k] = -__builtin_inff();
+      lv[k] = 0.0f;
+      if (v < nb) {
+        pv[k] = sane_parent(pv[k], v, badp);
+        if (in[k]) {
+          const size_t prow = (size_t)b * R + (pv[k] + 1);
+          lv[k] = row_lse[prow];
+          if (tv[k] >= 0 && tv[k] < V) xv[k] = strong[prow * V + tv[k]];
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int v = v0 + tid + k * kThreads;
+      if (v <= nb) lse_s[v] = rl[k];
+      if (v >= nb) continue;
+      inC[v] = in[k] ? 1 : 0;
+      done[v] = in[k] ? 0 : 1;
+      cum_s[v] = cv[k];
+      par_s[v] = pv[k];
+      dep_s[v] = dv[k];
+      cnt += in[k] ? 1 : 0;
+      if (in[k]) {
+        float x = -__builtin_inff();
+        if (tv[k] >= 0 && tv[k] < V)
+          x = clean_logit(xv[k], nonfin);
+        else
+          badtok = true;
+        lp_s[v] = edge_logp(x, lv[k]);
+      }
+    }
   }
   const int root_in = pool.root_in(tree, b) ? 1 : 0;
   if (badp) report(d_err, TG_DERR_BAD_PARENT);
@@ -400,36 +449,13 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   int poolC = root_in;
   for (int i = 0; i < kWaves; ++i) poolC += red[i];
 
-  // ---- log-sum-exp of every needed row
-  const uint8_t *need = needed + (size_t)b * R;
-  for (int r = tid; r <= nb; r += kThreads)
-    if (need[r]) lse_s[r] = row_lse[(size_t)b * R + r];
-  __syncthreads();
-
   const int nF = min(W, poolC);
   if (nb + nF * M > cap) {
     fail(TG_DERR_CAPACITY);
     return;
   }
-
-  // ---- rescoring: logp[v] = fl(x[pa(v)+1][tok v] - lse[pa(v)+1])
-  bool badtok = false, nonfin = false;
-  for (int v = tid; v < nb; v += kThreads) {
-    if (!inC[v]) continue;
-    const int p = par_s[v];
-    const int tok = tree.token[base + v];
-    float x = -__builtin_inff();
-    if (tok >= 0 && tok < V)
-      x = clean_logit(strong[((size_t)b * R + (p + 1)) * V + tok], nonfin);
-    else
-      badtok = true;
-    const float lp = edge_logp(x, lse_s[p + 1]);
-    lp_s[v] = lp;
-    tree.logp[base + v] = lp;
-  }
   if (badtok) report(d_err, TG_DERR_BAD_NODE);
   if (nonfin) report(d_err, TG_DERR_NONFINITE);
-  __syncthreads();
 
   // ---- cum recompute, parents before children: rounds of "every pool node
   // whose parent is final takes cum[parent] + logp" (one round per level)
@@ -457,7 +483,7 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   for (int i = tid; i < P2; i += kThreads) {
     uint64_t k = 0;
     if (i < nb) {
-      if (inC[i]) k = node_key(cum_s[i], tree.depth[base + i], i);
+      if (inC[i]) k = node_key(cum_s[i], dep_s[i], i);
     } else if (i == nb && root_in) {
       k = node_key(0.0f, 0, -1);
     }
@@ -470,6 +496,7 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   // whose staging reuses the per-node scratch)
   for (int v = tid; v < nb; v += kThreads) {
     if (inC[v]) {
+      tree.logp[base + v] = lp_s[v];
       tree.cum[base + v] = cum_s[v];
       tree.visited[base + v] = 1;
     }
@@ -486,35 +513,52 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   }
 
   // ---- non-destructive graft: new children only, ids nb + f*M + j (a
-  // thread per child)
-  for (int c = tid; c < nF * M; c += kThreads) {
+  // thread per child; the keys of a thread's first children stay in
+  // registers for the Top_N below)
+  const int total = nF * M;
+  auto graft_child = [&](int c) {
     const int f = c / M;
     const int v = node_key_id(skey[f]);
     const int row = v + 1;
     const uint64_t key = row_keys[((size_t)b * R + row) * M + (c - f * M)];
     const float cv = v < 0 ? 0.0f : cum_s[v];
-    const int dv = v < 0 ? 0 : tree.depth[base + v];
+    const int dv = v < 0 ? 0 : dep_s[v];
     const float lp = edge_logp(key_logit(key), lse_s[row]);
+    const float cum = __fadd_rn(cv, lp);
     const int id = nb + c;
     tree.parent[base + id] = v;
     tree.token[base + id] = (int)key_token(key);
     tree.depth[base + id] = dv + 1;
     tree.logp[base + id] = lp;
-    tree.cum[base + id] = __fadd_rn(cv, lp);
+    tree.cum[base + id] = cum;
     tree.visited[base + id] = 0;
+    return node_key(cum, dv + 1, id);
+  };
+  constexpr int kRegChildren = 4;
+  uint64_t ck[kRegChildren];
+#pragma unroll
+  for (int k = 0; k < kRegChildren; ++k) {
+    const int c = tid + k * kThreads;
+    ck[k] = c < total ? graft_child(c) : 0;
   }
+  for (int c = tid + kRegChildren * kThreads; c < total; c += kThreads) graft_child(c);
   for (int f = tid; f < W; f += kThreads)
     graft_frontier[(size_t)b * W + f] = f < nF ? node_key_id(skey[f]) : TG_NO_NODE;
   if (tid == 0) {
-    tree.n_nodes[b] = nb + nF * M;
+    tree.n_nodes[b] = nb + total;
     n_graft[b] = nF;
   }
   // ---- Top_N of the grafted children (the next small step's frontier)
   if (N > 0) {
-    __syncthreads();  // children written above are visible to the block
-    const int total = nF * M;
+    __syncthreads();  // the graft frontier is read; children past the
+                      // registers are visible to the block
     const int P2c = pow2_at_least(total > 0 ? total : 1);
-    for (int c = tid; c < P2c; c += kThreads) {
+#pragma unroll
+    for (int k = 0; k < kRegChildren; ++k) {
+      const int c = tid + k * kThreads;
+      if (c < P2c) skey[c] = ck[k];
+    }
+    for (int c = tid + kRegChildren * kThreads; c < P2c; c += kThreads) {
       uint64_t k = 0;
       if (c < total) {
         const int id = nb + c;
@@ -572,11 +616,11 @@ hipError_t launch_rescore_pool(const tg_tree &tree, int B, int R, uint8_t *neede
 
 size_t rescore_tree_lds(int cap, uint32_t flags, int *var_off) {
   // layout sized by cap (the kernel uses it up to the live node count):
-  // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent [cap] | inC, done [cap]
-  // (| variant records [5 cap] ints when a graft variant is on)
+  // keys [pow2(cap+1)] | lse [cap+1] | cum, logp, parent, depth [cap] |
+  // inC, done [cap] (| variant records [5 cap] ints when a graft variant is on)
   const int n = cap;
   size_t lds = (size_t)pow2_at_least(n + 1) * 8 + (size_t)(n + 1) * 4 +
-               (size_t)n * (4 + 4 + 4 + 1 + 1);
+               (size_t)n * (4 + 4 + 4 + 4 + 1 + 1);
   size_t vo = 0;
   if (flags & (TG_GRAFT_OVERWRITE | TG_GRAFT_DEDUP)) {
     vo = (lds + 15) / 16 * 16;
@@ -587,8 +631,7 @@ size_t rescore_tree_lds(int cap, uint32_t flags, int *var_off) {
 }
 
 hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
-                               int R, int V, int W, int M, const uint8_t *needed,
-                               const float *row_lse, const uint64_t *row_keys,
+                               int R, int V, int W, int M, const float *row_lse, const uint64_t *row_keys,
                                int32_t *graft_frontier, int32_t *n_graft,
                                int32_t *next_frontier, int32_t *n_next, int N,
                                uint32_t flags, const int32_t *new_from,
@@ -600,7 +643,7 @@ hipError_t launch_rescore_tree(const tg_tree &tree, const float *strong, int B,
                                      (int)lds);
   if (e != hipSuccess) return e;
   launch("rescore_tree", rescore_tree_kernel, dim3(B), dim3(kThreads), lds, stream, tree,
-         strong, R, V, W, M, needed, row_lse, row_keys, graft_frontier, n_graft,
+         strong, R, V, W, M, row_lse, row_keys, graft_frontier, n_graft,
          next_frontier, n_next, N, d_err, flags, new_from, var_off);
   return hipGetLastError();
 }

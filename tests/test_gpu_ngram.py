@@ -147,3 +147,25 @@ def test_llama8b_shape_prefill_and_steps(tg):
     fr, nf = np.full((1, 1), -1, np.int32), np.ones(1, np.int32)
     for step in range(3):
         t, fr, nf, mp = run_expand(tg, t, fr, nf, ctx, clen, tok_h, lp_h, fb_h, 8, 10, 4)
+
+
+@pytest.mark.parametrize("n_max", [1, 2, 4, 5, 16])
+@pytest.mark.parametrize("L", [300, 4096, 4097])
+def test_match_paths(tg, n_max, L):
+    """The match scan's three paths against the oracle: n-grams up to 4
+    tokens matched in registers, longer ones extended through LDS, and
+    prompts past 4096 tokens scanned from global memory.  A 30-token
+    vocabulary makes long repeated n-grams common."""
+    g = W.rng([950, n_max, L])
+    B, V, m, K, N = 2, 40, 4, 2, 6
+    ctx = np.stack([W.token_stream(g, L, 30) for _ in range(B)])
+    clen = np.array([L, L - 7], np.int32)
+    logits = W.normal(g, (B, L, V), 2.0)
+    tok, lp, fb = _cache_close(tg, logits, ctx, clen, m)
+    t = OT.Tree.empty(B, 256)
+    fr, nf = np.full((B, 1), -1, np.int32), np.ones(B, np.int32)
+    lens = []
+    for step in range(3):
+        t, fr, nf, mp = run_expand(tg, t, fr, nf, ctx, clen, tok, lp, fb, K, N, n_max)
+        lens.append(mp)
+    assert all((x >= 0).any() for x in lens)
