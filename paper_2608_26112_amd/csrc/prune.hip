@@ -2,13 +2,15 @@
 // verification buffers (Alg. 3), and the cache update after acceptance.
 //
 // prune_kernel: one workgroup per tree, everything in LDS (n <= 4096):
-//   depths by pointer jumping over the parent links (log2 n rounds);
-//   rank: exact rank of each node key (cum desc, depth asc, id asc) by
-//         counting the larger keys (keys are distinct), a bitonic sort past
-//         1024 nodes;
-//   keep: when every parent ranks before its children the kept set is the
-//         first B_ver ranked nodes (one parallel check); otherwise one thread
-//         runs the literal loop (chains added while they fit);
+//   depths by pointer jumping over the parent links (until every chain has
+//         reached the root);
+//   keep: node keys (cum desc, depth asc, id asc) are distinct and order the
+//         nodes as their ranks do, so one parallel pass checks that every
+//         parent's key is larger than its children's; then the kept set is
+//         the B_ver largest keys (selected, not ranked); otherwise the nodes
+//         are ranked exactly (counting the larger keys, a bitonic sort past
+//         1024 nodes) and one thread runs the literal loop (chains added
+//         while they fit);
 //   re-index: the kept nodes, compacted by a block scan, ranked the same way
 //         by (depth, id);
 //   buffers: parents, tokens, depths, ancestor bitsets, root-to-leaf paths.
@@ -90,25 +92,11 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   }
   const int16_t *depth = dep[cur];
 
-  // ---- rank by (cum desc, depth asc, id asc): exact ranks by counting
-  // (keys are distinct) for up to kRankCountMax nodes, else a bitonic sort
-  int16_t *rank = anc[cur ^ 1];  // free now
+  // ---- keys by (cum desc, depth asc, id asc); keys are distinct, and a
+  // node ranks before another exactly when its key is larger
   const int P2 = pow2_at_least(nn > 0 ? nn : 1);
   for (int i = tid; i < P2; i += kThreads)
     key[i] = i < nn ? node_key(tree.cum[base + i], depth[i], i) : 0;
-  __syncthreads();
-  if (nn <= kRankCountMax) {
-    rank_each<kThreads>(key, nn, [&](int i, uint64_t, int r) { rank[i] = (int16_t)r; });
-    __syncthreads();
-    for (int v = tid; v < nn; v += kThreads) order[rank[v]] = (int16_t)v;  // ranked ids
-  } else {
-    block_bitonic_desc(key, P2);
-    for (int i = tid; i < nn; i += kThreads) {
-      const int v = node_key_id(key[i]);
-      rank[v] = (int16_t)i;
-      order[i] = (int16_t)v;
-    }
-  }
   for (int v = tid; v < nn; v += kThreads) flag[v] = 0;
   __syncthreads();
 
@@ -116,21 +104,40 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   if (nn <= B_ver) {
     for (int v = tid; v < nn; v += kThreads) flag[v] = 1;
   } else {
+    // does some node rank before its parent?  (one direct pass: parent key
+    // against child key)
     bool viol = false;
-    for (int v = tid; v < nn; v += kThreads) viol |= par[v] >= 0 && rank[par[v]] > rank[v];
+    for (int v = tid; v < nn; v += kThreads) viol |= par[v] >= 0 && key[par[v]] < key[v];
     if (viol) viol_s = 1;
     __syncthreads();
     if (!viol_s) {
-      for (int v = tid; v < nn; v += kThreads) flag[v] = rank[v] < B_ver;
-    } else if (tid == 0) {
-      // the literal loop: add each ranked node's missing ancestor chain if it fits
-      int size = 1;
-      for (int i = 0; i < nn && size < M; ++i) {
-        int len = 0;
-        for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) ++len;
-        if (size + len <= M) {
-          for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) flag[u] = 1;
-          size += len;
+      // every ancestor outranks its descendants, so the B_ver best nodes are
+      // closed under parents and are the kept set: select them
+      if (nn > kThreads && nn <= kRankCountMax && B_ver <= kWave)
+        block_select_top<kThreads>(key, nn, B_ver);
+      else
+        block_top_keys<kThreads>(key, nn, P2, B_ver);
+      for (int i = tid; i < B_ver; i += kThreads) flag[node_key_id(key[i])] = 1;
+    } else {
+      // exact ranks (counting for up to kRankCountMax nodes, else a bitonic
+      // sort), then the literal loop: add each ranked node's missing
+      // ancestor chain if it fits
+      if (nn <= kRankCountMax) {
+        rank_each<kThreads>(key, nn, [&](int v, uint64_t, int r) { order[r] = (int16_t)v; });
+      } else {
+        block_bitonic_desc(key, P2);
+        for (int i = tid; i < nn; i += kThreads) order[i] = (int16_t)node_key_id(key[i]);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int size = 1;
+        for (int i = 0; i < nn && size < M; ++i) {
+          int len = 0;
+          for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) ++len;
+          if (size + len <= M) {
+            for (int u = order[i]; u >= 0 && !flag[u]; u = par[u]) flag[u] = 1;
+            size += len;
+          }
         }
       }
     }
