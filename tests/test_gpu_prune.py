@@ -240,3 +240,30 @@ def test_kv_compact_rejects_bad_paths(tg):
     assert int(err.item()) & OT.DERR_BAD_NODE
     assert list(nl.cpu().numpy()) == [8, 6, 2]
     assert torch.equal(k, k0) and torch.equal(v, v0)   # row 0 identity, rows 1-2 rejected
+
+
+@pytest.mark.parametrize("n", [257, 300, 513, 1024])
+def test_prune_selects_kept_set_of_monotone_trees(tg, n):
+    """Trees whose scores never rise from parent to child (as expansion builds
+    them): the kept set is the budget's largest keys, selected without ranking
+    the rest; past 256 nodes this takes the per-wave bound paths for budgets
+    up to 16 and up to 64.  Quantised log-probabilities make ties in cum
+    (broken by depth, then id)."""
+    g = W.rng([560, n])
+    B, cap = 2, 1024
+    t = OT.Tree.empty(B, cap)
+    for b in range(B):
+        par = W.uniform_parents(g, n)
+        lp = (-np.round(np.abs(W.normal(g, (n,), 1.0)) * 4) / 4).astype(np.float32)
+        cum = np.zeros(n, np.float32)
+        for i in range(n):
+            cum[i] = (cum[par[i]] if par[i] >= 0 else np.float32(0.0)) + lp[i]
+        t.parent[b, :n] = par
+        t.cum[b, :n] = cum
+        t.token[b, :n] = g.integers(0, 1000, size=n)
+        t.n_nodes[b] = n
+    for B_ver in (1, 10, 16, 17, 40, 64):
+        got, err = run_prune(tg, t, B_ver, cap + 1)
+        assert err == 0
+        for b in range(B):
+            check_tree(got, t, b, B_ver, cap + 1)
