@@ -83,6 +83,30 @@ def test_signals_grown_trees(tg, seed):
             assert close(sig[b], want), (b, Wd, L, sig[b], want)
 
 
+def test_signals_larger_grown_trees_select_the_preview(tg):
+    """552-node grown trees: the preview frontier Top_W(R) of a few hundred
+    candidates takes the selection paths (a per-wave bound, then counting
+    among the keys above it) for W up to 16 and up to 64."""
+    tree, _ = C.scored_tree(940, 2, 60, steps=7, width=12, K=8, cap=1024)
+    g = W.rng(941)
+    B, F = 2, 12
+    fr = np.full((B, F), -1, np.int32)
+    nf = np.zeros(B, np.int32)
+    for b in range(B):
+        n = int(tree.n_nodes[b])
+        assert n > 512
+        fr[b] = g.choice(np.arange(-1, n), size=F, replace=False)
+        nf[b] = F
+    for Wd, L in ((1, 0), (10, 5), (16, 9), (17, 9), (60, 9)):
+        sig, _, _, err = run(tg, tree, fr, nf, Wd, L)
+        assert err == 0
+        for b in range(B):
+            n = int(tree.n_nodes[b])
+            want, _ = OS.tree_signals(tree.parent[b], tree.depth[b], tree.cum[b], n,
+                                      list(fr[b, :nf[b]]), Wd, L)
+            assert close(sig[b], want), (b, Wd, L, sig[b], want)
+
+
 def test_signals_full_tree_with_infinite_scores_and_margin(tg):
     """4096-node random trees with -inf scores, and the predictor on top."""
     g = W.rng(920)

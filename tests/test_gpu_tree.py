@@ -136,6 +136,7 @@ CASES = [
     (1, 3, 64, 64, 17, "K = V"),
     (4, 32, 30000, 10, 60, "many rows"),
     (1, 64, 128256, 10, 60, "one full-vocab tree"),
+    (2, 40, 3000, 10, 10, "N = 10 of 400 children (selection)"),
 ]
 
 
