@@ -347,7 +347,9 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
 // One wave per row slot, live by the row pass's rule: the row's
 // log-sum-exp from its grain partials, folded in grain order (the lanes load
 // them, the fold reads them lane by lane: the same bits as a serial pass),
-// and its top-K from the chunk lists (staged in LDS, K-round merge).
+// and its top-K from the chunk lists (staged in LDS, K-round merge).  The
+// partials and up to 256 list keys are loaded before the row's liveness is
+// known (the workspace holds every row), so one round trip covers both.
 // Writes lse[s] and out_keys[s * K + j], best first.
 __global__ __launch_bounds__(kThreads) void row_finish_kernel(
     long long slots, int rows_per_batch, int K, int chunks, int n_ms,
@@ -360,15 +362,35 @@ __global__ __launch_bounds__(kThreads) void row_finish_kernel(
   if (s >= slots) return;  // wave-uniform from here on
   const int b = (int)(s / rows_per_batch);
   const int r = (int)(s - (long long)b * rows_per_batch);
-  if (needed) {
-    if (!needed[s]) return;
-  } else if (r >= (n_live ? n_live[b] : rows_per_batch)) {
-    return;
-  }
   const float2 *ms = part_ms + s * n_ms;
+  const uint64_t *lists = part_keys + s * chunks * K;
+  const int nk = chunks * K;
   float2 p = lane < n_ms ? ms[lane] : make_float2(-__builtin_inff(), 0.0f);
-  const uint64_t key = wave_finish_topk(part_keys + s * chunks * K, chunks, K,
-                                        stage + (size_t)w * chunks * K);
+  uint64_t t[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = u * kWave + lane;
+    t[u] = (chunks > 1 && i < nk) ? lists[i] : 0;
+  }
+  const bool live = needed ? needed[s] != 0 : r < (n_live ? n_live[b] : rows_per_batch);
+  if (!live) return;
+  uint64_t key;
+  uint64_t *ws = stage + (size_t)w * nk;
+  if (chunks == 1) {
+    key = lane < K ? lists[lane] : 0;
+  } else if (nk <= 4 * kWave) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = u * kWave + lane;
+      if (i < nk) ws[i] = t[u];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    key = wave_merge_lists(ws, chunks, K);
+  } else {
+    key = wave_finish_topk(lists, chunks, K, ws);
+  }
   float m = -__builtin_inff(), sum = 0.0f;
   for (int i0 = 0; i0 < n_ms; i0 += kWave) {
     if (i0 > 0) p = i0 + lane < n_ms ? ms[i0 + lane] : make_float2(-__builtin_inff(), 0.0f);
