@@ -100,11 +100,18 @@ constexpr int kCtxPer = kCtxLds / kThreads;  // prompt tokens a thread holds in 
 constexpr int kTreeLds = 1024;            // nodes whose fields are staged in LDS
 constexpr int kTreePer = kTreeLds / kThreads;
 
+// 64-bit words of the region the suffixes and then the child keys share.
+__host__ __device__ inline int ngram_region_words(int F, int K, int n_max) {
+  const int keys = pow2_at_least(F * K > 0 ? F * K : 1);
+  const int sufw = (F * n_max + 1) / 2;
+  return keys > sufw ? keys : sufw;
+}
+
 // One workgroup per tree.  Every global read the step can issue up front is
 // issued in one batch (bounded by the array sizes; the live sizes mask the
 // values afterwards): the prompt's first kCtxLds tokens (kept in registers
 // for the scan and copied to LDS for the match extension), the fields of the
-// first kTreeLds nodes, the frontier.
+// first kTreeLds nodes, the frontier (kept in LDS).
 __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     tg_tree tree, const int32_t *__restrict__ frontier, const int32_t *__restrict__ n_frontier,
     int F, const int32_t *__restrict__ context, const int32_t *__restrict__ ctx_len, int L,
@@ -112,7 +119,9 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     const int32_t *__restrict__ fallback_pos, int m, int K, int N, int n_max,
     int32_t *__restrict__ match_pos, int32_t *__restrict__ next_frontier,
     int32_t *__restrict__ n_next, uint32_t *d_err) {
-  // dynamic LDS: keys [pow2(F*K)] | best [F] u64 | suffixes [F * n_max] | plen [F]
+  // dynamic LDS: one region holding first the suffixes [F * n_max] int32,
+  // then (once the matching is done) the child keys [pow2(F*K)] u64 | best
+  // [F] u64 | plen [F] | frontier [F]
   extern __shared__ uint64_t skey[];
   __shared__ int32_t ctx_s[kCtxLds];
   __shared__ int32_t par_s[kTreeLds], tok_s[kTreeLds], dep_s[kTreeLds];
@@ -126,9 +135,10 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   const int Lb = ctx_len[b];
   const int total = Fb * K;
   const int P2 = pow2_at_least(F * K > 0 ? F * K : 1);
-  uint64_t *best = skey + P2;
-  int32_t *suf = reinterpret_cast<int32_t *>(best + F);
-  int32_t *plen = suf + F * n_max;
+  int32_t *suf = reinterpret_cast<int32_t *>(skey);
+  uint64_t *best = skey + ngram_region_words(F, K, n_max);
+  int32_t *plen = reinterpret_cast<int32_t *>(best + F);
+  int32_t *fr_s = plen + F;
   const int32_t *ctx_g = context + (size_t)b * L;
   const int32_t *fr = frontier + (size_t)b * F;
 
@@ -153,6 +163,7 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
     const int v = fr[f];
+    fr_s[f] = v;
     bad |= v < -1 || v >= nb;
   }
 #pragma unroll
@@ -198,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
   for (int f = tid; f < Fb; f += kThreads) {
     int32_t *sf = suf + f * n_max;
     int k = 0;
-    for (int u = fr[f]; u >= 0 && k < n_max; ++k) {
+    for (int u = fr_s[f]; u >= 0 && k < n_max; ++k) {
       sf[k] = tok_of(u);
       const int p = par_of(u);
       u = (p < -1 || p >= u) ? -1 : p;
@@ -268,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
       continue;
     }
     const int f = c / K, k = c - f * K;
-    const int v = fr[f];
+    const int v = fr_s[f];
     const size_t row = ((size_t)b * L + plen[f]) * m + k;
     const float cv = v < 0 ? 0.0f : (v < nt ? cum_s[v] : tree.cum[base + v]);
     const int dv = v < 0 ? 0 : (v < nt ? dep_s[v] : tree.depth[base + v]);
@@ -324,8 +335,8 @@ hipError_t launch_ngram_expand(const tg_tree &tree, const int32_t *frontier,
                                const int32_t *fallback_pos, int m, int K, int N, int n_max,
                                int32_t *match_pos, int32_t *next_frontier, int32_t *n_next,
                                uint32_t *d_err, hipStream_t stream) {
-  const size_t lds = (size_t)pow2_at_least(F * K > 0 ? F * K : 1) * sizeof(uint64_t) +
-                    (size_t)F * sizeof(uint64_t) + (size_t)F * (n_max + 1) * sizeof(int32_t);
+  const size_t lds = ((size_t)ngram_region_words(F, K, n_max) + F) * sizeof(uint64_t) +
+                    (size_t)F * 2 * sizeof(int32_t);
   hipError_t e = hipFuncSetAttribute((const void *)ngram_expand_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

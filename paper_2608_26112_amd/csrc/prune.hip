@@ -1,7 +1,8 @@
 // Final pruning to the verification budget with ancestor closure and the
 // verification buffers (Alg. 3), and the cache update after acceptance.
 //
-// prune_kernel: one workgroup per tree, everything in LDS (n <= 4096):
+// prune_kernel: one workgroup per tree, everything in LDS (n <= 4096); the
+// parents, path scores and tokens are read in one batch up front:
 //   depths by pointer jumping over the parent links (until every chain has
 //         reached the root);
 //   keep: node keys (cum desc, depth asc, id asc) are distinct and order the
@@ -28,6 +29,7 @@ namespace {
 constexpr int kThreads = 256;
 
 constexpr int kRankCountMax = kRankPerThread * kThreads;  // rank by counting up to here
+constexpr int kPre = 4;  // node slots per thread read in the first batch
 
 __global__ __launch_bounds__(kThreads) void prune_kernel(
     tg_tree tree, int B_ver, int max_path, int32_t *__restrict__ kept,
@@ -42,6 +44,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   __shared__ int16_t newid[TG_MAX_CAP];    // original id -> verify index (0 = dropped)
   __shared__ int16_t order[TG_MAX_CAP];    // kept index -> original id
   __shared__ uint8_t flag[TG_MAX_CAP + 1];
+  __shared__ int32_t tok_s[TG_MAX_CAP];
   __shared__ int cnt[kThreads];
   __shared__ int nk_s, nl_s, viol_s, deep_s;
 
@@ -50,7 +53,20 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   const int M = B_ver + 1;
   const int W = (M + 31) / 32;
   const size_t base = (size_t)b * cap;
-  int n = tree.n_nodes[b];
+  // ---- one batch of reads: the parents, path scores and tokens of the
+  // first kPre * kThreads slots, bounded by the capacity so that they need
+  // not wait for the node count (the count masks them once it arrives)
+  const int n_ld = load_vmem(tree.n_nodes + b);
+  int pr[kPre], tk[kPre];
+  float cm[kPre];
+#pragma unroll
+  for (int j = 0; j < kPre; ++j) {
+    const int v = tid + j * kThreads;
+    pr[j] = v < cap ? tree.parent[base + v] : -1;
+    cm[j] = v < cap ? tree.cum[base + v] : 0.0f;
+    tk[j] = v < cap ? tree.token[base + v] : 0;
+  }
+  int n = uniform_int(n_ld);
   if (n < 0 || n > cap) {
     if (tid == 0) report(d_err, TG_DERR_BAD_NODE);
     n = -1;  // nothing kept, outputs padded below
@@ -59,8 +75,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
 
   // ---- parents (sanitised) and depths by pointer jumping
   bool badp = false;
-  for (int v = tid; v < nn; v += kThreads) {
-    int p = tree.parent[base + v];
+  auto put_node = [&](int v, int p, int tok) {
     if (p < -1 || p >= v) {
       badp = true;
       p = -1;
@@ -68,7 +83,15 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
     par[v] = (int16_t)p;
     anc[0][v] = (int16_t)p;
     dep[0][v] = 1;
+    tok_s[v] = tok;
+  };
+#pragma unroll
+  for (int j = 0; j < kPre; ++j) {
+    const int v = tid + j * kThreads;
+    if (v < nn) put_node(v, pr[j], tk[j]);
   }
+  for (int v = tid + kPre * kThreads; v < nn; v += kThreads)
+    put_node(v, tree.parent[base + v], tree.token[base + v]);
   if (badp) report(d_err, TG_DERR_BAD_PARENT);
   if (tid == 0) {
     viol_s = 0;
@@ -95,7 +118,12 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   // ---- keys by (cum desc, depth asc, id asc); keys are distinct, and a
   // node ranks before another exactly when its key is larger
   const int P2 = pow2_at_least(nn > 0 ? nn : 1);
-  for (int i = tid; i < P2; i += kThreads)
+#pragma unroll
+  for (int j = 0; j < kPre; ++j) {
+    const int i = tid + j * kThreads;
+    if (i < P2) key[i] = i < nn ? node_key(cm[j], depth[i], i) : 0;
+  }
+  for (int i = tid + kPre * kThreads; i < P2; i += kThreads)
     key[i] = i < nn ? node_key(tree.cum[base + i], depth[i], i) : 0;
   for (int v = tid; v < nn; v += kThreads) flag[v] = 0;
   __syncthreads();
@@ -185,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
       const int p = par[v];
       kept[ob + j] = v;
       vparent[ob + j] = p < 0 ? -1 : newid[p] - 1;
-      vtoken[ob + j] = tree.token[base + v];
+      vtoken[ob + j] = tok_s[v];
     } else {
       kept[ob + j] = -1;
       vparent[ob + j] = -1;

@@ -62,6 +62,23 @@ __device__ __forceinline__ float edge_logp(float x, float lse) {
   return lse == -__builtin_inff() ? -__builtin_inff() : __fsub_rn(x, lse);
 }
 
+// One value that every lane needs (a live count, a flag), read through the
+// vector memory path: a scalar load shares its wait counter with the
+// kernel-argument loads and with LDS accesses, so the first wait for any of
+// those would also wait for this global read.  load_vmem issues the read (the
+// value lands in a vector register); uniform_int, called once the loads that
+// need not wait for it are issued, waits for it and makes it wave-uniform.
+template <typename T>
+__device__ __forceinline__ T load_vmem(const T *p) {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return p[z];
+}
+__device__ __forceinline__ int uniform_int(int v) {
+  asm volatile("" : "+v"(v));
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
 // ------------------------------------------------------------ wave helpers
 // Wave reductions by DPP lane moves (all VALU, no LDS round trips): two quad
 // swaps, row shifts by 4 and 8 (lane 15 of each row of 16 then holds the

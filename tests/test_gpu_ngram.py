@@ -169,3 +169,22 @@ def test_match_paths(tg, n_max, L):
         t, fr, nf, mp = run_expand(tg, t, fr, nf, ctx, clen, tok, lp, fb, K, N, n_max)
         lens.append(mp)
     assert all((x >= 0).any() for x in lens)
+
+
+@pytest.mark.parametrize("K", [4, 8])
+def test_largest_frontier_and_suffix(tg, K):
+    """The largest documented call shape: F = 1024 frontier slots (the root,
+    repeated), n_max = 16 and F*K = 4096 children (filling a 4096-slot tree)
+    or 8192 (past the capacity: CAPACITY, the tree unchanged).  The suffixes
+    and the child keys share one LDS region, so every documented combination
+    launches."""
+    g = W.rng(960 + K)
+    B, L, V, m, F = 1, 96, 300, 8, 1024
+    ctx = np.stack([W.token_stream(g, L, 20)])
+    clen = np.array([L], np.int32)
+    logits = W.normal(g, (B, L, V), 2.0)
+    tok, lp, fb = _cache_close(tg, logits, ctx, clen, m)
+    t = OT.Tree.empty(B, 4096)
+    fr, nf = np.full((B, F), -1, np.int32), np.array([F], np.int32)
+    got, nx, nn, mp = run_expand(tg, t, fr, nf, ctx, clen, tok, lp, fb, K, 64, 16)
+    assert int(got.n_nodes[0]) == (F * K if F * K <= 4096 else 0)
