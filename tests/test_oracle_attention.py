@@ -239,3 +239,40 @@ def test_kv_compact_identity_and_errors():
     assert err == 16
     _, _, nl, e0 = kv_compact(k, v, L, path, np.zeros(3, np.int32))
     assert e0 == 0 and list(nl) == list(L)
+
+
+def test_self_parent_reads_as_root_child():
+    """parent[i] == i (a node its own parent) is outside [-1, i-1] too."""
+    assert list(sanitize_parent(np.array([0, 1, 1, 3]))) == [-1, -1, 1, -1]
+
+
+@pytest.mark.parametrize("fast", [False, True])
+def test_widely_spread_scores_keep_the_dominant_value(fast):
+    """Scores 2000 apart: the softmax is one-hot on the larger (closed form),
+    which only a max-shifted exponent computes without overflow."""
+    D = 4
+    q = np.zeros((1, 1, 1, D)); q[0, 0, 0, 0] = 1.0
+    k = np.zeros((1, 1, 3, D)); k[0, 0, 1, 0] = 2000.0        # prefix key 1 dominates
+    v = np.arange(12, dtype=np.float64).reshape(1, 1, 3, D)
+    f = tree_verify_attention_fast if fast else tree_verify_attention
+    out = f(q, k, v, np.array([[-1]]), np.array([2]), 1.0)
+    assert np.array_equal(out[0, 0, 0], v[0, 0, 1])
+
+
+def test_kv_compact_edges():
+    """The input is left as it was; an empty prefix is valid; a chain that
+    repeats or decreases a slot, or is longer than the path array, is not."""
+    g = W.rng(711)
+    B, Hkv, S, D = 1, 1, 8, 2
+    k = W.normal(g, (B, Hkv, S, D)); v = W.normal(g, (B, Hkv, S, D))
+    k0, v0 = k.copy(), v.copy()
+    k2, v2, nl, err = kv_compact(k, v, np.array([0]), np.array([[0, 2, 5]], np.int32),
+                                 np.array([3], np.int32))
+    assert err == 0 and int(nl[0]) == 3
+    assert np.array_equal(k, k0) and np.array_equal(v, v0)
+    assert np.array_equal(k2[0, 0, :3], k0[0, 0, [0, 2, 5]])
+    assert np.array_equal(k2[0, 0, 3:], k0[0, 0, 3:])
+    for path, n in [([1, 1, 4], 3), ([2, 1, 4], 3), ([0, 1, 2], 4)]:
+        k3, _, nl3, e3 = kv_compact(k, v, np.array([2]), np.array([path], np.int32),
+                                    np.array([n], np.int32))
+        assert e3 == 16 and int(nl3[0]) == 2 and np.array_equal(k3, k0)

@@ -103,3 +103,65 @@ def test_empty_context_is_an_error_and_leaves_the_tree():
                                             np.zeros((1, 1), np.int32), np.array([0]),
                                             z, z.astype(np.float32), np.array([-1]), 2, 2, 3)
     assert err == T.DERR_BAD_PREFIX and int(t2.n_nodes[0]) == 0 and int(nn[0]) == 0
+
+
+def _hand_cache():
+    """ctx = [7, 2, 3, 1, 2, 4]; the cache row at position j holds two
+    candidates with exactly representable scores, -(j+1)/4 and -(j+1)/2."""
+    ctx = np.array([[7, 2, 3, 1, 2, 4]], np.int32)
+    tok = np.array([[[10, 20], [11, 21], [12, 22], [13, 23], [14, 24], [3, 7]]], np.int32)
+    lp = np.array([[[-(j + 1) / 4, -(j + 1) / 2] for j in range(6)]], np.float32)
+    return ctx, np.array([6], np.int32), tok, lp
+
+
+def test_hand_expansion_values_capacity_and_bad_frontier():
+    """Two steps worked by hand (cum is the exact sum of the scores on the
+    path, depth the path length); the second fills the 6-slot tree exactly,
+    a third would overflow it (CAPACITY, unchanged), a frontier id equal to
+    the node count is BAD_NODE."""
+    ctx, clen, tok, lp = _hand_cache()
+    fb = np.array([4], np.int32)
+    t = T.Tree.empty(1, 6)
+    # step 1: the root's prefix is the context itself: latest "1 2 4" ends at 5
+    t1, pos, nxt, nn, err = NG.expand_ngram(t, np.full((1, 1), -1, np.int32), None, ctx, clen,
+                                            tok, lp, fb, 2, 2, 3)
+    assert err == 0 and list(pos[0]) == [5] and list(nxt[0]) == [0, 1] and int(nn[0]) == 2
+    assert list(t1.token[0, :2]) == [3, 7] and list(t1.parent[0, :2]) == [-1, -1]
+    assert list(t1.depth[0, :2]) == [1, 1] and list(t1.cum[0, :2]) == [-1.5, -3.0]
+    # step 2: node 0 (token 3) matches "3" at 2; node 1 (token 7) matches "7" at 0
+    t2, pos, nxt, nn, err = NG.expand_ngram(t1, nxt, nn, ctx, clen, tok, lp, fb, 2, 3, 3)
+    assert err == 0 and list(pos[0]) == [2, 0] and int(t2.n_nodes[0]) == 6
+    assert list(t2.token[0, 2:6]) == [12, 22, 10, 20]
+    assert list(t2.parent[0, 2:6]) == [0, 0, 1, 1] and list(t2.depth[0, 2:6]) == [2, 2, 2, 2]
+    assert list(t2.logp[0, 2:6]) == [-0.75, -1.5, -0.25, -0.5]
+    assert list(t2.cum[0, 2:6]) == [-2.25, -3.0, -3.25, -3.5]
+    assert list(nxt[0]) == [2, 3, 4] and int(nn[0]) == 3
+    # step 3 would append 2 more to a full tree
+    t3, _, nxt3, nn3, err = NG.expand_ngram(t2, np.array([[2]], np.int32), None, ctx, clen,
+                                            tok, lp, fb, 2, 3, 3)
+    assert err == T.DERR_CAPACITY and int(nn3[0]) == 0 and int(t3.n_nodes[0]) == 6
+    # a frontier id equal to the node count is not a node
+    t4 = T.Tree.empty(1, 16)
+    t4.parent[0, :2], t4.token[0, :2], t4.depth[0, :2], t4.n_nodes[0] = [-1, 0], [3, 3], [1, 2], 2
+    _, _, _, nn4, err = NG.expand_ngram(t4, np.array([[2]], np.int32), None, ctx, clen, tok, lp,
+                                        fb, 2, 3, 3)
+    assert err == T.DERR_BAD_NODE and int(nn4[0]) == 0
+
+
+def test_fallback_positions_at_the_edges():
+    """A node whose token the context never holds takes fallback_pos: 0 is a
+    valid position; -1 and L are not (BAD_NODE, then position L - 1).  A
+    context token equal to V is out of range for the fallback count."""
+    ctx, clen, tok, lp = _hand_cache()
+    t = T.Tree.empty(1, 16)
+    t.parent[0, 0], t.token[0, 0], t.depth[0, 0], t.n_nodes[0] = -1, 9, 1, 1
+    t.cum[0, 0] = t.logp[0, 0] = -1.0
+    fr = np.array([[0]], np.int32)
+    for f, want, want_err in [(0, 0, 0), (-1, 5, T.DERR_BAD_NODE), (6, 5, T.DERR_BAD_NODE)]:
+        t2, pos, _, _, err = NG.expand_ngram(t, fr, None, ctx, clen, tok, lp,
+                                             np.array([f], np.int32), 2, 2, 3)
+        assert int(pos[0, 0]) == want and err == want_err
+        assert list(t2.cum[0, 1:3]) == [-1.0 + lp[0, want, 0], -1.0 + lp[0, want, 1]]
+    # token 5 = V (three times) is skipped: 1 and 2 tie, 1 wins, last at 0
+    fbp, err = NG.fallback_position(np.array([[1, 5, 2, 5, 5]], np.int32), np.array([5]), 5)
+    assert err == T.DERR_BAD_NODE and int(fbp[0]) == 0

@@ -572,3 +572,25 @@ def test_prune_bruteforce_tiny_against_subset_search():
             if len(K) == B_ver:
                 break
         assert kept == K
+
+
+def test_expand_frontier_id_equal_to_the_node_count_and_exact_capacity():
+    """A frontier id equal to n_b is not a node (BAD_NODE, tree unchanged);
+    F*K children that fill the tree exactly are appended."""
+    t = T.Tree.empty(1, 6)
+    t.parent[0, :2], t.token[0, :2], t.depth[0, :2], t.n_nodes[0] = [-1, 0], [1, 2], [1, 2], 2
+    logits = np.zeros((1, 2, 5), np.float32)
+    t1, _, _, nn, err = T.expand(t, logits, np.array([[1, 2]], np.int32), None, 2, 4)
+    assert err == T.DERR_BAD_NODE and int(nn[0]) == 0 and int(t1.n_nodes[0]) == 2
+    t2, _, _, nn, err = T.expand(t, logits, np.array([[0, 1]], np.int32), None, 2, 4)
+    assert err == 0 and int(t2.n_nodes[0]) == 6 and list(t2.depth[0, 2:6]) == [2, 2, 3, 3]
+
+
+def test_greedy_argmax_needs_the_rows_through_n_nodes():
+    """Rows 0..n_nodes are read: n_nodes = R - 1 fits, n_nodes = R does not."""
+    x = np.zeros((1, 4, 3), np.float32)
+    x[0, :, 2] = 1.0
+    g, err = T.greedy_argmax(x, np.array([3]))
+    assert err == 0 and list(g[0]) == [2, 2, 2, 2]
+    g, err = T.greedy_argmax(x, np.array([4]))
+    assert err == T.DERR_BAD_NODE and list(g[0]) == [2, 2, 2, 2]
