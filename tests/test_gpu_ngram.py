@@ -188,3 +188,48 @@ def test_largest_frontier_and_suffix(tg, K):
     fr, nf = np.full((B, F), -1, np.int32), np.array([F], np.int32)
     got, nx, nn, mp = run_expand(tg, t, fr, nf, ctx, clen, tok, lp, fb, K, 64, 16)
     assert int(got.n_nodes[0]) == (F * K if F * K <= 4096 else 0)
+
+
+def _hand_cache():
+    """ctx = [7, 2, 3, 1, 2, 4]; cache row j: two candidates with exactly
+    representable scores -(j+1)/4 and -(j+1)/2 (the oracle pins work this
+    case by hand)."""
+    ctx = np.array([[7, 2, 3, 1, 2, 4]], np.int32)
+    tok = np.array([[[10, 20], [11, 21], [12, 22], [13, 23], [14, 24], [3, 7]]], np.int32)
+    lp = np.array([[[-(j + 1) / 4, -(j + 1) / 2] for j in range(6)]], np.float32)
+    return ctx, np.array([6], np.int32), tok, lp
+
+
+def test_hand_expansion_fills_the_tree_then_overflows(tg):
+    """Root step, a step that fills the 6-slot tree exactly, one that would
+    overflow it (CAPACITY), and a frontier id equal to the node count."""
+    ctx, clen, tok, lp = _hand_cache()
+    fb = np.array([4], np.int32)
+    t = OT.Tree.empty(1, 6)
+    t, fr, nf, mp = run_expand(tg, t, np.full((1, 1), -1, np.int32), None, ctx, clen, tok, lp,
+                               fb, 2, 2, 3)
+    assert list(mp[0]) == [5]
+    t, fr, nf, mp = run_expand(tg, t, fr, nf, ctx, clen, tok, lp, fb, 2, 3, 3)
+    assert list(mp[0]) == [2, 0] and int(t.n_nodes[0]) == 6
+    assert list(t.cum[0, 2:6]) == [-2.25, -3.0, -3.25, -3.5]
+    t3, _, nn3, _ = run_expand(tg, t, np.array([[2]], np.int32), None, ctx, clen, tok, lp, fb,
+                               2, 3, 3)
+    assert int(t3.n_nodes[0]) == 6 and int(nn3[0]) == 0
+    t4 = OT.Tree.empty(1, 16)
+    t4.parent[0, :2], t4.token[0, :2], t4.depth[0, :2], t4.n_nodes[0] = [-1, 0], [3, 3], [1, 2], 2
+    t5, _, nn5, _ = run_expand(tg, t4, np.array([[2]], np.int32), None, ctx, clen, tok, lp, fb,
+                               2, 3, 3)
+    assert int(t5.n_nodes[0]) == 2 and int(nn5[0]) == 0
+
+
+@pytest.mark.parametrize("fbv", [0, -1, 6])
+def test_fallback_positions_at_the_edges(tg, fbv):
+    """A node whose token the context never holds takes fallback_pos: 0 is a
+    position; -1 and L are not (BAD_NODE, then position L - 1)."""
+    ctx, clen, tok, lp = _hand_cache()
+    t = OT.Tree.empty(1, 16)
+    t.parent[0, 0], t.token[0, 0], t.depth[0, 0], t.n_nodes[0] = -1, 9, 1, 1
+    t.cum[0, 0] = t.logp[0, 0] = -1.0
+    _, _, _, mp = run_expand(tg, t, np.array([[0]], np.int32), None, ctx, clen, tok, lp,
+                             np.array([fbv], np.int32), 2, 2, 3)
+    assert int(mp[0, 0]) == (0 if fbv == 0 else 5)

@@ -267,3 +267,24 @@ def test_prune_selects_kept_set_of_monotone_trees(tg, n):
         assert err == 0
         for b in range(B):
             check_tree(got, t, b, B_ver, cap + 1)
+
+
+def test_kv_compact_edges(tg):
+    """An empty prefix is valid; a chain that repeats or decreases a slot, or
+    that is longer than the path array, leaves its sequence untouched."""
+    g = W.rng(561)
+    B, Hkv, S, D = 4, 2, 16, 64
+    k = torch.from_numpy(W.normal(g, (B, Hkv, S, D))).to(DEV)
+    v = torch.from_numpy(W.normal(g, (B, Hkv, S, D))).to(DEV)
+    k_in, v_in = k.cpu().numpy(), v.cpu().numpy()
+    L = np.array([0, 2, 2, 2], np.int32)
+    path = np.array([[0, 2, 5], [1, 1, 4], [2, 1, 4], [0, 1, 2]], np.int32)
+    n = np.array([3, 3, 3, 4], np.int32)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    nl = tg.kv_compact(k, v, torch.from_numpy(L).to(DEV), torch.from_numpy(path).to(DEV),
+                       torch.from_numpy(n).to(DEV), d_err=err)
+    torch.cuda.synchronize()
+    k2, v2, nl_o, err_o = OA.kv_compact(k_in, v_in, L, path, n)
+    assert int(err.item()) == err_o and err_o & OT.DERR_BAD_NODE
+    assert list(nl.cpu().numpy()) == list(nl_o) == [3, 2, 2, 2]
+    assert np.array_equal(k.cpu().numpy(), k2) and np.array_equal(v.cpu().numpy(), v2)

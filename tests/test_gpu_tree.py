@@ -522,3 +522,15 @@ def test_accept_nd_example(tg):
         A = run_accept(tg, np.array([c["parent"]], np.int32), np.array([c["token"]], np.int32),
                        np.array([n]), np.array([c["greedy"]], np.int32), c["max_depth"])
         assert A[0] == c["expect"]["A"]
+
+
+def test_expand_frontier_id_equal_to_the_node_count(tg):
+    """Frontier id n_b is one past the last node: BAD_NODE, tree unchanged;
+    ids n_b - 1 fill the tree to its capacity exactly."""
+    t = OT.Tree.empty(1, 6)
+    t.parent[0, :2], t.token[0, :2], t.depth[0, :2], t.n_nodes[0] = [-1, 0], [1, 2], [1, 2], 2
+    logits = W.normal(W.rng(41), (1, 2, 50), 2.0)
+    got, _, _, nn, err = run_expand(tg, t, logits, np.array([[1, 2]], np.int32), None, 2, 4)
+    assert err & OT.DERR_BAD_NODE and int(nn[0]) == 0 and int(got.n_nodes[0]) == 2
+    got, _, _, nn, err = run_expand(tg, t, logits, np.array([[0, 1]], np.int32), None, 2, 4)
+    assert err == 0 and int(got.n_nodes[0]) == 6

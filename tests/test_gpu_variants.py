@@ -136,3 +136,29 @@ def test_accept_logits_matches_oracle(tg, seed):
     assert np.array_equal(path.cpu().numpy(), path_o)
     assert np.array_equal(bonus.cpu().numpy(), bonus_o)
     assert int(err.item()) == err_o
+
+
+@pytest.mark.parametrize("extra", [0, -1])
+def test_accept_logits_row_bound(tg, extra):
+    """Rows 0..n_nodes are read: R = n_nodes + 1 fits, R = n_nodes does not
+    (BAD_NODE; the missing row reads as no match)."""
+    g = W.rng(840)
+    tree, _ = C.scored_tree(841, 1, 40, steps=2, width=3, K=2, cap=32)
+    R = int(tree.n_nodes[0]) + 1 + extra
+    logits = np.round(W.normal(g, (1, R, 300), 1.5)).astype(np.float32)
+    for v in range(int(tree.n_nodes[0])):
+        p = int(tree.parent[0, v])
+        if p + 1 < R:
+            logits[0, p + 1, int(tree.token[0, v])] = 50.0
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ts = C.tree_to_dev(tg, tree)
+    greedy, A, path, bonus = tg.accept_logits(ts.parent, ts.token, ts.n_nodes, _d(logits), 6,
+                                              d_err=err)
+    torch.cuda.synchronize()
+    g_o, A_o, path_o, bonus_o, err_o = OT.accept_logits(tree.parent, tree.token,
+                                                        tree.n_nodes, logits, 6)
+    assert int(err.item()) == err_o == (0 if extra == 0 else OT.DERR_BAD_NODE)
+    Rw = min(R, tree.cap + 1)
+    assert np.array_equal(greedy.cpu().numpy()[:, :Rw], g_o[:, :Rw])
+    assert np.array_equal(A.cpu().numpy(), A_o) and np.array_equal(bonus.cpu().numpy(), bonus_o)
+    assert np.array_equal(path.cpu().numpy(), path_o)
