@@ -37,6 +37,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per tile
+constexpr int kMaxSplits = 64;  // key-tile splits of one sequence at most
 
 __device__ __forceinline__ bool bad_prefix(int L, int N, int S_max) {
   return L < 0 || L + N > S_max;
@@ -817,57 +818,72 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     const __bf16 *__restrict__ part_o, const float *__restrict__ part_lse,
     const int32_t *__restrict__ prefix_len, __bf16 *__restrict__ out, int B,
     int N, int Hq, int S_max, int n_splits) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  constexpr int E = D / 64;  // elements per lane
-  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  // kLpr = D / 8 lanes per row, eight outputs each (one 16-byte load per
+  // split); a wave combines kWave / kLpr rows.  Lane `sub` of a row holds
+  // the log2-sum-exp of splits sub, sub + kLpr, ...  Every read is issued
+  // before the prefix check (rows past the end read the last row), and the
+  // splits are added in split order.
+  constexpr int kLpr = D / 8, kRpw = kWave / kLpr, kSlots = kMaxSplits / kLpr;
+  typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+  const int lane = threadIdx.x & (kWave - 1), sub = lane & (kLpr - 1);
+  const int base = lane & ~(kLpr - 1);
   const int rows = B * N * Hq;
-  if (gw >= rows) return;
-  const int b = gw / (N * Hq);
-  __bf16 *op = out + (size_t)gw * D;
-  if (bad_prefix(prefix_len[b], N, S_max)) {
-    for (int d = lane; d < D; d += 64) op[d] = (__bf16)0.0f;
-    return;
-  }
-  const float ls = lane < n_splits ? part_lse[(size_t)lane * rows + gw] : -__builtin_inff();
-  auto lse_of = [&](int sp) {  // split sp's log-sum-exp, wave-uniform
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ls), sp & 63));
-  };
-  float M = -__builtin_inff();
-  for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, lse_of(sp));
-  float acc[E] = {};
-  float den = 0.0f;
-  const __bf16 *po = part_o + (size_t)gw * D + E * lane;
+  const int waves = (int)(blockDim.x / kWave);
+  const int gw = ((int)blockIdx.x * waves + (int)(threadIdx.x / kWave)) * kRpw + lane / kLpr;
+  const int row = gw < rows ? gw : rows - 1;
   const size_t sstride = (size_t)rows * D;
-  // eight splits per round, loads first (indices clamped, weights 0 past the end)
-  for (int s0 = 0; s0 < n_splits; s0 += 8) {
-    float v[8][E];
+  const __bf16 *po = part_o + (size_t)row * D + 8 * sub;
+  const int L = prefix_len[row / (N * Hq)];
+  const float ninf = -__builtin_inff();
+  float ls[kSlots];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const __bf16 *pi = po + (size_t)min(s0 + i, n_splits - 1) * sstride;
-      if constexpr (E == 2) {
-        const bf16x2 x = *reinterpret_cast<const bf16x2 *>(pi);
-        v[i][0] = (float)x[0];
-        v[i][1] = (float)x[1];
-      } else {
-        v[i][0] = (float)pi[0];
+  for (int k = 0; k < kSlots; ++k) {
+    const int sp = k * kLpr + sub;
+    ls[k] = sp < n_splits ? part_lse[(size_t)sp * rows + row] : ninf;
+  }
+  bf16x8 v0[8];  // the first eight splits' values (clamped indices)
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    v0[i] = *reinterpret_cast<const bf16x8 *>(po + (size_t)min(i, n_splits - 1) * sstride);
+  float M = ls[0];
+#pragma unroll
+  for (int k = 1; k < kSlots; ++k) M = fmaxf(M, ls[k]);
+#pragma unroll
+  for (int m = 1; m < kLpr; m <<= 1) M = fmaxf(M, __shfl_xor(M, m, kWave));
+  float wl[kSlots];
+#pragma unroll
+  for (int k = 0; k < kSlots; ++k) wl[k] = ls[k] != ninf ? exp2f(ls[k] - M) : 0.0f;
+  float acc[8] = {};
+  float den = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kSlots; ++k) {
+#pragma unroll
+    for (int h = 0; h < kLpr / 8; ++h) {
+      const int s0 = k * kLpr + h * 8;
+      if (s0 >= n_splits) break;
+      bf16x8 v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        v[i] = s0 == 0 ? v0[i]
+                       : *reinterpret_cast<const bf16x8 *>(
+                             po + (size_t)min(s0 + i, n_splits - 1) * sstride);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float w = s0 + i < n_splits ? __shfl(wl[k], base + h * 8 + i, kWave) : 0.0f;
+        den += w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, (float)v[i][e], acc[e]);
       }
     }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float lsi = lse_of(s0 + i);
-      const float w = (s0 + i < n_splits && lsi != -__builtin_inff()) ? exp2f(lsi - M) : 0.0f;
-      den += w;
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(w, v[i][e], acc[e]);
-    }
   }
+  if (gw >= rows) return;
+  // a sequence with a bad prefix length has no partials (its output is 0)
+  const bool bad = bad_prefix(L, N, S_max);
   const float inv = den > 0.0f ? 1.0f / den : 0.0f;
-  if constexpr (E == 2) {
-    *reinterpret_cast<bf16x2 *>(op + 2 * lane) = bf16x2{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv)};
-  } else {
-    op[lane] = (__bf16)(acc[0] * inv);
-  }
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = bad ? (__bf16)0.0f : (__bf16)(acc[e] * inv);
+  *reinterpret_cast<bf16x8 *>(out + (size_t)gw * D + 8 * sub) = o;
 }
 
 // ------------------------------------------------------------------- fp32
@@ -1000,7 +1016,7 @@ static AttnPlan attn_plan(const AttnShape &s) {
   if (base < want_wgs) {
     const long long min_per = pp ? 16 : 2;
     const long long per = std::max(min_per, (n_vt * base + want_wgs - 1) / want_wgs);
-    sp = (int)std::min<long long>(64, (n_vt + per - 1) / per);
+    sp = (int)std::min<long long>(kMaxSplits, (n_vt + per - 1) / per);
   }
   return AttnPlan{pp, tiles, std::max(sp, 1)};
 }
@@ -1073,12 +1089,19 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   if (e != hipSuccess) return e;
   e = hipGetLastError();
   if (e != hipSuccess || sp <= 1) return e;
-  const unsigned cgrid = (unsigned)((rows + 3) / 4);
+  // four waves per workgroup when that still makes 1024 workgroups or more,
+  // else one: a small combine spread over every compute unit leaves none idle
+  // for the next launch (measured: one-wave groups took the llama8b-shaped
+  // call's following attention kernel back from 15.9 to 14.3 us)
+  const int rows_per_wave = kWave / (s.D / 8);
+  const long long waves_needed = ((long long)rows + rows_per_wave - 1) / rows_per_wave;
+  const int wpb = waves_needed >= 4 * 1024 ? kThreads / kWave : 1;
+  const unsigned cgrid = (unsigned)((waves_needed + wpb - 1) / wpb);
   if (s.D == 64)
-    launch("attn_combine", attn_combine_kernel<64>, dim3(cgrid), dim3(kThreads), 0, stream,
+    launch("attn_combine", attn_combine_kernel<64>, dim3(cgrid), dim3(wpb * kWave), 0, stream,
                        part_o, part_lse, prefix_len, ob, s.B, s.N, s.Hq, s.S_max, sp);
   else
-    launch("attn_combine", attn_combine_kernel<128>, dim3(cgrid), dim3(kThreads), 0, stream,
+    launch("attn_combine", attn_combine_kernel<128>, dim3(cgrid), dim3(wpb * kWave), 0, stream,
                        part_o, part_lse, prefix_len, ob, s.B, s.N, s.Hq, s.S_max, sp);
   return hipGetLastError();
 }
