@@ -228,3 +228,26 @@ def test_repeatable_bitwise(tg):
     a, *_ = _run(tg, q, k, v, parent, [L], D ** -0.5, torch.bfloat16)
     b, *_ = _run(tg, q, k, v, parent, [L], D ** -0.5, torch.bfloat16)
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_many_splits_and_bad_prefix_in_split_mode(tg, D):
+    """One KV head and a 4000-key prefix: the key tiles are dealt to more
+    splits than one combine lane holds (more than D / 8), and with the
+    second sequence's prefix length invalid (L + N > S_max) its rows are 0
+    while the first sequence's are unchanged."""
+    g = W.rng(40 + D)
+    B, N, Hq, Hkv, L = 2, 16, 4, 1, 4000
+    rows = B * N * Hq
+    ws = tg.verify_attention_workspace(B, N, Hq, Hkv, D, L + N, tg.BF16)
+    splits = (ws - 256) // (rows * (2 * D + 4))
+    assert splits > D // 8
+    parent = np.stack([W.uniform_parents(g, N) for _ in range(B)])
+    q, k, v = _gen(41 + D, B, N, Hq, Hkv, D, L)
+    got, qq, kk, vv = _run(tg, q, k, v, parent, [L, L], D ** -0.5, torch.bfloat16)
+    want = tree_verify_attention_fast(qq, kk, vv, parent, np.array([L, L]), D ** -0.5)
+    C.attn_close_bf16(got, want)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got2, *_ = _run(tg, q, k, v, parent, [L, L + 1], D ** -0.5, torch.bfloat16, d_err=err)
+    assert int(err.item()) & tg.DERR_BAD_PREFIX
+    assert np.all(got2[1] == 0.0) and np.array_equal(got2[0], got[0])
