@@ -45,7 +45,7 @@ same steps records every kernel's device time with the library's trace events
 kernel's roofline comes from those.  The CPU baseline times the oracle (tests' CPU
 reference) on the same inputs.
 
-Prints ONE JSON line.  N > 1 GPUs is not supported by this build.
+Prints ONE JSON line.  One GPU only: N > 1 exits with a message.
 """
 from __future__ import annotations
 
@@ -549,8 +549,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; multi-GPU sharding of the "
-              "tree-verify path is described in DESIGN.md but not implemented", file=sys.stderr)
+        print("bench.py: runs on one GPU only; sharding the tree-verify path over "
+              "(batch, KV head) across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
     import torch
 

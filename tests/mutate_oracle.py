@@ -60,7 +60,10 @@ if __name__ == '__main__':
     for i in range(8):
         d = f'/tmp/mut_{i}'
         shutil.rmtree(d, ignore_errors=True)
-        shutil.copytree(SRC, d, ignore=shutil.ignore_patterns('.git', 'gpurun_out', '_work', '__pycache__'))
+        os.makedirs(d)
+        for sub in ('oracle', 'tests', 'workloads', 'paper_2608_26112_amd'):
+            shutil.copytree(os.path.join(SRC, sub), os.path.join(d, sub),
+                            ignore=shutil.ignore_patterns('__pycache__', '*.so'))
     jobs = []
     for fname in sorted(os.listdir(SRC + '/oracle')):
         if not fname.endswith('.py') or fname == '__init__.py': continue
