@@ -135,9 +135,10 @@ __global__ __launch_bounds__(kThreads) void rescore_pool_kernel(
     if (tid == 0 && pool.root_in(tree, b)) flag[0] = 1;
     bool dummy = false;
     for (int v = tid; v < nb; v += kThreads) {
+      const int p = tree.parent[base + v];  // read with the pool flag, not after it
       if (pool.in(tree, base, v)) {
         flag[v + 1] = 1;
-        flag[sane_parent(tree.parent[base + v], v, dummy) + 1] = 1;
+        flag[sane_parent(p, v, dummy) + 1] = 1;
       }
     }
   }
