@@ -251,3 +251,29 @@ def test_many_splits_and_bad_prefix_in_split_mode(tg, D):
     got2, *_ = _run(tg, q, k, v, parent, [L, L + 1], D ** -0.5, torch.bfloat16, d_err=err)
     assert int(err.item()) & tg.DERR_BAD_PREFIX
     assert np.all(got2[1] == 0.0) and np.array_equal(got2[0], got[0])
+
+
+def test_wide_combine_d64_sampled_rows(tg):
+    """D = 64 with 32768 (node, head) rows in split mode, so the combine runs
+    four-wave workgroups (eight rows per wave); 64 sampled rows plus the first
+    and last against the oracle."""
+    g = W.rng(47)
+    B, N, L, D, Hq, Hkv = 2, 256, 2048, 64, 64, 1
+    rows_total = B * N * Hq
+    ws = tg.verify_attention_workspace(B, N, Hq, Hkv, D, L + N, tg.BF16)
+    assert ws > 0 and rows_total // (64 // (D // 8)) >= 4 * 1024   # split mode, wide grid
+    parent = np.stack([W.uniform_parents(g, N) for _ in range(B)])
+    q, k, v = _gen(48, B, N, Hq, Hkv, D, L)
+    dq = torch.from_numpy(q).to(DEV).to(torch.bfloat16)
+    dk = torch.from_numpy(k).to(DEV).to(torch.bfloat16)
+    dv = torch.from_numpy(v).to(DEV).to(torch.bfloat16)
+    out = tg.verify_attention(dq, dk, dv, torch.from_numpy(parent).to(DEV),
+                              torch.full((B,), L, dtype=torch.int32, device=DEV), D ** -0.5)
+    torch.cuda.synchronize()
+    rows = [(int(g.integers(0, B)), int(g.integers(0, N)), int(g.integers(0, Hq)))
+            for _ in range(64)]
+    rows += [(0, 0, 0), (B - 1, N - 1, Hq - 1)]
+    got = np.stack([out[b, i, h].float().cpu().numpy() for b, i, h in rows])
+    qh, kh, vh = dq.float().cpu().numpy(), dk.float().cpu().numpy(), dv.float().cpu().numpy()
+    want = tree_verify_attention(qh, kh, vh, parent, np.array([L, L]), D ** -0.5, rows=rows)
+    C.attn_close_bf16(got, want)
