@@ -702,16 +702,13 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     const bool need = m_set ? mx > kSlack : mx != -__builtin_inff();
     if (__any(need)) {
-      // set or move this row's reference (rows that need neither keep theirs)
+      // set or move the reference of the rows that need it; every other row
+      // keeps its own, so a row's arithmetic never depends on its neighbours
       float shift = 0.0f, alpha = 1.0f;
-      if (!m_set) {
-        if (mx != -__builtin_inff()) {
-          shift = mx;  // o and l are still 0: no rescale
-          m_set = true;
-        }
-      } else if (mx > 0.0f) {
+      if (need) {
         shift = mx;
-        alpha = __builtin_amdgcn_exp2f(-mx);
+        if (m_set) alpha = __builtin_amdgcn_exp2f(-mx);  // else o and l are still 0
+        m_set = true;
       }
       l *= alpha;
 #pragma unroll

@@ -84,6 +84,25 @@ def test_random_small(tg, N, kind, dtype):
         C.attn_close_f32(got, want)
 
 
+@pytest.mark.parametrize("kind", ["random", "chain"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_largest_tree_1024_nodes(tg, kind, dtype):
+    """N = 1024, the largest verify tree: the fp32 kernel's per-wave root
+    path (a 1024-deep chain) and the bf16 kernel's 32-word bitsets."""
+    g = W.rng(1024 + (kind == "chain"))
+    B, N, Hq, Hkv, D = 1, 1024, 2, 1, 64
+    plen = np.array([50])
+    parent = _parents(kind, g, N)[None]
+    q, k, v = _gen(1025, B, N, Hq, Hkv, D, 50, extra=3)
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    got, q, k, v = _run(tg, q, k, v, parent, plen, D ** -0.5, dt)
+    want = tree_verify_attention_fast(q, k, v, parent, plen, D ** -0.5)
+    if dtype == "bf16":
+        C.attn_close_bf16(got, want)
+    else:
+        C.attn_close_f32(got, want)
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_empty_prefix_root_level_node_is_exactly_v_self(tg, dtype):
     g = W.rng(5)

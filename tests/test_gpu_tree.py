@@ -137,6 +137,8 @@ CASES = [
     (4, 32, 30000, 10, 60, "many rows"),
     (1, 64, 128256, 10, 60, "one full-vocab tree"),
     (2, 40, 3000, 10, 10, "N = 10 of 400 children (selection)"),
+    (1, 205, 700, 5, 60, "F*K = 1025: sorted selection"),
+    (2, 256, 600, 8, 300, "F*K = 2048: sorted selection"),
 ]
 
 
@@ -150,6 +152,35 @@ def test_expand_shapes(tg, case):
     nf = np.array([F] + [int(g.integers(0, F + 1)) for _ in range(B - 1)], np.int32)
     logits = W.normal(g, (B, F, V), 3.0)
     run_expand(tg, base, logits, fr, nf, K, N)
+
+
+@pytest.mark.parametrize("F,K", [(64, 64), (512, 8)])
+def test_expand_fills_capacity_with_4096_children(tg, F, K):
+    """F*K = 4096 children under the root of an empty tree of capacity 4096
+    (the largest tree): the sorted selection path, appending exactly to the
+    capacity, with duplicated frontier entries (every row is the root)."""
+    g = W.rng(F * 100 + K)
+    base = OT.Tree.empty(1, 4096)
+    fr = np.full((1, F), -1, np.int32)
+    logits = W.normal(g, (1, F, 300), 3.0)
+    got, _, _, nn, err = run_expand(tg, base, logits, fr, None, K, 500)
+    assert err == 0 and int(got.n_nodes[0]) == 4096 and int(nn[0]) == 500
+
+
+def test_expand_8192_children_overflow(tg):
+    """F*K = 8192 (the documented maximum) can never fit a tree of capacity
+    4096: the call reports CAPACITY, appends nothing and returns n_next = 0,
+    next to a tree whose 1025 children do fit."""
+    g = W.rng(8192)
+    base = OT.Tree.empty(2, 4096)
+    F, K = 128, 64
+    fr = np.full((2, F), -1, np.int32)
+    nf = np.array([F, 17], np.int32)             # 17 * 64 = 1088 children fit
+    logits = W.normal(g, (2, F, 200), 3.0)
+    got, _, _, nn, err = run_expand(tg, base, logits, fr, nf, K, 64)
+    assert err & OT.DERR_CAPACITY
+    assert int(got.n_nodes[0]) == 0 and int(nn[0]) == 0
+    assert int(got.n_nodes[1]) == 17 * 64 and int(nn[1]) == 64
 
 
 def test_expand_ties_and_special_values(tg):
