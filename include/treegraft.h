@@ -39,7 +39,9 @@
  *   - Rankings: a logits row's top-k tokens are ordered by (logit desc,
  *     token asc); node rankings use (cum desc, depth asc, id asc), the key
  *     Alg. 3 fixes for pruning.  -0.0 ranks equal to +0.0.
- *   - The library holds no mutable global state and is reentrant.
+ *   - Apart from the optional benchmark trace (tg_trace_*, process-global
+ *     and not thread-safe, off by default), the library holds no mutable
+ *     global state: with tracing off every call is reentrant.
  */
 #ifndef TREEGRAFT_H
 #define TREEGRAFT_H

@@ -172,16 +172,76 @@ def _dev(t, name, dtype=None):
     return t
 
 
-def _stream(stream):
-    s = torch.cuda.current_stream() if stream is None else stream
-    return ctypes.c_void_p(s.cuda_stream)
+def _stream_obj(stream, device):
+    return torch.cuda.current_stream(device) if stream is None else stream
 
 
-def _workspace(nbytes, device, workspace):
+def _stream(stream, device=None):
+    return ctypes.c_void_p(_stream_obj(stream, device).cuda_stream)
+
+
+def _out(t, name, shape, dtype, device):
+    """A caller-supplied output, checked (GPU, contiguous, dtype, shape, on
+    `device`), or a new empty tensor when `t` is None."""
+    shape = tuple(int(x) for x in shape)
+    if t is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    _dev(t, name, dtype)
+    if tuple(t.shape) != shape:
+        raise ValueError(f"{name} must have shape {shape}, got {tuple(t.shape)}")
+    if t.device != torch.device(device):
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    return t
+
+
+def _in(t, name, shape, dtype, device=None):
+    """A required input, checked like _out (shape entries None = any)."""
+    _dev(t, name, dtype)
+    if len(t.shape) != len(shape) or any(s is not None and int(a) != int(s)
+                                         for a, s in zip(t.shape, shape)):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if device is not None and t.device != torch.device(device):
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    return t
+
+
+def _err(d_err, device):
+    """The optional device error word: one int32 (the C ABI's uint32) on `device`."""
+    if d_err is None:
+        return None
+    _dev(d_err, "d_err", torch.int32)
+    if d_err.numel() < 1 or d_err.device != torch.device(device):
+        raise ValueError(f"d_err must hold at least one int32 on {device}")
+    return d_err
+
+
+def _tree_batch(tree, B):
+    if tree.B != B:
+        raise ValueError(f"the tree holds {tree.B} trees but the call has batch {B}")
+
+
+# Workspaces the binding allocates when the caller passes none: one per
+# (device, stream), grown to the largest size asked for and kept for later
+# calls (calls on one stream are ordered, so they can share it; the library
+# accepts any contents).  release_workspaces() drops them.
+_WS = {}
+
+
+def release_workspaces():
+    """Free the workspaces the binding allocated for calls without one."""
+    _WS.clear()
+
+
+def _workspace(nbytes, device, workspace, stream=None):
     if nbytes == 0:
         return None, 0
-    if workspace is None:   # zero-filled: the counter block must start at zero
-        workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+    if workspace is None:
+        dev = torch.device(device)
+        key = (dev.index, _stream_obj(stream, dev).cuda_stream)
+        workspace = _WS.get(key)
+        if workspace is None or workspace.numel() < nbytes:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            _WS[key] = workspace
     _dev(workspace, "workspace")
     return workspace, workspace.numel() * workspace.element_size()
 
@@ -246,19 +306,20 @@ def verify_attention(q, k_cache, v_cache, parent, prefix_len, sm_scale, out=None
     Hkv, S_max = k_cache.shape[1], k_cache.shape[2]
     if tuple(k_cache.shape) != (B, Hkv, S_max, D) or v_cache.shape != k_cache.shape:
         raise ValueError("k_cache/v_cache must be [B, Hkv, S_max, D]")
-    if tuple(parent.shape) != (B, N) or tuple(prefix_len.shape) != (B,):
-        raise ValueError("parent must be [B, N] and prefix_len [B]")
-    if out is None:
-        out = torch.empty_like(q)
-    _dev(out, "out", q.dtype)
+    dev = q.device
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        if t.device != dev:
+            raise ValueError(f"{n} must be on {dev}, got {t.device}")
+    _in(parent, "parent", (B, N), torch.int32, dev)
+    _in(prefix_len, "prefix_len", (B,), torch.int32, dev)
+    out = _out(out, "out", q.shape, q.dtype, dev)
+    d_err = _err(d_err, dev)
     nbytes = lib.tg_verify_attention_workspace(B, N, Hq, Hkv, D, S_max, dt)
-    ws, wsb = _workspace(nbytes, q.device, workspace)
-    if d_err is not None:
-        _dev(d_err, "d_err", torch.int32)
+    ws, wsb = _workspace(nbytes, dev, workspace, stream)
     st = lib.tg_tree_verify_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(parent),
                                       _ptr(prefix_len), _ptr(out), B, N, Hq, Hkv, D, S_max,
                                       float(sm_scale), dt, _ptr(ws), wsb, _ptr(d_err),
-                                      _stream(stream))
+                                      _stream(stream, dev))
     _check("tg_tree_verify_attention", st)
     return out
 
@@ -274,23 +335,24 @@ def expand_topk(tree: TreeState, logits, frontier, n_frontier, K, N, row_lse=Non
     n_frontier [B] int32 or None.  Returns (row_lse, next_frontier, n_next)."""
     lib = load()
     _dev(logits, "logits", torch.float32)
-    _dev(frontier, "frontier", torch.int32)
+    if logits.dim() != 3:
+        raise ValueError("logits must be [B, F, V]")
     B, F, V = logits.shape
-    if tuple(frontier.shape) != (B, F):
-        raise ValueError("frontier must be [B, F]")
-    if n_frontier is not None:
-        _dev(n_frontier, "n_frontier", torch.int32)
     dev = logits.device
-    row_lse = torch.empty((B, F), dtype=torch.float32, device=dev) if row_lse is None else row_lse
-    next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
-                     if next_frontier is None else next_frontier)
-    n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
-    ws, wsb = _workspace(lib.tg_expand_topk_workspace(B, F, V, K, N), dev, workspace)
+    _tree_batch(tree, B)
+    _in(frontier, "frontier", (B, F), torch.int32, dev)
+    if n_frontier is not None:
+        _in(n_frontier, "n_frontier", (B,), torch.int32, dev)
+    row_lse = _out(row_lse, "row_lse", (B, F), torch.float32, dev)
+    next_frontier = _out(next_frontier, "next_frontier", (B, N), torch.int32, dev)
+    n_next = _out(n_next, "n_next", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
+    ws, wsb = _workspace(lib.tg_expand_topk_workspace(B, F, V, K, N), dev, workspace, stream)
     ts = tree.struct()
     st = lib.tg_tree_expand_topk(ctypes.byref(ts), _ptr(logits), _ptr(frontier),
                                  _ptr(n_frontier), B, F, V, K, N, _ptr(row_lse),
                                  _ptr(next_frontier), _ptr(n_next), _ptr(ws), wsb,
-                                 _ptr(d_err), _stream(stream))
+                                 _ptr(d_err), _stream(stream, dev))
     _check("tg_tree_expand_topk", st)
     return row_lse, next_frontier, n_next
 
@@ -306,22 +368,20 @@ def ngram_cache(logits, context, ctx_len, m, cand_tok=None, cand_logp=None,
     [B,L,m], cand_logp [B,L,m], fallback_pos [B])."""
     lib = load()
     _dev(logits, "logits", torch.float32)
-    _dev(context, "context", torch.int32)
-    _dev(ctx_len, "ctx_len", torch.int32)
+    if logits.dim() != 3:
+        raise ValueError("logits must be [B, L, V]")
     B, L, V = logits.shape
-    if tuple(context.shape) != (B, L):
-        raise ValueError("context must be [B, L]")
     dev = logits.device
-    cand_tok = (torch.empty((B, L, m), dtype=torch.int32, device=dev)
-                if cand_tok is None else cand_tok)
-    cand_logp = (torch.empty((B, L, m), dtype=torch.float32, device=dev)
-                 if cand_logp is None else cand_logp)
-    fallback_pos = (torch.empty((B,), dtype=torch.int32, device=dev)
-                    if fallback_pos is None else fallback_pos)
-    ws, wsb = _workspace(lib.tg_ngram_cache_workspace(B, L, V, m), dev, workspace)
+    _in(context, "context", (B, L), torch.int32, dev)
+    _in(ctx_len, "ctx_len", (B,), torch.int32, dev)
+    cand_tok = _out(cand_tok, "cand_tok", (B, L, m), torch.int32, dev)
+    cand_logp = _out(cand_logp, "cand_logp", (B, L, m), torch.float32, dev)
+    fallback_pos = _out(fallback_pos, "fallback_pos", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
+    ws, wsb = _workspace(lib.tg_ngram_cache_workspace(B, L, V, m), dev, workspace, stream)
     st = lib.tg_ngram_cache(_ptr(logits), _ptr(context), _ptr(ctx_len), B, L, V, m,
                             _ptr(cand_tok), _ptr(cand_logp), _ptr(fallback_pos), _ptr(ws), wsb,
-                            _ptr(d_err), _stream(stream))
+                            _ptr(d_err), _stream(stream, dev))
     _check("tg_ngram_cache", st)
     return cand_tok, cand_logp, fallback_pos
 
@@ -332,29 +392,31 @@ def expand_ngram(tree: TreeState, frontier, n_frontier, context, ctx_len, cand_t
     """One small-drafter step with the n-gram drafter (see
     tg_tree_expand_ngram).  Returns (next_frontier, n_next, match_pos)."""
     lib = load()
-    for t, n in ((frontier, "frontier"), (context, "context"), (ctx_len, "ctx_len"),
-                 (cand_tok, "cand_tok"), (fallback_pos, "fallback_pos")):
-        _dev(t, n, torch.int32)
-    _dev(cand_logp, "cand_logp", torch.float32)
-    if n_frontier is not None:
-        _dev(n_frontier, "n_frontier", torch.int32)
+    _dev(frontier, "frontier", torch.int32)
+    if frontier.dim() != 2:
+        raise ValueError("frontier must be [B, F]")
     B, F = frontier.shape
-    L = context.shape[1]
-    m = cand_tok.shape[2]
-    if tuple(cand_tok.shape) != (B, L, m) or tuple(cand_logp.shape) != (B, L, m):
-        raise ValueError("cand_tok / cand_logp must be [B, L, m]")
     dev = frontier.device
-    match_pos = (torch.empty((B, F), dtype=torch.int32, device=dev)
-                 if match_pos is None else match_pos)
-    next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
-                     if next_frontier is None else next_frontier)
-    n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
+    _tree_batch(tree, B)
+    _in(context, "context", (B, None), torch.int32, dev)
+    L = context.shape[1]
+    _in(ctx_len, "ctx_len", (B,), torch.int32, dev)
+    _in(cand_tok, "cand_tok", (B, L, None), torch.int32, dev)
+    m = cand_tok.shape[2]
+    _in(cand_logp, "cand_logp", (B, L, m), torch.float32, dev)
+    _in(fallback_pos, "fallback_pos", (B,), torch.int32, dev)
+    if n_frontier is not None:
+        _in(n_frontier, "n_frontier", (B,), torch.int32, dev)
+    match_pos = _out(match_pos, "match_pos", (B, F), torch.int32, dev)
+    next_frontier = _out(next_frontier, "next_frontier", (B, N), torch.int32, dev)
+    n_next = _out(n_next, "n_next", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
     ts = tree.struct()
     st = lib.tg_tree_expand_ngram(ctypes.byref(ts), _ptr(frontier), _ptr(n_frontier),
                                   _ptr(context), _ptr(ctx_len), _ptr(cand_tok), _ptr(cand_logp),
                                   _ptr(fallback_pos), B, F, L, m, K, N, n_max, _ptr(match_pos),
                                   _ptr(next_frontier), _ptr(n_next), _ptr(d_err),
-                                  _stream(stream))
+                                  _stream(stream, dev))
     _check("tg_tree_expand_ngram", st)
     return next_frontier, n_next, match_pos
 
@@ -373,28 +435,31 @@ def rescore_graft(tree: TreeState, strong_logits, W, M, flags=0, row_lse=None,
     when N > 0."""
     lib = load()
     _dev(strong_logits, "strong_logits", torch.float32)
-    if new_from is not None:
-        _dev(new_from, "new_from", torch.int32)
+    if strong_logits.dim() != 3:
+        raise ValueError("strong_logits must be [B, R, V]")
     B, R, V = strong_logits.shape
     dev = strong_logits.device
-    row_lse = (torch.full((B, R), float("nan"), dtype=torch.float32, device=dev)
-               if row_lse is None else row_lse)
-    graft_frontier = (torch.empty((B, W), dtype=torch.int32, device=dev)
-                      if graft_frontier is None else graft_frontier)
-    n_graft = torch.empty((B,), dtype=torch.int32, device=dev) if n_graft is None else n_graft
+    _tree_batch(tree, B)
+    if new_from is not None:
+        _in(new_from, "new_from", (B,), torch.int32, dev)
+    if row_lse is None:
+        row_lse = torch.full((B, R), float("nan"), dtype=torch.float32, device=dev)
+    row_lse = _out(row_lse, "row_lse", (B, R), torch.float32, dev)
+    graft_frontier = _out(graft_frontier, "graft_frontier", (B, W), torch.int32, dev)
+    n_graft = _out(n_graft, "n_graft", (B,), torch.int32, dev)
     if N > 0:
-        next_frontier = (torch.empty((B, N), dtype=torch.int32, device=dev)
-                         if next_frontier is None else next_frontier)
-        n_next = torch.empty((B,), dtype=torch.int32, device=dev) if n_next is None else n_next
+        next_frontier = _out(next_frontier, "next_frontier", (B, N), torch.int32, dev)
+        n_next = _out(n_next, "n_next", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
     ws, wsb = _workspace(lib.tg_rescore_graft_workspace(B, R, V, W, M, tree.cap), dev,
-                         workspace)
+                         workspace, stream)
     ts = tree.struct()
     st = lib.tg_tree_rescore_graft(ctypes.byref(ts), _ptr(strong_logits), B, R, V, W, M,
                                    int(flags), _ptr(new_from), _ptr(row_lse),
                                    _ptr(graft_frontier),
                                    _ptr(n_graft), _ptr(next_frontier if N > 0 else None),
                                    _ptr(n_next if N > 0 else None), int(N), _ptr(ws), wsb,
-                                   _ptr(d_err), _stream(stream))
+                                   _ptr(d_err), _stream(stream, dev))
     _check("tg_tree_rescore_graft", st)
     if N > 0:
         return row_lse, graft_frontier, n_graft, next_frontier, n_next
@@ -409,17 +474,20 @@ def accept(parent, token, n_nodes, greedy, max_depth, accept_len=None, accept_pa
     for t, n in ((parent, "parent"), (token, "token"), (n_nodes, "n_nodes"),
                  (greedy, "greedy")):
         _dev(t, n, torch.int32)
+    if parent.dim() != 2:
+        raise ValueError("parent must be [B, cap]")
     B, cap = parent.shape
-    if tuple(greedy.shape) != (B, cap + 1):
-        raise ValueError("greedy must be [B, cap + 1]")
     dev = parent.device
-    accept_len = torch.empty((B,), dtype=torch.int32, device=dev) if accept_len is None else accept_len
-    accept_path = (torch.empty((B, max_depth), dtype=torch.int32, device=dev)
-                   if accept_path is None else accept_path)
-    bonus = torch.empty((B,), dtype=torch.int32, device=dev) if bonus is None else bonus
+    _in(token, "token", (B, cap), torch.int32, dev)
+    _in(n_nodes, "n_nodes", (B,), torch.int32, dev)
+    _in(greedy, "greedy", (B, cap + 1), torch.int32, dev)
+    accept_len = _out(accept_len, "accept_len", (B,), torch.int32, dev)
+    accept_path = _out(accept_path, "accept_path", (B, max_depth), torch.int32, dev)
+    bonus = _out(bonus, "bonus", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
     st = lib.tg_tree_accept(_ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(greedy), B, cap,
                             max_depth, _ptr(accept_len), _ptr(accept_path), _ptr(bonus),
-                            _ptr(d_err), _stream(stream))
+                            _ptr(d_err), _stream(stream, dev))
     _check("tg_tree_accept", st)
     return accept_len, accept_path, bonus
 
@@ -433,19 +501,23 @@ def accept_logits(parent, token, n_nodes, logits, max_depth, greedy=None, accept
     for t, n in ((parent, "parent"), (token, "token"), (n_nodes, "n_nodes")):
         _dev(t, n, torch.int32)
     _dev(logits, "logits", torch.float32)
+    if parent.dim() != 2:
+        raise ValueError("parent must be [B, cap]")
     B, cap = parent.shape
-    R, V = logits.shape[1], logits.shape[2]
-    if logits.shape[0] != B:
-        raise ValueError("logits must be [B, R, V]")
     dev = parent.device
-    greedy = torch.empty((B, cap + 1), dtype=torch.int32, device=dev) if greedy is None else greedy
-    accept_len = torch.empty((B,), dtype=torch.int32, device=dev) if accept_len is None else accept_len
-    accept_path = (torch.empty((B, max_depth), dtype=torch.int32, device=dev)
-                   if accept_path is None else accept_path)
-    bonus = torch.empty((B,), dtype=torch.int32, device=dev) if bonus is None else bonus
+    _in(token, "token", (B, cap), torch.int32, dev)
+    _in(n_nodes, "n_nodes", (B,), torch.int32, dev)
+    _in(logits, "logits", (B, None, None), torch.float32, dev)
+    R, V = logits.shape[1], logits.shape[2]
+    greedy = _out(greedy, "greedy", (B, cap + 1), torch.int32, dev)
+    accept_len = _out(accept_len, "accept_len", (B,), torch.int32, dev)
+    accept_path = _out(accept_path, "accept_path", (B, max_depth), torch.int32, dev)
+    bonus = _out(bonus, "bonus", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
     st = lib.tg_tree_accept_logits(_ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(logits), B,
                                    cap, R, V, max_depth, _ptr(greedy), _ptr(accept_len),
-                                   _ptr(accept_path), _ptr(bonus), _ptr(d_err), _stream(stream))
+                                   _ptr(accept_path), _ptr(bonus), _ptr(d_err),
+                                   _stream(stream, dev))
     _check("tg_tree_accept_logits", st)
     return greedy, accept_len, accept_path, bonus
 
@@ -461,22 +533,18 @@ def global_prune(tree: TreeState, B_ver: int, max_path: int | None = None, d_err
     B, dev = tree.B, tree.parent.device
     M = B_ver + 1
     max_path = M if max_path is None else int(max_path)
-    i32 = dict(dtype=torch.int32, device=dev)
-    if out is None:
-        out = dict(kept=torch.empty((B, B_ver), **i32), vparent=torch.empty((B, B_ver), **i32),
-                   vtoken=torch.empty((B, B_ver), **i32),
-                   position_ids=torch.empty((B, M), **i32),
-                   mask=torch.empty((B, M, (M + 31) // 32), dtype=torch.int32, device=dev),
-                   retrieval=torch.empty((B, M, max_path), **i32),
-                   n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
-    elif tuple(out["retrieval"].shape) != (B, M, max_path):
-        raise ValueError("out['retrieval'] must be [B, B_ver + 1, max_path]")
+    shapes = dict(kept=(B, B_ver), vparent=(B, B_ver), vtoken=(B, B_ver), position_ids=(B, M),
+                  mask=(B, M, (M + 31) // 32), retrieval=(B, M, max_path), n_keep=(B,),
+                  n_leaves=(B,))
+    out = {} if out is None else out
+    out = {k: _out(out.get(k), f"out['{k}']", shp, torch.int32, dev) for k, shp in shapes.items()}
+    d_err = _err(d_err, dev)
     ts = tree.struct()
     st = lib.tg_tree_global_prune(ctypes.byref(ts), B, int(B_ver), max_path,
                                   *(_ptr(out[k]) for k in ("kept", "vparent", "vtoken",
                                                            "position_ids", "mask", "retrieval",
                                                            "n_keep", "n_leaves")),
-                                  _ptr(d_err), _stream(stream))
+                                  _ptr(d_err), _stream(stream, dev))
     _check("tg_tree_global_prune", st)
     return out
 
@@ -489,17 +557,22 @@ def kv_compact(k_cache, v_cache, prefix_len, path, n_path, new_prefix_len=None, 
     lib = load()
     _dev(k_cache, "k_cache")
     _dev(v_cache, "v_cache")
-    for t, n in ((prefix_len, "prefix_len"), (path, "path"), (n_path, "n_path")):
-        _dev(t, n, torch.int32)
-    if k_cache.shape != v_cache.shape or k_cache.dtype != v_cache.dtype:
-        raise ValueError("k_cache and v_cache must match")
+    if (k_cache.shape != v_cache.shape or k_cache.dtype != v_cache.dtype or
+            k_cache.device != v_cache.device or k_cache.dim() != 4):
+        raise ValueError("k_cache and v_cache must be matching [B, Hkv, S_max, D] tensors")
+    if k_cache.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("k_cache must be bfloat16 or float32")
     B, Hkv, S_max, D = k_cache.shape
+    dev = k_cache.device
+    _in(prefix_len, "prefix_len", (B,), torch.int32, dev)
+    _in(path, "path", (B, None), torch.int32, dev)
+    _in(n_path, "n_path", (B,), torch.int32, dev)
     dt = {torch.bfloat16: BF16, torch.float32: F32}[k_cache.dtype]
-    if new_prefix_len is None:
-        new_prefix_len = torch.empty((B,), dtype=torch.int32, device=k_cache.device)
+    new_prefix_len = _out(new_prefix_len, "new_prefix_len", (B,), torch.int32, dev)
+    d_err = _err(d_err, dev)
     st = lib.tg_kv_compact(_ptr(k_cache), _ptr(v_cache), _ptr(prefix_len), _ptr(path),
                            _ptr(n_path), B, Hkv, S_max, D, path.shape[1], dt,
-                           _ptr(new_prefix_len), _ptr(d_err), _stream(stream))
+                           _ptr(new_prefix_len), _ptr(d_err), _stream(stream, dev))
     _check("tg_kv_compact", st)
     return new_prefix_len
 
@@ -513,24 +586,28 @@ def tree_signals(tree: TreeState, frontier, n_frontier, W: int, lookback: int = 
     n_frontier [B] or None.  Returns (signals [B, 10], margin, action)."""
     lib = load()
     _dev(frontier, "frontier", torch.int32)
-    if n_frontier is not None:
-        _dev(n_frontier, "n_frontier", torch.int32)
+    if frontier.dim() != 2:
+        raise ValueError("frontier must be [B, F]")
     B, F = frontier.shape
     dev = frontier.device
-    sig = torch.empty((B, 10), dtype=torch.float32, device=dev) if signals is None else signals
+    _tree_batch(tree, B)
+    if n_frontier is not None:
+        _in(n_frontier, "n_frontier", (B,), torch.int32, dev)
+    sig = _out(signals, "signals", (B, 10), torch.float32, dev)
     if params is not None:
-        _dev(params, "params", torch.float32)
-        _dev(context, "context", torch.float32)
-        if params.numel() != 3265 or tuple(context.shape) != (B, 11):
-            raise ValueError("params must hold 3265 values and context be [B, 11]")
-        margin = torch.empty((B,), dtype=torch.float32, device=dev) if margin is None else margin
-        action = torch.empty((B,), dtype=torch.int32, device=dev) if action is None else action
+        _in(params, "params", (3265,), torch.float32, dev)
+        if context is None:
+            raise ValueError("context [B, 11] is required with params")
+        _in(context, "context", (B, 11), torch.float32, dev)
+        margin = _out(margin, "margin", (B,), torch.float32, dev)
+        action = _out(action, "action", (B,), torch.int32, dev)
     else:
         margin = action = None
+    d_err = _err(d_err, dev)
     ts = tree.struct()
     st = lib.tg_tree_signals(ctypes.byref(ts), _ptr(frontier), _ptr(n_frontier), B, F, int(W),
                              int(lookback), _ptr(context), _ptr(params), _ptr(sig),
-                             _ptr(margin), _ptr(action), _ptr(d_err), _stream(stream))
+                             _ptr(margin), _ptr(action), _ptr(d_err), _stream(stream, dev))
     _check("tg_tree_signals", st)
     return sig, margin, action
 
@@ -539,7 +616,8 @@ def tree_reset(tree: TreeState, stream=None):
     """Empty every tree (n_nodes = 0, root unvisited) with a device kernel."""
     lib = load()
     ts = tree.struct()
-    _check("tg_tree_reset", lib.tg_tree_reset(ctypes.byref(ts), tree.B, _stream(stream)))
+    _check("tg_tree_reset", lib.tg_tree_reset(ctypes.byref(ts), tree.B,
+                                              _stream(stream, tree.parent.device)))
 
 
 def trace_begin(capacity: int = 4096):

@@ -140,6 +140,18 @@ def test_hand_expansion_values_capacity_and_bad_frontier():
     t3, _, nxt3, nn3, err = NG.expand_ngram(t2, np.array([[2]], np.int32), None, ctx, clen,
                                             tok, lp, fb, 2, 3, 3)
     assert err == T.DERR_CAPACITY and int(nn3[0]) == 0 and int(t3.n_nodes[0]) == 6
+    # a partial overflow: 5 live nodes, one frontier node with K = 2 children
+    # would need 7 slots of the 6; CAPACITY, nothing appended
+    t5 = t2.copy()
+    t5.n_nodes[0] = 5
+    t6, _, _, nn6, err = NG.expand_ngram(t5, np.array([[2]], np.int32), None, ctx, clen,
+                                         tok, lp, fb, 2, 3, 3)
+    assert err == T.DERR_CAPACITY and int(nn6[0]) == 0 and int(t6.n_nodes[0]) == 5
+    assert np.array_equal(t6.token, t5.token) and np.array_equal(t6.parent, t5.parent)
+    # one child fewer fits exactly (K = 1: 5 + 1 = 6 slots)
+    t7, _, _, nn7, err = NG.expand_ngram(t5, np.array([[2]], np.int32), None, ctx, clen,
+                                         tok, lp, fb, 1, 3, 3)
+    assert err == 0 and int(nn7[0]) == 1 and int(t7.n_nodes[0]) == 6
     # a frontier id equal to the node count is not a node
     t4 = T.Tree.empty(1, 16)
     t4.parent[0, :2], t4.token[0, :2], t4.depth[0, :2], t4.n_nodes[0] = [-1, 0], [3, 3], [1, 2], 2
