@@ -1,51 +1,46 @@
 #!/usr/bin/env python3
 """Benchmark of the tree-verify / tree-expand hot path on one MI355X.
 
-One step = one TreeGraft decoding turn's data-parallel work on the
-Llama-3-8B-shaped workload (batch 1, vocabulary 128256, frontier W = 10,
-m = 8 children per node, 32/8 heads, head_dim 128, prefix 2048, bf16):
+Headline (one step = one call of tg_tree_verify_attention): the
+Llama-3-70B-shaped verify layer, the largest single-GPU workload - batch 8,
+64 query heads / 8 KV heads, head_dim 128, bf16, a 32768-token prefix per
+sequence and a 256-node draft tree per sequence (12 levels, at most 8
+children per node), Q/K/V i.i.d. N(0,1).  This is target-side verification,
+the largest per-call cost of a decoding turn.  `value` is the call's
+algorithmic flops (4 * D per (query row, visible key); ancestors only) per
+second with every input resident in HBM; `roofline` is the ping-pong
+attention kernel's own launch time, taken with HIP events on the launch
+stream around the timed calls (one kernel per call at this shape).
 
-  reset          the shared tree becomes the lone root (T_1 = {r}, P_1 = {})
-  every step     tg_tree_signals        the scheduler's ten tree signals and
-                                        its margin predictor (the action it
-                                        returns is overridden by the fixed
-                                        schedule below, so the tree is the same
-                                        every turn)
-  k=1  middle    tg_tree_rescore_graft  pool {root}: graft its top-8 children
-  k=2  small     tg_tree_expand_ngram   the n-gram drafter expands Top_W of
-                                        the grafted children from the prefill
-                                        cache (8 candidates per position)
-  k=3  middle    tg_tree_rescore_graft  pool = 72 unvisited nodes, rescore,
-                                        reselect 10 graft points, +80 nodes
-  k=4  small     tg_tree_expand_ngram   expand Top_W of those 80
-  k=5  middle    tg_tree_rescore_graft  pool = 160 nodes, rescore, +80 nodes
-  prune          tg_tree_global_prune   the 312-node tree -> 64 nodes (Alg. 3)
-                                        + verification buffers
-  verify         tg_tree_verify_attention  one target layer over the pruned
-                                        tree (its parent array as is: -1 =
-                                        the prefix end, which holds the root)
-  accept         tg_tree_accept         greedy acceptance on the pruned tree
-  cache          tg_kv_compact          the accepted rows extend the prefix
+Besides the headline, the default run measures every other workload once and
+reports each under `extra` with its own roofline and CPU baseline:
+  tiny                the tiny fp32 workload: attention (B1, 4/4 heads, D64,
+                      prefix 128, 16 nodes), one expansion (V=1000, F=8, K=4,
+                      N=8) and acceptance, as one step (microseconds)
+  attn-llama8b        the Llama-3-8B-shaped verify layer (B1, 32/8 heads,
+                      prefix 2048, 64 nodes) - one call (split-prefix mode)
+  attn-llama8b-x32    32 independent layers of that shape back to back
+                      (310 MB): the steady-state bandwidth the single call's
+                      launch latency hides
+  attn-longctx        long-context verify (B4, 32/8 heads, prefix 8192, 128
+                      nodes of 10 levels)
+  expand-twodrafter   two-drafter expansion: B8 trees of 256 nodes (a 5-step
+                      weak top-10 / frontier-10 expansion pruned by Alg. 3),
+                      the 64 best leaves expanded (K=10, N=60), V=128256
+  rescore-twodrafter  the middle step on the same trees (257 strong rows,
+                      W=60, m=10; strong = 0.8 weak + 0.6 noise)
+  turn                one TreeGraft turn (schedule [1,0,1,0,1], n-gram small
+                      drafter, scheduler signals, GlobalPrune to 64 nodes,
+                      Llama-3-8B verify layer, accept, KV update), replayed as
+                      one HIP graph
+`--workload NAME` times only that workload as the headline; `--only` skips
+the extras.  All inputs are seeded synthetic data with the workloads' shapes
+and distributions (no model weights or datasets).  The CPU baselines time the
+oracle (the tests' plain CPU reference, untuned) on a bounded sample of the
+same inputs on this machine's host cores, and report how far the GPU result
+is from it.
 
-The schedule [1,0,1,0,1] is the paper's fixed ablation schedule (Sec. 5.3);
-the small drafter is the paper's n-gram drafter, whose cache (the target's
-top-8 next tokens at each of the 2048 prompt positions) is built once per
-input copy at set-up, as at prefill.
-Drafter and target logits, Q/K/V and tokens are seeded synthetic data of the
-workload's shapes and distributions (logits N(0,3) fp32; the prompt a token
-stream of recurring phrases; Q/K/V N(0,1)/sqrt(128)
-bf16; the target's greedy token at each pruned-tree node is its first child's
-token with p = 0.7, fixed once per input copy from the tree the turn builds).  Inputs rotate over several resident copies (> the 256 MB MALL) so no
-timed read is served from the last-level cache.
-
-The timed region replays one captured HIP graph per input copy (the whole
-step, so host launch overhead is not measured).  A second, eager pass over the
-same steps records every kernel's device time with the library's trace events
-(an event pair on the launch stream around each kernel); the dominant
-kernel's roofline comes from those.  The CPU baseline times the oracle (tests' CPU
-reference) on the same inputs.
-
-Prints ONE JSON line.  One GPU only: N > 1 exits with a message.
+Prints ONE JSON line.  One GPU only: --gpus N > 1 exits with a message.
 """
 from __future__ import annotations
 
@@ -64,39 +59,33 @@ if ROOT not in sys.path:
 METRIC = "tree-verify attention TB/s & TFLOP/s (% roofline); draft-tree nodes/sec"
 PEAK_HBM = 8.0e12        # B/s, MI355X HBM3E
 PEAK_BF16 = 2.5e15       # flop/s, dense bf16 MFMA
+PEAK_FP32 = 157.3e12     # flop/s, fp32 vector
 ATTN_MAIN = ("attn_pingpong", "attn_mfma", "attn_f32")   # tree-verify attention kernels
-
-# workload (Llama-3-8B-shaped turn)
-V, W_FR, M_CH = 128256, 10, 8
-SCHEDULE = (1, 0, 1, 0, 1)
-B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64     # N_VER = B_ver pruned nodes
-CAP = 512
-MAX_DEPTH = 8            # accept path width (the turn's trees are at most 5 deep)
-R_ROWS = 313             # strong-logits rows (root + up to 312 nodes)
-NG_NMAX = 4              # n-gram drafter: longest n-gram matched
+WORKLOADS = ["attn-llama70b", "tiny", "attn-llama8b", "attn-llama8b-x32", "attn-longctx",
+             "expand-twodrafter", "rescore-twodrafter", "turn"]
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--copies", type=int, default=4, help="resident input copies")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="attn-llama70b", choices=WORKLOADS,
+                    help="the headline workload (default: the Llama-3-70B-shaped layer)")
+    ap.add_argument("--only", action="store_true", help="measure the headline workload only")
+    ap.add_argument("--copies", type=int, default=4, help="turn: resident input copies")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="approximate CPU time budget of the oracle baseline")
+                    help="approximate CPU time of the headline's oracle baseline")
+    ap.add_argument("--extra-cpu-seconds", type=float, default=3.0,
+                    help="approximate CPU time of each extra workload's oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="profiling aid: run one device copy of this many MiB first, so a "
                          "counter pass can scale FETCH_SIZE/WRITE_SIZE by a known size")
     ap.add_argument("--rescore-flags", type=int, default=0,
-                    help="rescore-twodrafter only: middle-step variant flags (1 = pool of the "
+                    help="rescore-twodrafter: middle-step variant flags (1 = pool of the "
                          "previous step's new nodes, 2 = overwriting graft, 4 = skip "
                          "duplicate siblings; the Sec. 5.3 ablations and a filter)")
-    ap.add_argument("--workload", default="turn",
-                    choices=["turn", "attn-llama8b", "attn-longctx", "attn-llama70b",
-                             "expand-twodrafter", "rescore-twodrafter"],
-                    help="turn (default) or tree-verify attention alone at one shape")
     return ap.parse_args()
 
 
@@ -125,7 +114,626 @@ def profile_traffic(name):
         return None
 
 
-# ---------------------------------------------------------------- inputs
+TRAFFIC_FILES = {
+    ("attn-llama70b", "attn_pingpong"): "attn_pingpong_llama70b_traffic.md",
+    ("attn-longctx", "attn_pingpong"): "attn_pingpong_longctx_traffic.md",
+    ("expand-twodrafter", "row_partial"): "row_partial_expand_twodrafter_traffic.md",
+    ("rescore-twodrafter", "row_partial"): "row_partial_rescore_twodrafter_traffic.md",
+    ("turn", "row_partial"): "row_partial_turn_llama8b_traffic.md",
+}
+
+
+def traffic_for(workload, kernel):
+    f = TRAFFIC_FILES.get((workload, kernel))
+    return profile_traffic(f) if f else None
+
+
+# ------------------------------------------------------------ timing
+
+def time_calls(torch, fn, steps, warmup):
+    """Average milliseconds of fn() over `steps` calls (after `warmup`),
+    bracketed by HIP events on the current stream, the stream the library
+    launches on, with a device synchronisation on both sides."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        fn(warmup + i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def kernel_times(tg, torch, fn, steps, start=0):
+    """Per-kernel device times of `steps` eager calls from the library's trace
+    events (an event pair on the launch stream around each kernel; a separate
+    pass from the timed one).  Returns {kernel: [launches, total ms]}."""
+    torch.cuda.synchronize()
+    tg.trace_begin(64 * (steps + 1))
+    try:
+        for i in range(steps):
+            fn(start + i)
+        torch.cuda.synchronize()
+    finally:
+        recs = tg.trace_end()
+    kern = {}
+    for name, ms in recs:
+        d = kern.setdefault(name, [0, 0.0])
+        d[0] += 1
+        d[1] += ms
+    return kern, recs
+
+
+def kernels_json(kern, steps):
+    return {k: {"launches_per_step": v[0] / steps, "avg_us": 1e3 * v[1] / v[0],
+                "us_per_step": 1e3 * v[1] / steps} for k, v in kern.items()}
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return 1
+
+
+def line(value, unit, steps, warmup, ms, config, roofline, dtype, higher=True, **extra):
+    out = {"metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": ms, "higher_is_better": higher, "scaling": "weak",
+           "vs_baseline": None, "dtype": dtype, "data": "synthetic", "config": config,
+           "roofline": roofline}
+    out.update(extra)
+    return out
+
+
+# ------------------------------------------------------- attention alone
+
+ATTN_SHAPES = {
+    # name: (B, Hq, Hkv, D, prefix, nodes, levels, qkv scale, dtype, description)
+    "attn-llama70b": (8, 64, 8, 128, 32768, 256, 12, 1.0, "bf16",
+                      "Llama-3-70B-shaped verify layer"),
+    "attn-longctx": (4, 32, 8, 128, 8192, 128, 10, 1.0, "bf16", "long-context verify layer"),
+    "attn-llama8b": (1, 32, 8, 128, 2048, 64, None, 1.0 / np.sqrt(128.0), "bf16",
+                     "Llama-3-8B-shaped verify layer"),
+    "tiny": (1, 4, 4, 64, 128, 16, "uniform", 1.0, "f32", "tiny fp32 verify layer"),
+}
+
+
+def attn_parents(name, g):
+    Bq, _, _, _, _, Nn, levels, _, _, _ = ATTN_SHAPES[name]
+    import workloads as W
+    if levels is None:         # root + draft nodes shaped like a pruned expansion
+        return np.stack([W.verify_layout_with_root(W.expansion_shaped_tree(g, Nn - 1, 6, 8, 10))
+                         for _ in range(Bq)]).astype(np.int32)
+    if levels == "uniform":
+        return np.stack([W.uniform_parents(g, Nn) for _ in range(Bq)]).astype(np.int32)
+    return np.stack([W.level_tree(g, Nn, levels, 8) for _ in range(Bq)]).astype(np.int32)
+
+
+def path_len_sum(vpar):
+    """Sum over nodes of the number of tree keys a node attends to (its
+    ancestors and itself)."""
+    tot = 0
+    for i in range(len(vpar)):
+        u = i
+        while u != -1:
+            tot += 1
+            u = int(vpar[u])
+    return tot
+
+
+def attn_work(name, par):
+    """Algorithmic bytes (each K/V element read once, Q read, O written, the
+    parent array) and flops (4 * D per (query row, visible key), ancestors
+    only) of one call."""
+    Bq, Hq, Hkv, Dh, Lp, Nn, _, _, dt, _ = ATTN_SHAPES[name]
+    es = 2 if dt == "bf16" else 4
+    keys = sum(Nn * Lp + path_len_sum(par[b]) for b in range(Bq))
+    flops = 4 * Dh * Hq * keys
+    nbytes = 2 * Bq * Hkv * (Lp + Nn) * Dh * es + 2 * Bq * Nn * Hq * Dh * es + par.nbytes
+    return nbytes, flops
+
+
+def attn_inputs(torch, dev, name, n_copies, seed=2000):
+    import workloads as W
+    Bq, Hq, Hkv, Dh, Lp, Nn, _, scale, dt, _ = ATTN_SHAPES[name]
+    dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+    S = Lp + Nn
+    bufs = []
+    for c in range(n_copies):
+        gc = W.rng([seed, c])
+        q = torch.empty((Bq, Nn, Hq, Dh), dtype=dtype, device=dev)
+        k = torch.empty((Bq, Hkv, S, Dh), dtype=dtype, device=dev)
+        v = torch.empty((Bq, Hkv, S, Dh), dtype=dtype, device=dev)
+        for b in range(Bq):     # per-sequence draws keep host memory small
+            q[b] = torch.from_numpy(W.normal(gc, (Nn, Hq, Dh)) * np.float32(scale)).to(dev)
+            k[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
+            v[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
+        bufs.append((q, k, v, torch.empty_like(q)))
+    return bufs
+
+
+def attn_cpu_baseline(name, par, buf, budget_s):
+    """The oracle on whole (batch, KV head) groups of input copy 0, in a fixed
+    seeded order, until about `budget_s` seconds are spent; also the GPU's
+    error against it on those groups (max abs, tensor-relative Frobenius)."""
+    from oracle.attention import tree_verify_attention_fast
+    import workloads as W
+    Bq, Hq, Hkv, Dh, Lp, Nn, _, _, _, _ = ATTN_SHAPES[name]
+    G = Hq // Hkv
+    q, k, v, o = buf
+    order = W.rng(77).permutation(Bq * Hkv)
+    flops = nbytes = 0
+    done, err_abs, num, den = 0, 0.0, 0.0, 0.0
+    t_cpu = 0.0
+    for gi in order:
+        b, g0 = divmod(int(gi), Hkv)
+        qh = q[b:b + 1, :, g0 * G:(g0 + 1) * G].float().cpu().numpy()
+        kh = k[b:b + 1, g0:g0 + 1].float().cpu().numpy()
+        vh = v[b:b + 1, g0:g0 + 1].float().cpu().numpy()
+        t0 = time.perf_counter()
+        want = tree_verify_attention_fast(qh, kh, vh, par[b:b + 1], [Lp], Dh ** -0.5)
+        t_cpu += time.perf_counter() - t0
+        got = o[b:b + 1, :, g0 * G:(g0 + 1) * G].float().cpu().numpy().astype(np.float64)
+        err_abs = max(err_abs, float(np.abs(got - want).max()))
+        num += float(((got - want) ** 2).sum())
+        den += float((want ** 2).sum())
+        flops += 4 * Dh * G * (Nn * Lp + path_len_sum(par[b]))
+        nbytes += 2 * (Lp + Nn) * Dh * 2 + 2 * Nn * G * Dh * 2
+        done += 1
+        if t_cpu >= budget_s:
+            break
+    parity = {"groups_checked": done, "groups_total": Bq * Hkv, "max_abs_err": err_abs,
+              "rel_fro_err": (num / den) ** 0.5 if den > 0 else 0.0,
+              "bars": {"max_abs": 2e-2, "rel_fro": 1e-2}}
+    return flops, nbytes, t_cpu, done, parity
+
+
+def attention_bench(tg, torch, dev, name, steps, warmup, cpu_s):
+    """tg_tree_verify_attention alone at one workload shape; inputs rotate over
+    enough copies to exceed 512 MB so no timed read hits the 256 MB MALL."""
+    import workloads as W
+    Bq, Hq, Hkv, Dh, Lp, Nn, _, _, dt, desc = ATTN_SHAPES[name]
+    es = 2 if dt == "bf16" else 4
+    par = attn_parents(name, W.rng(2000))
+    per_copy = 2 * Bq * Hkv * (Lp + Nn) * Dh * es
+    copies = max(1, min(8, -(-(512 << 20) // per_copy)))
+    bufs = attn_inputs(torch, dev, name, copies)
+    parent = torch.from_numpy(par).to(dev)
+    plen = torch.full((Bq,), Lp, dtype=torch.int32, device=dev)
+    nws = tg.verify_attention_workspace(Bq, Nn, Hq, Hkv, Dh, Lp + Nn,
+                                        tg.BF16 if dt == "bf16" else tg.F32)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+
+    def call(i):
+        q, k, v, o = bufs[i % copies]
+        tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
+
+    ms = time_calls(torch, call, steps, warmup)
+    kern, _ = kernel_times(tg, torch, call, steps, start=0)
+    call(0)                       # copy 0's output for the parity margin
+    torch.cuda.synchronize()
+    main_k = next(k for k in ATTN_MAIN if k in kern)
+    nbytes, flops = attn_work(name, par)
+    one_kernel = len(kern) == 1 and kern[main_k][0] == steps
+    # the main kernel's launch time: the timed pass itself when a call is
+    # that one kernel, else the trace pass's event pairs around it
+    main_us = 1e3 * ms if one_kernel else 1e3 * kern[main_k][1] / kern[main_k][0]
+    if dt == "f32":
+        bound = "hbm" if nbytes / PEAK_HBM > flops / PEAK_FP32 else "alu"
+    else:
+        bound = "mfma" if flops / nbytes > PEAK_BF16 / PEAK_HBM else "hbm"
+    if bound == "mfma":
+        ach, peak, unit = flops / (main_us * 1e-6) / 1e12, PEAK_BF16 / 1e12, "TFLOP/s"
+    elif bound == "alu":
+        ach, peak, unit = flops / (main_us * 1e-6) / 1e12, PEAK_FP32 / 1e12, "TFLOP/s"
+    else:
+        ach, peak, unit = nbytes / (main_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s"
+    roof = {"bound": bound, "kernel": main_k, "achieved": ach, "peak": peak, "unit": unit,
+            "frac": ach / peak, "traffic": traffic_for(name, main_k),
+            "avg_launch_us": main_us,
+            "launch_time_from": "timed pass (one kernel per call)" if one_kernel
+            else "trace pass (event pair around each kernel)"}
+    call_s = ms * 1e-3
+    if bound == "hbm":
+        value, vunit = nbytes / call_s / 1e12, "TB/s"
+    else:
+        value, vunit = flops / call_s / 1e12, "TFLOP/s"
+    out = line(value, vunit, steps, warmup, ms,
+               {"workload": f"{desc} (B{Bq}, {Hq}/{Hkv} heads, D{Dh}, prefix {Lp}, "
+                            f"{Nn} tree nodes, {dt})", "batch": Bq, "q_heads": Hq,
+                "kv_heads": Hkv, "head_dim": Dh, "prefix": Lp, "tree_nodes": Nn,
+                "input_copies": copies},
+               roof, dt, **{"TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
+                            "bytes": nbytes, "flops": flops,
+                            "kernels": kernels_json(kern, steps)})
+    if cpu_s > 0:
+        f_cpu, b_cpu, t_cpu, done, parity = attn_cpu_baseline(name, par, bufs[0], cpu_s)
+        out["cpu_baseline"] = {
+            "value": (b_cpu if bound == "hbm" else f_cpu) / t_cpu / 1e12, "unit": vunit,
+            "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{done} of {Bq * Hkv} (batch, KV head) groups of the same inputs in "
+                      f"{t_cpu:.1f} s (fp64 NumPy; its matrix products on the BLAS threads "
+                      f"counted in cores), rate scaled by that group's share of the work"}
+        out["parity"] = parity
+    return out
+
+
+def attention_layers_bench(tg, torch, dev, steps, warmup, cpu_s, layers=32):
+    """`layers` independent Llama-3-8B-shaped verify layers (each its own Q,
+    K/V cache and output: 310 MB at 32) back to back; one step = all of them."""
+    import workloads as W
+    name = "attn-llama8b"
+    Bq, Hq, Hkv, Dh, Lp, Nn, _, _, _, desc = ATTN_SHAPES[name]
+    par = attn_parents(name, W.rng(2000))
+    bufs = attn_inputs(torch, dev, name, layers, seed=2100)
+    parent = torch.from_numpy(par).to(dev)
+    plen = torch.full((Bq,), Lp, dtype=torch.int32, device=dev)
+    nws = tg.verify_attention_workspace(Bq, Nn, Hq, Hkv, Dh, Lp + Nn, tg.BF16)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+
+    def step(i):
+        for q, k, v, o in bufs:
+            tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
+
+    ms = time_calls(torch, step, steps, warmup)
+    kern, _ = kernel_times(tg, torch, step, max(2, steps // 4))
+    nb1, fl1 = attn_work(name, par)
+    nbytes, flops = layers * nb1, layers * fl1
+    ach = nbytes / (ms * 1e-3)
+    roof = {"bound": "hbm", "kernel": "attn_mfma + attn_combine (all launches of the step)",
+            "achieved": ach / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+            "frac": ach / PEAK_HBM, "traffic": None, "avg_launch_us": None,
+            "launch_time_from": "timed pass (whole step)"}
+    out = line(nbytes / (ms * 1e-3) / 1e12, "TB/s", steps, warmup, ms,
+               {"workload": f"{layers} independent {desc}s back to back (B{Bq}, {Hq}/{Hkv} "
+                            f"heads, D{Dh}, prefix {Lp}, {Nn} tree nodes, bf16)",
+                "layers": layers}, roof, "bf16",
+               **{"TFLOP/s": flops / (ms * 1e-3) / 1e12, "bytes": nbytes, "flops": flops,
+                  "kernels": kernels_json(kern, max(2, steps // 4))})
+    if cpu_s > 0:
+        f_cpu, b_cpu, t_cpu, done, parity = attn_cpu_baseline(name, par, bufs[0], cpu_s)
+        out["cpu_baseline"] = {"value": b_cpu / t_cpu / 1e12, "unit": "TB/s",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"{done} (batch, KV head) groups of layer 0 in "
+                                         f"{t_cpu:.1f} s"}
+        out["parity"] = parity
+    return out
+
+
+# --------------------------------------------------------- tiny workload
+
+def tiny_bench(tg, torch, dev, steps, warmup, cpu_s):
+    """The tiny fp32 workload as one step: attention, one expansion from the 8
+    best nodes of a 16-node tree (V=1000, K=4, N=8) and acceptance (target
+    tokens match a random child with p = 0.5).  Launch-latency bound: the
+    line reports microseconds per step."""
+    import workloads as W
+    cfg = W.CONFIGS["tiny"]
+    g = W.rng(cfg["seed"])
+    Nn, Lp, Dh, Vv = cfg["N"], cfg["L"], cfg["D"], cfg["vocab"]
+    parent = W.uniform_parents(g, Nn)[None]
+    q = torch.from_numpy(W.normal(g, (1, Nn, 4, Dh))).to(dev)
+    k = torch.from_numpy(W.normal(g, (1, 4, Lp + Nn, Dh))).to(dev)
+    v = torch.from_numpy(W.normal(g, (1, 4, Lp + Nn, Dh))).to(dev)
+    tok = W.distinct_sibling_tokens(g, parent[0], Vv)
+    greedy = W.greedy_match_random_child(g, parent[0], tok, Vv, 0.5)
+    logits = torch.from_numpy(W.normal(g, (1, 8, Vv), cfg["logit_std"])).to(dev)
+    dpar = torch.from_numpy(parent).to(dev)
+    plen = torch.tensor([Lp], dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    # the expansion's tree: the 16 nodes, each with a synthetic path score
+    # (-depth - id / 100; it only orders the frontier and offsets the
+    # children's scores) in a tree of capacity 64
+    depth = W.node_depths(parent[0])
+    cum = -depth.astype(np.float32) - np.float32(0.01) * np.arange(Nn, dtype=np.float32)
+
+    def pad(a, fill, dtype):
+        o = np.full((1, 64), fill, dtype)
+        o[0, :Nn] = a
+        return o
+    base = tg.TreeState.from_host(dict(parent=pad(parent[0], -1, np.int32),
+                                       token=pad(tok, 0, np.int32),
+                                       depth=pad(depth, 0, np.int32),
+                                       logp=pad(-1.0, 0.0, np.float32),
+                                       cum=pad(cum, 0.0, np.float32),
+                                       visited=np.zeros((1, 64), np.uint8),
+                                       root_visited=np.zeros(1, np.uint8),
+                                       n_nodes=np.array([Nn], np.int32)), 64, dev)
+    order = sorted(range(Nn), key=lambda i: (-float(cum[i]), int(depth[i]), i))
+    fr = torch.tensor([order[:8]], dtype=torch.int32, device=dev)
+    n_trees = warmup + 2 * steps + 1
+    trees = [tg.TreeState(1, 64, dev) for _ in range(n_trees)]
+    for t in trees:
+        for f in tg.TreeState.FIELDS:
+            getattr(t, f).copy_(getattr(base, f))
+    ws = torch.empty(tg.expand_topk_workspace(1, 8, Vv, 4, 8), dtype=torch.uint8, device=dev)
+    lse = torch.empty((1, 8), dtype=torch.float32, device=dev)
+    nx = torch.empty((1, 8), dtype=torch.int32, device=dev)
+    nn = torch.empty((1,), dtype=torch.int32, device=dev)
+    dtok = torch.from_numpy(tok[None]).to(dev)
+    dgreedy = torch.from_numpy(greedy[None]).to(dev)
+    nnodes = torch.tensor([Nn], dtype=torch.int32, device=dev)
+    A = torch.empty((1,), dtype=torch.int32, device=dev)
+    path = torch.empty((1, Nn), dtype=torch.int32, device=dev)
+    bonus = torch.empty((1,), dtype=torch.int32, device=dev)
+
+    def step(i):
+        tg.verify_attention(q, k, v, dpar, plen, Dh ** -0.5, out=out)
+        tg.expand_topk(trees[i], logits, fr, None, 4, 8, row_lse=lse, next_frontier=nx,
+                       n_next=nn, workspace=ws)
+        tg.accept(dpar, dtok, nnodes, dgreedy, Nn, accept_len=A, accept_path=path, bonus=bonus)
+
+    ms = time_calls(torch, step, steps, warmup)
+    kern, _ = kernel_times(tg, torch, step, steps, start=warmup + steps)
+    nbytes, flops = attn_work("tiny", parent)
+    a_us = 1e3 * kern["attn_f32"][1] / kern["attn_f32"][0]
+    roof = {"bound": "hbm", "kernel": "attn_f32", "achieved": nbytes / (a_us * 1e-6) / 1e9,
+            "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+            "frac": nbytes / (a_us * 1e-6) / PEAK_HBM, "traffic": None, "avg_launch_us": a_us,
+            "launch_time_from": "trace pass (event pair around each kernel)",
+            "note": "launch-latency bound: 0.33 MB per call"}
+    res = line(1e3 * ms, "us", steps, warmup, ms,
+               {"workload": "tiny fp32 workload: attention (B1, 4/4 heads, D64, prefix 128, "
+                            "16 nodes) + expansion (V=1000, F=8, K=4, N=8) + acceptance"},
+               roof, "f32", higher=False, kernels=kernels_json(kern, steps))
+    if cpu_s > 0:
+        from oracle import attention as OA
+        from oracle import tree as OT
+        th = base.to_host()
+        tree_h = OT.Tree(th["parent"], th["token"], th["depth"], th["logp"], th["cum"],
+                         th["visited"], th["root_visited"], th["n_nodes"], cap=64)
+        qh, kh, vh = q.cpu().numpy(), k.cpu().numpy(), v.cpu().numpy()
+        lh, frh = logits.cpu().numpy(), fr.cpu().numpy()
+        n, t0 = 0, time.perf_counter()
+        while True:
+            want = OA.tree_verify_attention(qh, kh, vh, parent, [Lp], Dh ** -0.5)
+            _, _, nx_o, nn_o, _ = OT.expand(tree_h, lh, frh, None, 4, 8)
+            A_o, _, _, _ = OT.accept(parent, tok[None], np.array([Nn]), greedy[None], Nn)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= cpu_s:
+                break
+        step(n_trees - 1)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().astype(np.float64)
+        rowerr = np.abs(got - want).max(axis=-1) / np.abs(want).max(axis=-1)
+        res["cpu_baseline"] = {"value": 1e6 * el / n, "unit": "us", "cores": 1, "kind": "oracle",
+                               "sample": f"{n} full steps in {el:.1f} s (single-threaded NumPy)"}
+        res["parity"] = {"attention_max_row_rel_err": float(rowerr.max()), "bar": 1e-5,
+                         "next_frontier_equal": bool(np.array_equal(nx.cpu().numpy(), nx_o)),
+                         "accept_len_equal": bool(int(A.item()) == int(A_o[0]))}
+    return res
+
+
+# ------------------------------------------- two-drafter tree workloads
+
+TD_B, TD_V, TD_K, TD_N, TD_W, TD_M, TD_F, TD_R = 8, 128256, 10, 60, 60, 10, 64, 257
+
+
+def twodrafter_trees(tg, torch, dev):
+    """The two-drafter workload's trees, built on the GPU by the library: per
+    tree a 5-step weak expansion from the root (frontier 10, top-10: 410
+    nodes) pruned by Alg. 3 to 256 nodes, re-indexed, with its logits rows
+    re-indexed alike (row 0 = root, row 1 + i = kept node i); weak rows
+    N(0,3), strong = 0.8 * weak + 0.6 * N(0,3) (correlation 0.8).  Returns
+    (template TreeState, weak rows, strong rows, frontier of the 64 best
+    leaves)."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3000)
+    big_rows = torch.empty((TD_B, 411, TD_V), dtype=torch.float32, device=dev)
+    big_rows.normal_(0.0, 3.0, generator=gen)       # row 0 root, row 1 + id
+    ts = tg.TreeState(TD_B, 512, dev)
+    fr = torch.full((TD_B, 1), -1, dtype=torch.int32, device=dev)
+    nf = torch.ones(TD_B, dtype=torch.int32, device=dev)
+    bidx = torch.arange(TD_B, device=dev)[:, None]
+    for _ in range(5):
+        lg = big_rows[bidx, (fr + 1).long()].contiguous()
+        _, fr, nf = tg.expand_topk(ts, lg, fr.contiguous(), nf, 10, 10)
+    torch.cuda.synchronize()
+    assert int(ts.n_nodes.min().item()) == 410 == int(ts.n_nodes.max().item())
+    pr = tg.global_prune(ts, 256)
+    torch.cuda.synchronize()
+    assert int(pr["n_keep"].min().item()) == 256
+    kept = pr["kept"].long()
+    tmpl = tg.TreeState(TD_B, 2048, dev)
+    tmpl.parent[:, :256] = pr["vparent"]
+    tmpl.token[:, :256] = pr["vtoken"]
+    tmpl.depth[:, :256] = torch.gather(ts.depth, 1, pr["kept"].long())
+    tmpl.logp[:, :256] = torch.gather(ts.logp, 1, kept)
+    tmpl.cum[:, :256] = torch.gather(ts.cum, 1, kept)
+    tmpl.n_nodes.fill_(256)
+    rows = torch.cat([torch.zeros((TD_B, 1), dtype=torch.long, device=dev), kept + 1], dim=1)
+    weak = big_rows[bidx, rows].contiguous()
+    del big_rows
+    noise = torch.empty_like(weak)
+    noise.normal_(0.0, 3.0, generator=gen)
+    strong = (0.8 * weak + 0.6 * noise).contiguous()
+    del noise
+    # the expansion's frontier: the 64 best leaves by (cum desc, depth asc, id asc)
+    par_h, cum_h, dep_h = (tmpl.parent[:, :256].cpu().numpy(), tmpl.cum[:, :256].cpu().numpy(),
+                           tmpl.depth[:, :256].cpu().numpy())
+    front = np.empty((TD_B, TD_F), np.int32)
+    for b in range(TD_B):
+        has_kid = set(int(p) for p in par_h[b])
+        leaves = [u for u in range(256) if u not in has_kid]
+        leaves.sort(key=lambda u: (-float(cum_h[b, u]), int(dep_h[b, u]), u))
+        front[b] = leaves[:TD_F]
+    return tmpl, weak, strong, torch.from_numpy(front).to(dev)
+
+
+def tree_bench(tg, torch, dev, name, steps, warmup, cpu_s, flags=0, shared=None):
+    """tg_tree_expand_topk (the 64 best leaves of each tree, K=10, N=60) or
+    tg_tree_rescore_graft (W=60, m=10) on the two-drafter trees; every timed
+    call gets a fresh copy of the tree (the calls append to it)."""
+    tmpl, weak, strong, front = shared if shared is not None else twodrafter_trees(tg, torch, dev)
+    rescore = name == "rescore-twodrafter"
+    bidx = torch.arange(TD_B, device=dev)[:, None]
+    if rescore:
+        copies = 1                                           # 1.05 GB > the MALL
+        logits = [strong]
+    else:
+        exp_rows = weak[bidx, (front + 1).long()].contiguous()  # [B, 64, V], 263 MB
+        copies = 3
+        logits = [exp_rows] + [exp_rows.clone() for _ in range(copies - 1)]
+    n_trees = warmup + 2 * steps + 1
+    trees = [tg.TreeState(TD_B, 2048, dev) for _ in range(n_trees)]
+    for ts in trees:
+        for f in tg.TreeState.FIELDS:
+            getattr(ts, f).copy_(getattr(tmpl, f))
+    i32 = dict(dtype=torch.int32, device=dev)
+    if rescore:
+        ws = torch.empty(tg.rescore_graft_workspace(TD_B, TD_R, TD_V, TD_W, TD_M, 2048),
+                         dtype=torch.uint8, device=dev)
+        lse = torch.empty((TD_B, TD_R), dtype=torch.float32, device=dev)
+        gf, ng = torch.empty((TD_B, TD_W), **i32), torch.empty((TD_B,), **i32)
+        new_from = torch.full((TD_B,), 16, **i32) if flags & 1 else None
+
+        def call(i):
+            tg.rescore_graft(trees[i], logits[i % copies], TD_W, TD_M, row_lse=lse,
+                             graft_frontier=gf, n_graft=ng, workspace=ws, flags=flags,
+                             new_from=new_from)
+        # rows read: every pool node's row and its parent's (the paper's pool:
+        # the 257 rows; w/o EG: the pool ids >= 16 and their parents)
+        if flags & 1:
+            par_h = tmpl.parent[:, :256].cpu().numpy()
+            rows_read = sum(len({u + 1 for u in range(16, 256)} |
+                                {int(par_h[b, u]) + 1 for u in range(16, 256)})
+                            for b in range(TD_B))
+            pool = TD_B * 240
+        else:
+            rows_read, pool = TD_B * TD_R, TD_B * 257
+        nbytes = rows_read * TD_V * 4
+        nodes = pool + TD_B * TD_W * TD_M
+    else:
+        ws = torch.empty(tg.expand_topk_workspace(TD_B, TD_F, TD_V, TD_K, TD_N),
+                         dtype=torch.uint8, device=dev)
+        lse = torch.empty((TD_B, TD_F), dtype=torch.float32, device=dev)
+        nx, nn = torch.empty((TD_B, TD_N), **i32), torch.empty((TD_B,), **i32)
+
+        def call(i):
+            tg.expand_topk(trees[i], logits[i % copies], front, None, TD_K, TD_N, row_lse=lse,
+                           next_frontier=nx, n_next=nn, workspace=ws)
+        nbytes = TD_B * TD_F * TD_V * 4
+        nodes = TD_B * TD_F * TD_K
+    ms = time_calls(torch, call, steps, warmup)
+    kern, _ = kernel_times(tg, torch, call, steps, start=warmup + steps)
+    row_us = 1e3 * kern["row_partial"][1] / kern["row_partial"][0]
+    ach = nbytes / (row_us * 1e-6)
+    roof = {"bound": "hbm", "kernel": "row_partial", "achieved": ach / 1e9,
+            "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": ach / PEAK_HBM,
+            "traffic": traffic_for(name, "row_partial") if flags == 0 else None,
+            "avg_launch_us": row_us,
+            "launch_time_from": "trace pass (event pair around each kernel)"}
+    out = line(nodes / (ms * 1e-3), "nodes/s", steps, warmup, ms,
+               {"workload": "two-drafter " + ("rescore + graft (257 strong rows per tree, W=60, "
+                                              "m=10)" if rescore else
+                                              "expansion (64 leaves per tree, K=10, N=60)") +
+                            ", B8 trees of 256 nodes (5-step weak expansion pruned by Alg. 3), "
+                            "V=128256, fp32 logits",
+                "batch": TD_B, "vocab": TD_V, "rescore_flags": flags if rescore else None,
+                "input_copies": copies},
+               roof, "f32", **{"call_TB/s": nbytes / (ms * 1e-3) / 1e12, "bytes": nbytes,
+                               "nodes_per_call": nodes, "kernels": kernels_json(kern, steps)})
+    if cpu_s > 0:
+        # one more call on a fresh tree copy, input copy 0, kept for the check
+        last = n_trees - 1
+        call_out = trees[last]
+        th = call_out.to_host()                      # the tree before the call
+        call(last)
+        torch.cuda.synchronize()
+        got_tree = call_out.to_host()
+        got = (gf.cpu().numpy(), ng.cpu().numpy()) if rescore else (nx.cpu().numpy(),
+                                                                   nn.cpu().numpy())
+        lse_g = lse.cpu().numpy()
+        out["cpu_baseline"], out["parity"] = tree_cpu_baseline(
+            rescore, th, logits[0], front.cpu().numpy(), got, got_tree, lse_g, cpu_s, nbytes)
+    return out
+
+
+def tree_cpu_baseline(rescore, th, logits_dev, front, got, got_tree, lse_g, budget_s, nbytes):
+    """The oracle on whole trees of the same call (input copy 0) until about
+    `budget_s` seconds are spent.  Parity on those trees: the oracle re-run
+    with the GPU's row log-sum-exps gives every integer output and score bit
+    for bit (the split check), the free oracle's selection is compared where
+    its boundary gap exceeds twice the score discrepancy, and the gap, the
+    discrepancy and the largest lse difference are reported."""
+    from oracle import tree as OT
+    done, t_cpu = 0, 0.0
+    exact, free_ok, checked_free = True, True, 0
+    min_gap, max_disc, max_dlse = float("inf"), 0.0, 0.0
+    for b in range(TD_B):
+        t1 = OT.Tree(*(th[f][b:b + 1] for f in ("parent", "token", "depth", "logp", "cum",
+                                                 "visited", "root_visited", "n_nodes")),
+                     cap=th["parent"].shape[1])
+        lg = logits_dev[b:b + 1].cpu().numpy()
+        t0 = time.perf_counter()
+        if rescore:
+            free, lse_f, sel_f, nsel_f, _ = OT.rescore_graft(t1, lg, TD_W, TD_M)
+        else:
+            free, lse_f, sel_f, nsel_f, _ = OT.expand(t1, lg, front[b:b + 1], None, TD_K, TD_N)
+        t_cpu += time.perf_counter() - t0
+        lse_b = np.nan_to_num(lse_g[b:b + 1], nan=0.0)
+        if rescore:
+            want, _, sel_o, nsel_o, _ = OT.rescore_graft(t1, lg, TD_W, TD_M, lse_override=lse_b)
+        else:
+            want, _, sel_o, nsel_o, _ = OT.expand(t1, lg, front[b:b + 1], None, TD_K, TD_N,
+                                                 lse_override=lse_b)
+        n = int(want.n_nodes[0])
+        exact = exact and np.array_equal(got[0][b], sel_o[0]) and int(got[1][b]) == int(nsel_o[0])
+        for f in ("parent", "token", "depth"):
+            exact = exact and np.array_equal(got_tree[f][b, :n], getattr(want, f)[0, :n])
+        for f in ("logp", "cum"):
+            exact = exact and np.array_equal(got_tree[f][b, :n].view(np.uint32),
+                                             getattr(want, f)[0, :n].view(np.uint32))
+        live = ~np.isnan(lse_f[0])
+        max_dlse = max(max_dlse, float(np.abs(lse_f[0][live].astype(np.float64) -
+                                              lse_g[b][live].astype(np.float64)).max()))
+        # selection boundary of the free oracle
+        n0 = int(t1.n_nodes[0])
+        if rescore:
+            cand = [(-0.0, 0, -1)] + [OT.node_key(free.cum[0, u], free.depth[0, u], u)
+                                      for u in range(n0) if not t1.visited[0, u]]
+            disc = float(np.abs(free.cum[0, :n0].astype(np.float64) -
+                                got_tree["cum"][b, :n0].astype(np.float64)).max())
+        else:
+            cand = [OT.node_key(free.cum[0, u], free.depth[0, u], u) for u in range(n0, n)]
+            disc = float(np.abs(free.cum[0, n0:n].astype(np.float64) -
+                                got_tree["cum"][b, n0:n].astype(np.float64)).max())
+        cand.sort()
+        k = int(nsel_f[0])
+        gap = abs(cand[k][0] - cand[k - 1][0]) if 0 < k < len(cand) else float("inf")
+        min_gap, max_disc = min(min_gap, gap), max(max_disc, disc)   # inf: nothing rejected
+        if gap > 2 * disc:
+            checked_free += 1
+            free_ok = free_ok and np.array_equal(sel_f[0], got[0][b])
+        done += 1
+        if t_cpu >= budget_s:
+            break
+    cpu = {"value": nbytes * done / TD_B / t_cpu / 1e9, "unit": "GB/s", "cores": blas_threads(),
+           "kind": "oracle",
+           "sample": f"{done} of {TD_B} trees of the same call in {t_cpu:.1f} s (NumPy; full "
+                     f"sorts), logits bytes per second"}
+    parity = {"trees_checked": done, "exact_with_gpu_lse": bool(exact),
+              "free_oracle_selection_equal": bool(free_ok), "free_checked_trees": checked_free,
+              "min_selection_gap": min_gap if np.isfinite(min_gap) else None,
+              "max_score_discrepancy": max_disc,
+              "max_lse_abs_diff": max_dlse}
+    return cpu, parity
+
+
+# -------------------------------------------------------------- the turn
+# (Llama-3-8B-shaped TreeGraft turn)
+V, W_FR, M_CH = 128256, 10, 8
+SCHEDULE = (1, 0, 1, 0, 1)
+B, HQ, HKV, D, L, N_VER = 1, 32, 8, 128, 2048, 64     # N_VER = B_ver pruned nodes
+CAP = 512
+MAX_DEPTH = 8            # accept path width (the turn's trees are at most 5 deep)
+R_ROWS = 313             # strong-logits rows (root + up to 312 nodes)
+NG_NMAX = 4              # n-gram drafter: longest n-gram matched
+
 
 def make_inputs(c, dev):
     """Input copy c (seed 1002 + 100 * c): the workload's tensors on the GPU."""
@@ -182,12 +790,11 @@ class Step:
         self.tg, self.inp = tg, inp
         i32 = dict(dtype=torch.int32, device=dev)
         self.tree = tg.TreeState(B, CAP, dev)
-        # zero-filled once (the library's row counters start at zero)
-        self.ws_r = torch.zeros(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
+        self.ws_r = torch.empty(tg.rescore_graft_workspace(B, R_ROWS, V, W_FR, M_CH, CAP),
                                 dtype=torch.uint8, device=dev)
         # n-gram drafter: the prefill cache (built once, untimed)
         self.clen = torch.full((B,), L, **i32)
-        ws_c = torch.zeros(tg.ngram_cache_workspace(B, L, V, M_CH), dtype=torch.uint8,
+        ws_c = torch.empty(tg.ngram_cache_workspace(B, L, V, M_CH), dtype=torch.uint8,
                            device=dev)
         self.c_tok, self.c_lp, self.c_fb = tg.ngram_cache(inp["prefill"], inp["ctx"], self.clen,
                                                           M_CH, workspace=ws_c)
@@ -200,7 +807,7 @@ class Step:
         self.margin = [torch.empty((B,), dtype=torch.float32, device=dev) for _ in SCHEDULE]
         self.action = [torch.empty((B,), **i32) for _ in SCHEDULE]
         nv = tg.verify_attention_workspace(B, N_VER, HQ, HKV, D, L + N_VER, tg.BF16)
-        self.ws_v = torch.zeros(max(nv, 1), dtype=torch.uint8, device=dev)
+        self.ws_v = torch.empty(max(nv, 1), dtype=torch.uint8, device=dev)
         self.r_lse = [torch.empty((B, R_ROWS), dtype=torch.float32, device=dev) for _ in range(3)]
         self.gf = [torch.empty((B, W_FR), **i32) for _ in range(3)]
         self.ng = [torch.empty((B,), **i32) for _ in range(3)]
@@ -252,8 +859,6 @@ class Step:
                       new_prefix_len=self.new_plen)
 
 
-# ------------------------------------------------------------ accounting
-
 def rows_read_per_step():
     """Middle-drafter logits rows one turn reads (structural: independent of
     the values).  k=1 pool {root}: row 0.  k=3 pool = 72 unvisited nodes:
@@ -270,21 +875,8 @@ def ngram_bytes_per_step():
     return sum(L * 4 + f * M_CH * 8 for f in (8, 10))
 
 
-def path_len_sum(vpar):
-    """Sum over nodes of the number of tree keys a node attends to (its
-    ancestors and itself)."""
-    tot = 0
-    for i in range(len(vpar)):
-        u = i
-        while u != -1:
-            tot += 1
-            u = int(vpar[u])
-    return tot
-
-
 def verify_work(vpar):
-    """Algorithmic bytes and flops of one verify call (each K/V element read
-    once, Q read, O written; flops over ancestor-or-self keys only)."""
+    """Algorithmic bytes and flops of the turn's verify call."""
     kv = 2 * B * HKV * (L + N_VER) * D * 2
     qo = 2 * B * N_VER * HQ * D * 2
     keys = N_VER * L + path_len_sum(vpar)
@@ -292,20 +884,13 @@ def verify_work(vpar):
     return kv + qo + vpar.nbytes, flops
 
 
-# -------------------------------------------------------------- cpu leg
-
-def cpu_baseline(inp, greedy0, budget_s):
+def turn_cpu_baseline(inp, greedy0, budget_s):
     """The oracle (the tests' CPU reference, untuned) running the same turn on
     input copy 0 until about `budget_s` seconds have been spent."""
     from oracle import attention as OA
-    from oracle import tree as OT
-    try:
-        from threadpoolctl import threadpool_info
-        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        blas = 1
     from oracle import ngram as NG
     from oracle import signals as OS
+    from oracle import tree as OT
     strong = inp["strong"].cpu().numpy()
     ctx = inp["ctx"].cpu().numpy()
     clen = np.array([L], np.int32)
@@ -340,210 +925,130 @@ def cpu_baseline(inp, greedy0, budget_s):
         turns += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
-            return turns, el, blas
+            return turns, el
 
 
-# ------------------------------------------------------- attention alone
-
-ATTN_SHAPES = {
-    # name: (B, Hq, Hkv, D, prefix, nodes, levels, qkv scale)
-    "attn-llama8b": (1, 32, 8, 128, 2048, 64, None, 1.0 / np.sqrt(128.0)),
-    "attn-longctx": (4, 32, 8, 128, 8192, 128, 10, 1.0),
-    "attn-llama70b": (8, 64, 8, 128, 32768, 256, 12, 1.0),
-}
-
-
-def attention_bench(args, tg, torch, dev):
-    """tg_tree_verify_attention alone at one workload shape; inputs rotate over
-    enough copies to exceed 512 MB so no timed read hits the MALL."""
-    import workloads as W
-    Bq, Hq, Hkv, Dh, Lp, Nn, levels, scale = ATTN_SHAPES[args.workload]
-    g = W.rng(2000)
-    if levels is None:
-        par = np.stack([W.verify_layout_with_root(W.expansion_shaped_tree(g, Nn - 1, 6, 8, 10))
-                        for _ in range(Bq)])
-    else:
-        par = np.stack([W.level_tree(g, Nn, levels, 8) for _ in range(Bq)])
-    S = Lp + Nn
-    per_copy = 2 * Bq * Hkv * S * Dh * 2
-    copies = max(1, min(8, -(-(512 << 20) // per_copy)))
-    bufs = []
-    for c in range(copies):
-        gc = W.rng([2000, c])
-        q = torch.empty((Bq, Nn, Hq, Dh), dtype=torch.bfloat16, device=dev)
-        k = torch.empty((Bq, Hkv, S, Dh), dtype=torch.bfloat16, device=dev)
-        v = torch.empty((Bq, Hkv, S, Dh), dtype=torch.bfloat16, device=dev)
-        for b in range(Bq):
-            q[b] = torch.from_numpy(W.normal(gc, (Nn, Hq, Dh)) * np.float32(scale)).to(dev)
-            k[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
-            v[b] = torch.from_numpy(W.normal(gc, (Hkv, S, Dh)) * np.float32(scale)).to(dev)
-        bufs.append((q, k, v, torch.empty_like(q)))
-    parent = torch.from_numpy(par.astype(np.int32)).to(dev)
-    plen = torch.full((Bq,), Lp, dtype=torch.int32, device=dev)
-    nws = tg.verify_attention_workspace(Bq, Nn, Hq, Hkv, Dh, S, tg.BF16)
-    ws = torch.zeros(max(nws, 1), dtype=torch.uint8, device=dev)
-
-    def call(i):
-        q, k, v, o = bufs[i % copies]
-        tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
-
-    for i in range(args.warmup):
-        call(i)
+def turn_bench(tg, torch, dev, steps, warmup, copies, cpu_s):
+    """One TreeGraft turn per step, replayed as one captured HIP graph per
+    input copy (inputs rotate over `copies` resident copies, > the MALL)."""
+    inputs = [make_inputs(c, dev) for c in range(copies)]
+    steps_ = [Step(tg, inputs[c], dev) for c in range(copies)]
     torch.cuda.synchronize()
-    tg.trace_begin(4 * (args.steps + 1))
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(args.steps):
-        call(i)
-    e1.record()
+    # set-up (untimed): every copy's turn once; the structural guard, and the
+    # synthetic target's greedy tokens for the pruned tree each copy builds
+    pruned = []
+    n_nodes = 8 + 64 + 80 + 80 + 80
+    for st in steps_:
+        st.run()
+        torch.cuda.synchronize()
+        assert int(st.tree.n_nodes[0].item()) == n_nodes
+        assert int(st.pr["n_keep"][0].item()) == N_VER
+        par = st.pr["vparent"][0].cpu().numpy()
+        tok = st.pr["vtoken"][0].cpu().numpy()
+        st.greedy.copy_(torch.from_numpy(greedy_for((par, tok))[None]))
+        pruned.append((par, tok))
     torch.cuda.synchronize()
-    recs = tg.trace_end()
-    ms = e0.elapsed_time(e1) / args.steps
-    kern = {}
-    for name, t in recs:
-        d = kern.setdefault(name, [0, 0.0])
-        d[0] += 1
-        d[1] += t
-    main_k = next(k for k in ATTN_MAIN if k in kern)
-    main_us = 1e3 * kern[main_k][1] / kern[main_k][0]
-    keys = sum(Nn * Lp + path_len_sum(par[b]) for b in range(Bq))
-    flops = 4 * Dh * Hq * keys
-    nbytes = 2 * Bq * Hkv * S * Dh * 2 + 2 * Bq * Nn * Hq * Dh * 2 + par.nbytes
-    ridge = PEAK_BF16 / PEAK_HBM
-    bound = "mfma" if flops / nbytes > ridge else "hbm"
-    call_s = ms * 1e-3
-    if bound == "mfma":
-        ach, peak, unit = flops / (main_us * 1e-6) / 1e12, PEAK_BF16 / 1e12, "TFLOP/s"
-    else:
-        ach, peak, unit = nbytes / (main_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s"
-    out = {
-        "metric": METRIC, "value": (flops if bound == "mfma" else nbytes) / call_s / 1e12,
-        "unit": "TFLOP/s" if bound == "mfma" else "TB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": args.workload, "batch": Bq, "q_heads": Hq, "kv_heads": Hkv,
-                   "head_dim": Dh, "prefix": Lp, "tree_nodes": Nn, "input_copies": copies},
-        "roofline": {"bound": bound, "kernel": main_k, "achieved": ach, "peak": peak,
-                     "unit": unit, "frac": ach / peak,
-                     "traffic": profile_traffic("attn_pingpong_llama70b_traffic.md")
-                     if args.workload == "attn-llama70b" and main_k == "attn_pingpong" else None,
-                     "avg_launch_us": main_us},
-        "TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
-        "bytes": nbytes, "flops": flops,
-        "kernels": {k: {"launches_per_call": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0]}
-                    for k, v in kern.items()},
-    }
-    print(json.dumps(out), flush=True)
-
-
-# --------------------------------------------------- tree calls alone
-
-def tree_bench(args, tg, torch, dev):
-    """Two-drafter shapes: expand of 64 frontier rows per tree (K=10, N=60)
-    or a middle step over 256-node trees (257 strong rows, W=60, m=10), B=8,
-    vocabulary 128256, logits N(0,3).  The trees are grown on the GPU from the
-    root (16 children, then 15 under each: 256 nodes in two levels) with the
-    library's own expansion; inputs rotate over copies beyond 512 MB."""
-    import workloads as W
-    Bt, Vv, K, Nn, Wd, Mm, F, R = 8, 128256, 10, 60, 60, 10, 64, 257
-    rescore = args.workload == "rescore-twodrafter"
-    rows = R if rescore else F
-    per_copy = Bt * rows * Vv * 4
-    copies = max(1, min(8, -(-(512 << 20) // per_copy)))
-    g = W.rng(3000)
-    logits = []
-    for c in range(copies):
-        t = torch.empty((Bt, rows, Vv), dtype=torch.float32, device=dev)
-        for b in range(Bt):
-            t[b] = torch.from_numpy(W.normal(g, (rows, Vv), 3.0)).to(dev)
-        logits.append(t)
-    grow = torch.from_numpy(W.normal(g, (Bt, 16, Vv), 3.0)).to(dev)
-
-    def base_tree():
-        ts = tg.TreeState(Bt, 1024, dev)
-        fr = torch.full((Bt, 16), -1, dtype=torch.int32, device=dev)
-        one = torch.ones(Bt, dtype=torch.int32, device=dev)
-        _, nx, nn = tg.expand_topk(ts, grow[:, :1].contiguous(), fr[:, :1].contiguous(), one,
-                                   16, 16)
-        tg.expand_topk(ts, grow, nx, nn, 15, 16)
-        return ts
-
-    template = base_tree()
+    graphs, timing = [], "eager launches"
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for st in steps_:
+            st.run()
+    torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
-    assert int(template.n_nodes[0].item()) == 256
-    # per-iteration fresh copies of the tree (the calls append to it)
-    trees = [tg.TreeState(Bt, 1024, dev) for _ in range(args.steps + args.warmup)]
-    for ts in trees:
-        for f in tg.TreeState.FIELDS:
-            getattr(ts, f).copy_(getattr(template, f))
-    fr = torch.arange(192, 256, dtype=torch.int32, device=dev).repeat(Bt, 1).contiguous()
-    if rescore:
-        ws = torch.zeros(tg.rescore_graft_workspace(Bt, R, Vv, Wd, Mm, 1024), dtype=torch.uint8,
-                         device=dev)
-        lse = torch.empty((Bt, R), dtype=torch.float32, device=dev)
-        gf = torch.empty((Bt, Wd), dtype=torch.int32, device=dev)
-        ng = torch.empty((Bt,), dtype=torch.int32, device=dev)
-        flags = args.rescore_flags
-        # w/o EG: the pool is the template's last expansion (ids 16..255)
-        new_from = torch.full((Bt,), 16, dtype=torch.int32, device=dev) if flags & 1 else None
-        call = lambda i: tg.rescore_graft(trees[i], logits[i % copies], Wd, Mm, row_lse=lse,
-                                          graft_frontier=gf, n_graft=ng, workspace=ws,
-                                          flags=flags, new_from=new_from)
-        # rows read: the pool's own rows and its parents' (w/o EG: nodes 16..255 and
-        # their parents 0..15, the root row is not read)
-        nbytes = Bt * (R - 1 if flags & 1 else R) * Vv * 4
-        # pool nodes rescored (root included) + graft slots
-        nodes = Bt * ((240 if flags & 1 else 257) + Wd * Mm)
-    else:
-        ws = torch.zeros(tg.expand_topk_workspace(Bt, F, Vv, K, Nn), dtype=torch.uint8,
-                         device=dev)
-        lse = torch.empty((Bt, F), dtype=torch.float32, device=dev)
-        nx = torch.empty((Bt, Nn), dtype=torch.int32, device=dev)
-        nn = torch.empty((Bt,), dtype=torch.int32, device=dev)
-        call = lambda i: tg.expand_topk(trees[i], logits[i % copies], fr, None, K, Nn,
-                                        row_lse=lse, next_frontier=nx, n_next=nn, workspace=ws)
-        nbytes = Bt * F * Vv * 4
-        nodes = Bt * F * K
-    for i in range(args.warmup):
-        call(i)
-    torch.cuda.synchronize()
-    tg.trace_begin(8 * (args.steps + 1))
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(args.warmup, args.warmup + args.steps):
-        call(i)
-    e1.record()
-    torch.cuda.synchronize()
-    recs = tg.trace_end()
-    ms = e0.elapsed_time(e1) / args.steps
-    kern = {}
-    for name, t in recs:
-        d = kern.setdefault(name, [0, 0.0])
-        d[0] += 1
-        d[1] += t
-    row_us = 1e3 * kern["row_partial"][1] / kern["row_partial"][0]
-    ach = nbytes / (row_us * 1e-6)
-    out = {
-        "metric": METRIC, "value": nodes / (ms * 1e-3), "unit": "nodes/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp32",
-        "data": "synthetic",
-        "config": {"workload": args.workload, "batch": Bt, "vocab": Vv, "rows_per_tree": rows,
-                   "K_or_m": Mm if rescore else K, "input_copies": copies,
-                   "rescore_flags": args.rescore_flags if rescore else None},
-        "roofline": {"bound": "hbm", "kernel": "row_partial", "achieved": ach / 1e9,
-                     "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": ach / PEAK_HBM,
-                     "traffic": None if rescore else
-                     profile_traffic("row_partial_expand_twodrafter_traffic.md"),
-                     "avg_launch_us": row_us},
-        "call_TB/s": nbytes / (ms * 1e-3) / 1e12,
-        "kernels": {k: {"launches_per_call": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0]}
-                    for k, v in kern.items()},
-    }
-    print(json.dumps(out), flush=True)
+    try:
+        for st in steps_:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                st.run()
+            graphs.append(g)
+        torch.cuda.synchronize()
+        timing = "one captured HIP graph per step"
+    except Exception as exc:  # report and time eager launches instead
+        print(f"bench.py: graph capture failed ({exc}); timing eager launches", file=sys.stderr)
+        graphs = []
+    if graphs:        # replaying a graph must reproduce the eager turn
+        graphs[0].replay()
+        torch.cuda.synchronize()
+        assert int(steps_[0].tree.n_nodes[0].item()) == n_nodes
+
+    def run(i):
+        if graphs:
+            graphs[i % len(graphs)].replay()
+        else:
+            steps_[i % len(steps_)].run()
+
+    ms_step = time_calls(torch, run, steps, warmup)
+    eager = lambda i: steps_[i % len(steps_)].run()
+    ms_eager = time_calls(torch, eager, steps, warmup)
+    kern, recs = kernel_times(tg, torch, eager, steps)
+    kernels = kernels_json(kern, steps)
+    per_step = len(recs) // steps
+    timeline = [[name, round(1e3 * ms, 2)] for name, ms in recs[-per_step:]]
+    rows_r = rows_read_per_step()
+    row_bytes = V * 4
+    works = [verify_work(par) for par, _ in pruned]
+    v_bytes = sum(w[0] for w in works) / len(works)
+    v_flops = sum(w[1] for w in works) / len(works)
+    step_bytes = sum(rows_r) * row_bytes + ngram_bytes_per_step() + v_bytes
+    rescored = 72 + 160                       # non-root pool nodes rescored
+    slowest = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    dom = "row_partial"
+    dom_bytes = sum(rows_r) * row_bytes
+    launches = kern[dom][0]
+    achieved = dom_bytes * steps / (kern[dom][1] * 1e-3)
+    roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+            "unit": "GB/s", "frac": achieved / PEAK_HBM,
+            "traffic": traffic_for("turn", dom),
+            "bytes_per_launch": dom_bytes * steps / launches,
+            "avg_launch_us": 1e3 * kern[dom][1] / launches,
+            "launch_time_from": "trace pass (event pair around each kernel)"}
+    attn_us = sum(kernels[k]["us_per_step"] for k in ATTN_MAIN + ("attn_combine",) if k in kernels)
+    out = line(step_bytes / (ms_step * 1e-3) / 1e12, "TB/s", steps, warmup, ms_step,
+               {"workload": "TreeGraft turn (schedule 1,0,1,0,1) + Llama-3-8B-shaped verify "
+                            "layer", "batch": B, "vocab": V, "frontier_W": W_FR,
+                "children_m": M_CH, "q_heads": HQ, "kv_heads": HKV, "head_dim": D, "prefix": L,
+                "verify_nodes": N_VER, "input_copies": copies,
+                "small_drafter": f"n-gram (cache m = {M_CH}, n_max = {NG_NMAX})",
+                "scheduler": "signals + margin predictor every step, fixed schedule",
+                "timing": timing},
+               roof, "fp32+bf16",
+               **{"largest_kernel": {"name": slowest,
+                                     "us_per_step": kernels[slowest]["us_per_step"]},
+                  "draft_nodes_per_s": (n_nodes + rescored) / (ms_step * 1e-3),
+                  "verify_attention": {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
+                                       "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
+                                       "frac_hbm": v_bytes / (attn_us * 1e-6) / PEAK_HBM},
+                  "step_bytes": step_bytes, "eager_ms_per_step": ms_eager,
+                  "kernels": kernels, "step_timeline_us": timeline})
+    if cpu_s > 0:
+        turns, el = turn_cpu_baseline(inputs[0], steps_[0].greedy.cpu().numpy(), cpu_s)
+        out["cpu_baseline"] = {"value": step_bytes * turns / el / 1e12, "unit": "TB/s",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"{turns} full turns of the same workload on input "
+                                         f"copy 0 in {el:.1f} s (tree steps single-threaded "
+                                         f"NumPy; attention matmuls on the BLAS threads; the "
+                                         f"n-gram prefill cache built untimed first)"}
+    return out
 
 
 # ------------------------------------------------------------------ main
+
+def run_workload(name, args, tg, torch, dev, steps, warmup, cpu_s, shared):
+    if name.startswith("attn-llama8b-x32"):
+        return attention_layers_bench(tg, torch, dev, steps, warmup, cpu_s)
+    if name.startswith("attn-"):
+        return attention_bench(tg, torch, dev, name, steps, warmup, cpu_s)
+    if name == "tiny":
+        return tiny_bench(tg, torch, dev, steps, warmup, cpu_s)
+    if name.endswith("-twodrafter"):
+        if "td" not in shared:
+            shared["td"] = twodrafter_trees(tg, torch, dev)
+        return tree_bench(tg, torch, dev, name, steps, warmup, cpu_s,
+                          flags=args.rescore_flags if name.startswith("rescore") else 0,
+                          shared=shared["td"])
+    return turn_bench(tg, torch, dev, steps, warmup, args.copies, cpu_s)
+
 
 def main():
     args = parse()
@@ -565,166 +1070,23 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.workload.startswith("attn-"):
-        attention_bench(args, tg, torch, dev)
-        return
-    if args.workload.endswith("-twodrafter"):
-        tree_bench(args, tg, torch, dev)
-        return
-
-    inputs = [make_inputs(c, dev) for c in range(args.copies)]
-    steps = [Step(tg, inputs[c], dev) for c in range(args.copies)]
-    torch.cuda.synchronize()
-
-    # set-up (untimed): every copy's turn once; the structural guard, and the
-    # synthetic target's greedy tokens for the pruned tree each copy builds
-    pruned = []
-    for st in steps:
-        st.run()
-        torch.cuda.synchronize()
-        n_nodes = int(st.tree.n_nodes[0].item())
-        assert n_nodes == 8 + 64 + 80 + 80 + 80, n_nodes
-        assert int(st.pr["n_keep"][0].item()) == N_VER
-        par = st.pr["vparent"][0].cpu().numpy()
-        tok = st.pr["vtoken"][0].cpu().numpy()
-        st.greedy.copy_(torch.from_numpy(greedy_for((par, tok))[None]))
-        pruned.append((par, tok))
-    torch.cuda.synchronize()
-    trees = dict(host=dict(pruned=pruned))
-
-    # ---- graph capture: one graph per input copy
-    graphs = []
-    timing = "eager launches"
-    if not args.no_graph:
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            for st in steps:
-                st.run()
-        torch.cuda.current_stream().wait_stream(s)
-        torch.cuda.synchronize()
-        try:
-            for st in steps:
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g):
-                    st.run()
-                graphs.append(g)
-            torch.cuda.synchronize()
-            timing = "one captured HIP graph per step"
-        except Exception as exc:  # report and time eager launches instead
-            print(f"bench.py: graph capture failed ({exc}); timing eager launches",
-                  file=sys.stderr)
-            graphs = []
-        # replaying a graph must reproduce the eager turn
-        if graphs:
-            graphs[0].replay()
-            torch.cuda.synchronize()
-            assert int(steps[0].tree.n_nodes[0].item()) == n_nodes
-
-    def run_steps(n, graph=True):
-        for i in range(n):
-            if graph and graphs:
-                graphs[i % len(graphs)].replay()
-            else:
-                steps[i % len(steps)].run()
-
-    # ---- warmup + timed region (graph replay)
-    run_steps(args.warmup, graph=True)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    run_steps(args.steps, graph=True)
-    e1.record()
-    torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
-
-    # ---- eager pass with per-kernel trace events (same steps)
-    run_steps(args.warmup, graph=False)
-    torch.cuda.synchronize()
-    tg.trace_begin(64 * (args.steps + 1))
-    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e2.record()
-    run_steps(args.steps, graph=False)
-    e3.record()
-    torch.cuda.synchronize()
-    recs = tg.trace_end()
-    ms_eager = e2.elapsed_time(e3) / args.steps
-    kern = {}
-    for name, ms in recs:
-        d = kern.setdefault(name, [0, 0.0])
-        d[0] += 1
-        d[1] += ms
-    kernels = {k: {"launches_per_step": v[0] / args.steps, "avg_us": 1e3 * v[1] / v[0],
-                   "us_per_step": 1e3 * v[1] / args.steps} for k, v in kern.items()}
-    per_step = len(recs) // args.steps
-    timeline = [[name, round(1e3 * ms, 2)] for name, ms in recs[-per_step:]]
-
-    # ---- accounting
-    rows_r = rows_read_per_step()
-    row_bytes = V * 4
-    works = [verify_work(par) for par, _ in trees["host"]["pruned"]]
-    v_bytes = sum(w[0] for w in works) / len(works)
-    v_flops = sum(w[1] for w in works) / len(works)
-    step_bytes = sum(rows_r) * row_bytes + ngram_bytes_per_step() + v_bytes
-    nodes = 8 + 64 + 80 + 80 + 80            # created per turn
-    rescored = 72 + 160                       # non-root pool nodes rescored
-    value = step_bytes / (ms_step * 1e-3) / 1e12
-
-    # roofline of the turn's bandwidth kernel: row_partial streams every
-    # logits row the turn reads (the other kernels are single-workgroup,
-    # latency-bound tree phases with a few KB of traffic; the largest of all
-    # by time is reported beside it)
-    slowest = max(kernels, key=lambda k: kernels[k]["us_per_step"])
-    dom = "row_partial"
-    if dom in kernels:
-        dom_bytes = sum(rows_r) * row_bytes
-        launches = kern[dom][0]
-        achieved = dom_bytes * args.steps / (kern[dom][1] * 1e-3)
-        roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": achieved / PEAK_HBM,
-                "traffic": profile_traffic("row_partial_turn_llama8b_traffic.md"),
-                "bytes_per_launch": dom_bytes * args.steps / launches,
-                "avg_launch_us": 1e3 * kern[dom][1] / launches}
-    else:
-        roof = {"bound": "hbm", "kernel": dom, "achieved": None, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": None, "traffic": None, "avg_launch_us": None}
-    attn_us = sum(kernels[k]["us_per_step"] for k in ATTN_MAIN + ("attn_combine",) if k in kernels)
-    verify = {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
-              "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
-              "frac_hbm": v_bytes / (attn_us * 1e-6) / PEAK_HBM,
-              "frac_mfma": v_flops / (attn_us * 1e-6) / PEAK_BF16,
-              "bytes": v_bytes, "flops": v_flops}
-
-    out = {
-        "metric": METRIC, "value": value, "unit": "TB/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp32+bf16", "data": "synthetic",
-        "config": {"workload": "TreeGraft turn (schedule 1,0,1,0,1) + Llama-3-8B-shaped "
-                               "verify layer", "batch": B, "vocab": V, "frontier_W": W_FR,
-                   "children_m": M_CH, "q_heads": HQ, "kv_heads": HKV, "head_dim": D,
-                   "prefix": L, "verify_nodes": N_VER, "input_copies": args.copies,
-                   "small_drafter": f"n-gram (cache m = {M_CH}, n_max = {NG_NMAX})",
-                   "scheduler": "signals + margin predictor every step, fixed schedule",
-                   "timing": timing},
-        "roofline": roof,
-        "largest_kernel": {"name": slowest, "us_per_step": kernels[slowest]["us_per_step"]},
-        "draft_nodes_per_s": (nodes + rescored) / (ms_step * 1e-3),
-        "verify_attention": verify,
-        "step_bytes": step_bytes,
-        "eager_ms_per_step": ms_eager,
-        "kernels": kernels,
-        "step_timeline_us": timeline,
-    }
-    if not args.no_cpu_baseline:
-        turns, el, blas = cpu_baseline(inputs[0], steps[0].greedy.cpu().numpy(),
-                                       args.cpu_seconds)
-        out["cpu_baseline"] = {"value": step_bytes * turns / el / 1e12, "unit": "TB/s",
-                               "cores": blas, "kind": "oracle",
-                               "sample": f"{turns} full turns of the same workload on input "
-                                         f"copy 0 in {el:.1f} s (tree steps single-threaded "
-                                         f"NumPy; attention matmuls on {blas} BLAS threads; "
-                                         f"the n-gram prefill cache built untimed first)"}
+    cpu_main = 0.0 if args.no_cpu_baseline else args.cpu_seconds
+    cpu_extra = 0.0 if args.no_cpu_baseline else args.extra_cpu_seconds
+    shared = {}
+    print(f"bench.py: {args.workload} ...", file=sys.stderr, flush=True)
+    out = run_workload(args.workload, args, tg, torch, dev, args.steps, args.warmup, cpu_main,
+                       shared)
+    if not args.only:
+        extra = {}
+        for name in WORKLOADS:
+            if name == args.workload:
+                continue
+            print(f"bench.py: {name} ...", file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
+            extra[name] = run_workload(name, args, tg, torch, dev, max(5, args.steps),
+                                       max(2, args.warmup), cpu_extra, shared)
+            shared.pop("td", None) if name == "rescore-twodrafter" else None
+        out["extra"] = extra
     print(json.dumps(out), flush=True)
 
 
