@@ -442,14 +442,18 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr int LOADS = BN * D * 2 / 16 / NT;  // 16-byte loads per thread per tile
-  // two stages each of K and V (distinct objects, so the compiler knows a
-  // read of one stage does not alias loads in flight into another)
+  // three stages each of K and V (distinct objects, so the compiler knows a
+  // read of one stage does not alias loads in flight into another): tiles
+  // are requested two tiles ahead of their use
   __shared__ __attribute__((aligned(16))) __bf16 kst0[Lds::TILE];
   __shared__ __attribute__((aligned(16))) __bf16 kst1[Lds::TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 kst2[Lds::TILE];
   __shared__ __attribute__((aligned(16))) __bf16 vst0[Lds::TILE];
   __shared__ __attribute__((aligned(16))) __bf16 vst1[Lds::TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 vst2[Lds::TILE];
   extern __shared__ __attribute__((aligned(16))) uint32_t anc_s[];
-  int *par_s = reinterpret_cast<int *>(kst0);  // prologue only (N ints fit a tile)
+  // prologue only (N ints fit a tile); no tile is loaded into it before the loop
+  int *par_s = reinterpret_cast<int *>(vst2);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
@@ -487,6 +491,52 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
     return;
   }
+
+  // key tiles: the prefix's, then the tree's, dealt out as equal runs
+  const int n_pt = (L + BN - 1) / BN;
+  const int n_vt = n_pt + (N + BN - 1) / BN;
+  const int per_split = (n_vt + n_splits - 1) / n_splits;
+  const int vt0 = min(n_vt, split * per_split);
+  const int n = min(n_vt, vt0 + per_split) - vt0;
+
+  const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
+  const __bf16 *kb = kc + kv_base;
+  const __bf16 *vb = vc + kv_base;
+
+  auto tree_tile_at = [&](int t) { return vt0 + t >= n_pt; };
+  auto tile_k0 = [&](int t) { return tree_tile_at(t) ? L + (vt0 + t - n_pt) * BN : (vt0 + t) * BN; };
+  auto tile_lim = [&](int t) { return tree_tile_at(t) ? L + N : L; };
+  constexpr int RPI = 64 / Lds::CPR;
+  // offsets recomputed per issue (a few VALU ops) rather than held in registers
+  auto issue = [&](const __bf16 *src, int t, __bf16 *dst) __attribute__((always_inline)) {
+    const int k0 = tile_k0(t), lim = tile_lim(t);
+    const __bf16 *st = src + (size_t)k0 * D;
+    int goff[LOADS], grow[LOADS];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int row = (w * LOADS + i) * RPI + lane / Lds::CPR;
+      grow[i] = row;
+      goff[i] = row * D + (((lane % Lds::CPR) ^ Lds::swz(row)) & Lds::CM) * 8;
+    }
+    auto one = [&](int i, int off) {
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void *)(st + off),
+          (__attribute__((address_space(3))) void *)(dst + (w * LOADS + i) * 512), 16, 0, 0);
+    };
+    if (k0 + BN <= lim) {
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) one(i, goff[i]);
+    } else {
+      // rows past the range re-read the last valid row (finite, masked later)
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) one(i, goff[i] - max(0, k0 + grow[i] - (lim - 1)) * D);
+    }
+  };
+
+  // the first tiles stream in while the prologue runs
+  if (n > 0) issue(kb, 0, kst0);
+  if (n > 1) issue(kb, 1, kst1);
+  if (n > 0) issue(vb, 0, vst0);
 
   // ---- ancestor-or-self bitsets of this tile's nodes (a1)
   const int node_lo = row0 / G;
@@ -532,17 +582,6 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
   }
 
-  // key tiles: the prefix's, then the tree's, dealt out as equal runs
-  const int n_pt = (L + BN - 1) / BN;
-  const int n_vt = n_pt + (N + BN - 1) / BN;
-  const int per_split = (n_vt + n_splits - 1) / n_splits;
-  const int vt0 = min(n_vt, split * per_split);
-  const int n = min(n_vt, vt0 + per_split) - vt0;
-
-  const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
-  const __bf16 *kb = kc + kv_base;
-  const __bf16 *vb = vc + kv_base;
-
   // Running row reference m (log2 units): the max of the row's first tile
   // with a visible key, then moved up only when a tile's scores exceed it by
   // more than kSlack, so the exponentials stay below 2^kSlack and the O / l
@@ -556,36 +595,6 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   float l = 0.0f;
   f32x16 acc[2];
   bf16x8 pb[2][2];
-
-  auto tree_tile_at = [&](int t) { return vt0 + t >= n_pt; };
-  auto tile_k0 = [&](int t) { return tree_tile_at(t) ? L + (vt0 + t - n_pt) * BN : (vt0 + t) * BN; };
-  auto tile_lim = [&](int t) { return tree_tile_at(t) ? L + N : L; };
-  constexpr int RPI = 64 / Lds::CPR;
-  // offsets recomputed per issue (a few VALU ops) rather than held in registers
-  auto issue = [&](const __bf16 *src, int t, __bf16 *dst) __attribute__((always_inline)) {
-    const int k0 = tile_k0(t), lim = tile_lim(t);
-    const __bf16 *st = src + (size_t)k0 * D;
-    int goff[LOADS], grow[LOADS];
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int row = (w * LOADS + i) * RPI + lane / Lds::CPR;
-      grow[i] = row;
-      goff[i] = row * D + (((lane % Lds::CPR) ^ Lds::swz(row)) & Lds::CM) * 8;
-    }
-    auto one = [&](int i, int off) {
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void *)(st + off),
-          (__attribute__((address_space(3))) void *)(dst + (w * LOADS + i) * 512), 16, 0, 0);
-    };
-    if (k0 + BN <= lim) {
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) one(i, goff[i]);
-    } else {
-      // rows past the range re-read the last valid row (finite, masked later)
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) one(i, goff[i] - max(0, k0 + grow[i] - (lim - 1)) * D);
-    }
-  };
 
   // Per-lane LDS element offsets of the fragment reads.  The swizzle only
   // looks at the low four row bits, so the row offset of a 16- or 32-key
@@ -679,60 +688,78 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
         }
       }
     }
-    float mx;
-    {
-      float t3[11];
+    // Fast path, no row maximum: every row keeps its reference m and the
+    // probabilities are taken against it.  It stands when, in every lane of
+    // the wave, the sum of the lane's 32 probabilities is at most
+    // 32 * 2^kSlack (so each is bounded; 32 of them at most 2^kSlack always
+    // pass) and no row without a reference has a visible key.  Otherwise
+    // the row maxima are taken and the rows whose maximum exceeds the
+    // reference by more than kSlack move it (the same decision for both
+    // lanes of a row).
+    auto probs = [&](float *ls) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < 10; ++i) {
-        const int a = 3 * i, bb = a + 1, c = a + 2;
-        t3[i] = __builtin_fmaxf(acc[a >> 4][a & 15],
-                                __builtin_fmaxf(acc[bb >> 4][bb & 15], acc[c >> 4][c & 15]));
+      for (int r = 0; r < 4; ++r) {
+        const float p0 = __builtin_amdgcn_exp2f(acc[0][r] - m);
+        const float p1 = __builtin_amdgcn_exp2f(acc[0][r + 4] - m);
+        pb[0][0][r] = (__bf16)p0;
+        pb[0][0][r + 4] = (__bf16)p1;
+        ls[r] = p0 + p1;
       }
-      t3[10] = __builtin_fmaxf(acc[1][14], acc[1][15]);
-      const float u0 = __builtin_fmaxf(t3[0], __builtin_fmaxf(t3[1], t3[2]));
-      const float u1 = __builtin_fmaxf(t3[3], __builtin_fmaxf(t3[4], t3[5]));
-      const float u2 = __builtin_fmaxf(t3[6], __builtin_fmaxf(t3[7], t3[8]));
-      const float u3 = __builtin_fmaxf(t3[9], t3[10]);
-      mx = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int r = blk ? 0 : 8; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
+          ls[r & 3] += p;
+          pb[blk][r >> 3][r & 7] = (__bf16)p;
+        }
+    };
+    float ls[4];
+    probs(ls);
+    float lsum = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    constexpr float kFastMax = 32.0f * (1 << (int)kSlack);
+    const bool fast = m_set ? lsum <= kFastMax : lsum == 0.0f;
+    if (!__all(fast)) {
+      float mx;
+      {
+        float t3[11];
+#pragma unroll
+        for (int i = 0; i < 10; ++i) {
+          const int a = 3 * i, bb = a + 1, c = a + 2;
+          t3[i] = __builtin_fmaxf(acc[a >> 4][a & 15],
+                                  __builtin_fmaxf(acc[bb >> 4][bb & 15], acc[c >> 4][c & 15]));
+        }
+        t3[10] = __builtin_fmaxf(acc[1][14], acc[1][15]);
+        const float u0 = __builtin_fmaxf(t3[0], __builtin_fmaxf(t3[1], t3[2]));
+        const float u1 = __builtin_fmaxf(t3[3], __builtin_fmaxf(t3[4], t3[5]));
+        const float u2 = __builtin_fmaxf(t3[6], __builtin_fmaxf(t3[7], t3[8]));
+        const float u3 = __builtin_fmaxf(t3[9], t3[10]);
+        mx = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
+      }
+      // max over the row's 64 keys, relative to the reference
+      mx = __builtin_fmaxf(mx, half_swap(mx)) - m;
+      const bool need = m_set ? mx > kSlack : mx != -__builtin_inff();
+      if (__any(need)) {
+        // set or move the reference of the rows that need it; every other
+        // row keeps its own, so a row's arithmetic never depends on its
+        // neighbours (its probabilities are recomputed to the same bits)
+        float shift = 0.0f, alpha = 1.0f;
+        if (need) {
+          shift = mx;
+          if (m_set) alpha = __builtin_amdgcn_exp2f(-mx);  // else o and l are still 0
+          m_set = true;
+        }
+        l *= alpha;
+#pragma unroll
+        for (int i = 0; i < DB; ++i) o[i] *= alpha;
+        m += shift;
+        probs(ls);
+        lsum = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      }
     }
-    // max over the row's 64 keys, relative to the reference
-    mx = __builtin_fmaxf(mx, half_swap(mx)) - m;
     // the normaliser sums the fp32 probabilities (plain adds: the bf16 dot
     // instruction would wait for the other wave's MFMAs)
-    float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    const bool need = m_set ? mx > kSlack : mx != -__builtin_inff();
-    if (__any(need)) {
-      // set or move the reference of the rows that need it; every other row
-      // keeps its own, so a row's arithmetic never depends on its neighbours
-      float shift = 0.0f, alpha = 1.0f;
-      if (need) {
-        shift = mx;
-        if (m_set) alpha = __builtin_amdgcn_exp2f(-mx);  // else o and l are still 0
-        m_set = true;
-      }
-      l *= alpha;
-#pragma unroll
-      for (int i = 0; i < DB; ++i) o[i] *= alpha;
-      m += shift;
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
-          ls[r & 3] += p;
-          pb[blk][r >> 3][r & 7] = (__bf16)p;
-        }
-    } else {
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
-          ls[r & 3] += p;
-          pb[blk][r >> 3][r & 7] = (__bf16)p;
-        }
-    }
-    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    l += lsum;
   };
 
   // phase barriers: the even ones leave loads in flight
@@ -741,35 +768,77 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  auto bar_odd = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
+  // the odd ones wait for this wave's loads of the next phase pair's tiles
+  // and for its LDS reads; `younger` loads (issued after those) may stay in
+  // flight.  s_waitcnt immediate: vmcnt in bits [3:0], expcnt [6:4] left at
+  // its maximum (no wait), lgkmcnt [11:8] = 0.
+  auto bar_odd = [&](int younger) __attribute__((always_inline)) {
+    if (younger >= 2 * LOADS)
+      __builtin_amdgcn_s_waitcnt((2 * LOADS) | (7 << 4));
+    else if (younger >= LOADS)
+      __builtin_amdgcn_s_waitcnt(LOADS | (7 << 4));
+    else
+      __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   };
 
-  if (n > 0) issue(kb, 0, kst0);
-  bar_odd();
-  // one pair of phases per j; stage parity is fixed per half of the unrolled loop
-  auto pair = [&](int j, __bf16 *kj, __bf16 *kj1, __bf16 *vj, __bf16 *vjm1)
+  bar_odd(0);
+  // One pair of phases per j (tile j's QK^T, tile j-1's PV).  Tile j's K sits
+  // in stage j % 3 and its V in stage j % 3; phase 2j requests K(j+2) and
+  // V(j+1), whose stages held K(j-1) and V(j-2), last read in phase 2j-1.
+  // The odd barrier of pair j needs K(j+1) and V(j) (requested in pair j-1):
+  // the two requests of pair j are younger and may stay in flight.
+  auto requests = [&](int j, __bf16 *kis, __bf16 *vis) __attribute__((always_inline)) {
+    const bool ld_k = j + 2 < n, ld_v = j + 1 < n;
+    if (ld_k) issue(kb, j + 2, kis);
+    if (ld_v) issue(vb, j + 1, vis);
+    return LOADS * ((int)ld_k + (int)ld_v);
+  };
+  // pairs 1 .. n-1 run both products
+  auto pair = [&](int j, __bf16 *kq, __bf16 *kis, __bf16 *vis, __bf16 *vp)
                   __attribute__((always_inline)) {
-    // phase 2j
-    if (j + 1 < n) issue(kb, j + 1, kj1);
-    if (j < n) issue(vb, j, vj);
+    const int younger = requests(j, kis, vis);
     if (lead)
-      mphase(j >= 1, vjm1, j < n, kj);
-    else if (j >= 1)
+      mphase(true, vp, true, kq);
+    else
       sphase(j - 1);
     bar_even();
-    // phase 2j+1
-    if (lead) {
-      if (j < n) sphase(j);
-    } else {
-      mphase(j >= 1, vjm1, j < n, kj);
-    }
-    bar_odd();
+    if (lead)
+      sphase(j);
+    else
+      mphase(true, vp, true, kq);
+    bar_odd(younger);
   };
-  for (int j = 0; j <= n; j += 2) {
-    pair(j, kst0, kst1, vst0, vst1);
-    if (j + 1 <= n) pair(j + 1, kst1, kst0, vst1, vst0);
+  if (n > 0) {
+    // pair 0: QK^T of tile 0 only
+    {
+      const int younger = requests(0, kst2, vst1);
+      if (lead) mphase(false, vst2, true, kst0);
+      bar_even();
+      if (lead)
+        sphase(0);
+      else
+        mphase(false, vst2, true, kst0);
+      bar_odd(younger);
+    }
+    int j = 1;
+    for (; j + 2 < n; j += 3) {
+      pair(j, kst1, kst0, vst2, vst0);
+      pair(j + 1, kst2, kst1, vst0, vst1);
+      pair(j + 2, kst0, kst2, vst1, vst2);
+    }
+    if (j < n) pair(j, kst1, kst0, vst2, vst0);
+    if (j + 1 < n) pair(j + 1, kst2, kst1, vst0, vst1);
+    // pair n: PV of tile n-1 only
+    const int r = (n - 1) % 3;
+    __bf16 *vlast = r == 0 ? vst0 : (r == 1 ? vst1 : vst2);
+    if (lead)
+      mphase(true, vlast, false, kst0);
+    else
+      sphase(n - 1);
+    bar_even();
+    if (!lead) mphase(true, vlast, false, kst0);
+    bar_odd(0);
   }
 
   // ---- finalize
