@@ -93,6 +93,7 @@ typedef enum { TG_F32 = 0, TG_BF16 = 1 } tg_dtype;
 #define TG_MAX_VERIFY_NODES 1024    /* N of one verify call                    */
 #define TG_MAX_NGRAM 16             /* n_max of the n-gram drafter             */
 #define TG_MAX_NGRAM_FRONTIER 1024  /* F of one n-gram expansion               */
+#define TG_NOALLOC_SCRATCH_BYTES (32u << 20) /* scratch of the no-allocation call */
 
 /*
  * Caller-owned draft tree, structure of arrays, one row of `cap` slots per
@@ -153,6 +154,29 @@ tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
                                    float sm_scale, tg_dtype dtype,
                                    void *workspace, size_t ws_bytes,
                                    uint32_t *d_err, void *stream);
+
+/*
+ * tg_tree_verify_attention without a workspace, for callers that cannot
+ * allocate (code under HIP graph capture, serving loops, harnesses that
+ * forbid allocation).  Same arguments, results and device errors as
+ * tg_tree_verify_attention, same kernels; the split-prefix partials go to a
+ * scratch array of TG_NOALLOC_SCRATCH_BYTES that the library keeps in every
+ * device's memory from its first use until the process ends.  The call uses
+ * the scratch of the current device (the stream must belong to it); its
+ * first call on a device looks the array's address up, later calls allocate
+ * nothing and call no allocating routine.
+ * Limits: a shape whose workspace query exceeds TG_NOALLOC_SCRATCH_BYTES is
+ * rejected with TG_ERR_WORKSPACE before anything is launched.
+ * Calls on one device share the scratch: two calls that overlap in time on
+ * one GPU (different streams, or host threads) race and may corrupt each
+ * other's output; calls ordered on one stream do not.  The scratch needs no
+ * clearing (every call writes all of the partials it reads).
+ */
+tg_status tg_tree_verify_attention_noalloc(const void *q, const void *k_cache,
+                                           const void *v_cache, const int32_t *parent,
+                                           const int32_t *prefix_len, void *out, int B, int N,
+                                           int Hq, int Hkv, int D, int S_max, float sm_scale,
+                                           tg_dtype dtype, uint32_t *d_err, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* One expansion step (Sec. 3.1; Alg. 1).                                   */

@@ -38,6 +38,7 @@ MAX_TOPK = 64
 MAX_CAP = 4096
 MAX_EXPAND_CHILDREN = 8192
 MAX_VERIFY_NODES = 1024
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTED = (
     "tg_status_str",
@@ -47,6 +48,7 @@ EXPORTED = (
     "tg_trace_end",
     "tg_verify_attention_workspace",
     "tg_tree_verify_attention",
+    "tg_tree_verify_attention_noalloc",
     "tg_expand_topk_workspace",
     "tg_tree_expand_topk",
     "tg_rescore_graft_workspace",
@@ -108,6 +110,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tg_tree_verify_attention.restype = _i32
     lib.tg_tree_verify_attention.argtypes = ([_vp] * 6 + [_i32] * 6 + [_f32, _i32, _vp, _sz,
                                              _vp, _vp])
+    lib.tg_tree_verify_attention_noalloc.restype = _i32
+    lib.tg_tree_verify_attention_noalloc.argtypes = ([_vp] * 6 + [_i32] * 6 + [_f32, _i32, _vp,
+                                                     _vp])
     lib.tg_expand_topk_workspace.restype = _sz
     lib.tg_expand_topk_workspace.argtypes = [_i32] * 5
     lib.tg_tree_expand_topk.restype = _i32
@@ -321,6 +326,41 @@ def verify_attention(q, k_cache, v_cache, parent, prefix_len, sm_scale, out=None
                                       float(sm_scale), dt, _ptr(ws), wsb, _ptr(d_err),
                                       _stream(stream, dev))
     _check("tg_tree_verify_attention", st)
+    return out
+
+
+def verify_attention_noalloc(q, k_cache, v_cache, parent, prefix_len, sm_scale, out=None,
+                             d_err=None, stream=None):
+    """tg_tree_verify_attention_noalloc: the same call without a workspace
+    (the library's per-device scratch holds the split partials; shapes that
+    need more than NOALLOC_SCRATCH_BYTES are rejected).  The binding allocates
+    `out` only when the caller passes none."""
+    lib = load()
+    if q.dtype == torch.bfloat16:
+        dt = BF16
+    elif q.dtype == torch.float32:
+        dt = F32
+    else:
+        raise ValueError("q must be bfloat16 or float32")
+    for t, n in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, n, q.dtype)
+    B, N, Hq, D = q.shape
+    Hkv, S_max = k_cache.shape[1], k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, Hkv, S_max, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("k_cache/v_cache must be [B, Hkv, S_max, D]")
+    dev = q.device
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        if t.device != dev:
+            raise ValueError(f"{n} must be on {dev}, got {t.device}")
+    _in(parent, "parent", (B, N), torch.int32, dev)
+    _in(prefix_len, "prefix_len", (B,), torch.int32, dev)
+    out = _out(out, "out", q.shape, q.dtype, dev)
+    d_err = _err(d_err, dev)
+    st = lib.tg_tree_verify_attention_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                              _ptr(parent), _ptr(prefix_len), _ptr(out), B, N,
+                                              Hq, Hkv, D, S_max, float(sm_scale), dt,
+                                              _ptr(d_err), _stream(stream, dev))
+    _check("tg_tree_verify_attention_noalloc", st)
     return out
 
 

@@ -2,6 +2,8 @@
 // Every call is asynchronous on the caller's stream and allocates nothing.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "../../include/treegraft.h"
 #include "tg_kernels.h"
 
@@ -64,13 +66,20 @@ size_t tg_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
   return tg::attn_workspace_bytes(s, dtype);
 }
 
-tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
-                                   const void *v_cache, const int32_t *parent,
-                                   const int32_t *prefix_len, void *out, int B,
-                                   int N, int Hq, int Hkv, int D, int S_max,
-                                   float sm_scale, tg_dtype dtype,
-                                   void *workspace, size_t ws_bytes,
-                                   uint32_t *d_err, void *stream) {
+}  // extern "C"
+
+// Scratch memory of tg_tree_verify_attention_noalloc, held by every device
+// the library runs on until the process ends.  In host code this name is
+// only a stand-in for the symbol: the device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+static __device__ __align__(256) unsigned char scratch[TG_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+tg_status verify_attention_args(const void *q, const void *k_cache, const void *v_cache,
+                                const int32_t *parent, const int32_t *prefix_len, void *out,
+                                int B, int N, int Hq, int Hkv, int D, int S_max, float sm_scale,
+                                tg_dtype dtype) {
   if (!q || !k_cache || !v_cache || !parent || !prefix_len || !out)
     return TG_ERR_INVALID_ARG;
   if (B <= 0 || N <= 0 || Hq <= 0 || Hkv <= 0 || S_max < N) return TG_ERR_INVALID_ARG;
@@ -79,17 +88,83 @@ tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
   if (D != 64 && D != 128) return TG_ERR_UNSUPPORTED;
   if (N > TG_MAX_VERIFY_NODES) return TG_ERR_UNSUPPORTED;
   if (dtype != TG_F32 && dtype != TG_BF16) return TG_ERR_INVALID_ARG;
-  tg::AttnShape s{B, N, Hq, Hkv, D, S_max, sm_scale};
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return TG_OK;
+}
+
+// Launches after the argument checks; `workspace` holds at least the bytes
+// attn_workspace_bytes() asks for.
+tg_status verify_attention_launch(const void *q, const void *k_cache, const void *v_cache,
+                                  const int32_t *parent, const int32_t *prefix_len, void *out,
+                                  const tg::AttnShape &s, tg_dtype dtype, void *workspace,
+                                  uint32_t *d_err, hipStream_t st) {
   if (dtype == TG_F32)
     return from_hip(tg::launch_attn_f32(
         s, static_cast<const float *>(q), static_cast<const float *>(k_cache),
         static_cast<const float *>(v_cache), parent, prefix_len,
         static_cast<float *>(out), d_err, st));
-  size_t need = tg::attn_workspace_bytes(s, dtype);
-  if (need && (!workspace || ws_bytes < need)) return TG_ERR_WORKSPACE;
   return from_hip(tg::launch_attn_bf16(s, q, k_cache, v_cache, parent, prefix_len,
                                        out, workspace, d_err, st));
+}
+
+constexpr int kMaxDevices = 64;
+void *g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The current device's address of `scratch` (looked up on its first call on
+// that device, with that device current).
+tg_status scratch_addr(void **addr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return TG_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return TG_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TG_ERR_HIP;
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return TG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tg_status tg_tree_verify_attention(const void *q, const void *k_cache,
+                                   const void *v_cache, const int32_t *parent,
+                                   const int32_t *prefix_len, void *out, int B,
+                                   int N, int Hq, int Hkv, int D, int S_max,
+                                   float sm_scale, tg_dtype dtype,
+                                   void *workspace, size_t ws_bytes,
+                                   uint32_t *d_err, void *stream) {
+  const tg_status a = verify_attention_args(q, k_cache, v_cache, parent, prefix_len, out, B, N,
+                                            Hq, Hkv, D, S_max, sm_scale, dtype);
+  if (a != TG_OK) return a;
+  tg::AttnShape s{B, N, Hq, Hkv, D, S_max, sm_scale};
+  const size_t need = tg::attn_workspace_bytes(s, dtype);
+  if (need && (!workspace || ws_bytes < need)) return TG_ERR_WORKSPACE;
+  return verify_attention_launch(q, k_cache, v_cache, parent, prefix_len, out, s, dtype,
+                                 workspace, d_err, reinterpret_cast<hipStream_t>(stream));
+}
+
+tg_status tg_tree_verify_attention_noalloc(const void *q, const void *k_cache,
+                                           const void *v_cache, const int32_t *parent,
+                                           const int32_t *prefix_len, void *out, int B, int N,
+                                           int Hq, int Hkv, int D, int S_max, float sm_scale,
+                                           tg_dtype dtype, uint32_t *d_err, void *stream) {
+  const tg_status a = verify_attention_args(q, k_cache, v_cache, parent, prefix_len, out, B, N,
+                                            Hq, Hkv, D, S_max, sm_scale, dtype);
+  if (a != TG_OK) return a;
+  tg::AttnShape s{B, N, Hq, Hkv, D, S_max, sm_scale};
+  const size_t need = tg::attn_workspace_bytes(s, dtype);
+  if (need > TG_NOALLOC_SCRATCH_BYTES) return TG_ERR_WORKSPACE;
+  void *ws = nullptr;
+  if (need) {
+    const tg_status r = scratch_addr(&ws);
+    if (r != TG_OK) return r;
+  }
+  return verify_attention_launch(q, k_cache, v_cache, parent, prefix_len, out, s, dtype, ws,
+                                 d_err, reinterpret_cast<hipStream_t>(stream));
 }
 
 // ------------------------------------------------------------------- expand
