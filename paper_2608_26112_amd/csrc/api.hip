@@ -84,7 +84,9 @@ tg_status verify_attention_args(const void *q, const void *k_cache, const void *
     return TG_ERR_INVALID_ARG;
   if (B <= 0 || N <= 0 || Hq <= 0 || Hkv <= 0 || S_max < N) return TG_ERR_INVALID_ARG;
   if (Hq % Hkv) return TG_ERR_INVALID_ARG;
-  if (!(sm_scale == sm_scale)) return TG_ERR_INVALID_ARG;
+  // a finite, non-negative softmax scale (the kernels take each row's
+  // maximum of the unscaled scores as the maximum of the scaled ones)
+  if (!(sm_scale >= 0.0f) || sm_scale == __builtin_inff()) return TG_ERR_INVALID_ARG;
   if (D != 64 && D != 128) return TG_ERR_UNSUPPORTED;
   if (N > TG_MAX_VERIFY_NODES) return TG_ERR_UNSUPPORTED;
   if (dtype != TG_F32 && dtype != TG_BF16) return TG_ERR_INVALID_ARG;

@@ -123,9 +123,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   const int g = rest % Hkv;
   const int b = rest / Hkv;
 
+  // Every global read of the prologue is issued before the first one is
+  // waited for: the prefix length, this thread's parents (at most
+  // TG_MAX_VERIFY_NODES / kThreads of them) and its Q fragment.
   const int L = prefix_len[b];
   const int rows_total = N * G;
   const int row0 = tile * BM;
+  constexpr int kParPerThread = (TG_MAX_VERIFY_NODES + kThreads - 1) / kThreads;
+  int pv[kParPerThread];
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = tid + k * kThreads;
+    pv[k] = i < N ? parent[(size_t)b * N + i] : -1;
+  }
+  const int node_lo = row0 / G;
+  const int qrow = row0 + w * 32 + r32;
+  const bool qvalid = qrow < rows_total;
+  const int qnode = qvalid ? qrow / G : node_lo;
+  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  bf16x8 qf[KS];
+  {
+    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+  }
   if (bad_prefix(L, N, S_max)) {
     if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
     if (n_splits == 1) {
@@ -206,18 +228,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   if (n_tiles_all > 0) issue(0, stage0);
 
   // ---- parents and ancestor-or-self bitsets of this tile's nodes (a1)
-  const int node_lo = row0 / G;
   const int node_hi = min(N, (row0 + BM - 1) / G + 1);
   const int nloc = node_hi - node_lo;
   const int NW = (N + 31) >> 5;
   bool badp = false;
-  for (int i = tid; i < N; i += kThreads) {
-    int p = parent[(size_t)b * N + i];
-    if (p < -1 || p >= i) {
-      badp = true;
-      p = -1;
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = tid + k * kThreads;
+    int p = pv[k];
+    if (i < N) {
+      if (p < -1 || p >= i) {
+        badp = true;
+        p = -1;
+      }
+      par_s[i] = p;
     }
-    par_s[i] = p;
   }
   if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
   for (int i = tid; i < nloc * NW; i += kThreads) anc_s[i] = 0;
@@ -228,19 +253,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   }
   __syncthreads();  // bitsets ready; par_s (stage 1) free again
 
-  // ---- this lane's query row, Q fragment in registers
-  const int qrow = row0 + w * 32 + r32;
-  const bool qvalid = qrow < rows_total;
-  const int qnode = qvalid ? qrow / G : node_lo;
-  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  // ---- this lane's query row (its Q fragment is already in flight)
   const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
-  bf16x8 qf[KS];
-  {
-    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
-#pragma unroll
-    for (int s = 0; s < KS; ++s)
-      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
-  }
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -475,9 +489,33 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   const int g = rest % Hkv;
   const int b = rest / Hkv;
 
+  // Every global read of the prologue is issued before the first one is
+  // waited for: the prefix length, this thread's parents and its Q fragment.
   const int L = prefix_len[b];
   const int rows_total = N * G;
   const int row0 = tile * BMP;
+  constexpr int kParPerThread = (TG_MAX_VERIFY_NODES + NT - 1) / NT;
+  int pv[kParPerThread];
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = tid + k * NT;
+    pv[k] = i < N ? parent[(size_t)b * N + i] : -1;
+  }
+  const int node_lo = row0 / G;
+  const int qrow = row0 + w * 32 + r32;
+  const bool qvalid = qrow < rows_total;
+  const int qnode = qvalid ? qrow / G : node_lo;
+  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  // Q as given; scores leave the MFMA in raw units and are scaled to log2
+  // units (sm_scale * log2 e) by the fused multiply-add that also subtracts
+  // the reference
+  bf16x8 qf[KS];
+  {
+    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+  }
   if (bad_prefix(L, N, S_max)) {
     if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
     if (n_splits == 1) {
@@ -539,18 +577,21 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   if (n > 0) issue(vb, 0, vst0);
 
   // ---- ancestor-or-self bitsets of this tile's nodes (a1)
-  const int node_lo = row0 / G;
   const int node_hi = min(N, (row0 + BMP - 1) / G + 1);
   const int nloc = node_hi - node_lo;
   const int NW = (N + 31) >> 5;
   bool badp = false;
-  for (int i = tid; i < N; i += NT) {
-    int p = parent[(size_t)b * N + i];
-    if (p < -1 || p >= i) {
-      badp = true;
-      p = -1;
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = tid + k * NT;
+    int p = pv[k];
+    if (i < N) {
+      if (p < -1 || p >= i) {
+        badp = true;
+        p = -1;
+      }
+      par_s[i] = p;
     }
-    par_s[i] = p;
   }
   if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
   for (int i = tid; i < nloc * NW; i += NT) anc_s[i] = 0;
@@ -563,24 +604,8 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   for (int i = 0; i < w; ++i) lead = lead && simd_s[i] != my_simd;
   __syncthreads();
 
-  // ---- this lane's query row, Q fragment in registers
-  const int qrow = row0 + w * 32 + r32;
-  const bool qvalid = qrow < rows_total;
-  const int qnode = qvalid ? qrow / G : node_lo;
-  const int qhead = g * G + (qvalid ? qrow % G : 0);
+  // ---- this lane's query row (its Q fragment is already in flight)
   const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
-  // Q pre-scaled by sm_scale * log2(e) (one bf16 rounding), so that scores
-  // come out of the MFMA in log2 units
-  bf16x8 qf[KS];
-  {
-    const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const bf16x8 raw = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)((float)raw[e] * scale2);
-    }
-  }
 
   // Running row reference m (log2 units): the max of the row's first tile
   // with a visible key, then moved up only when a tile's scores exceed it by
@@ -662,7 +687,6 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
     __builtin_amdgcn_s_setprio(0);
   };
-
   // vector phase: softmax of tile t's scores (acc) into pb, m, l, o scale
   auto sphase = [&](int t) __attribute__((always_inline)) {
     const bool tree_tile = tree_tile_at(t);
@@ -699,8 +723,8 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     auto probs = [&](float *ls) __attribute__((always_inline)) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p0 = __builtin_amdgcn_exp2f(acc[0][r] - m);
-        const float p1 = __builtin_amdgcn_exp2f(acc[0][r + 4] - m);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(acc[0][r], scale2, -m));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(acc[0][r + 4], scale2, -m));
         pb[0][0][r] = (__bf16)p0;
         pb[0][0][r + 4] = (__bf16)p1;
         ls[r] = p0 + p1;
@@ -709,7 +733,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
         for (int r = blk ? 0 : 8; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(acc[blk][r] - m);
+          const float p = __builtin_amdgcn_exp2f(fmaf(acc[blk][r], scale2, -m));
           ls[r & 3] += p;
           pb[blk][r >> 3][r & 7] = (__bf16)p;
         }
@@ -737,7 +761,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
         mx = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
       }
       // max over the row's 64 keys, relative to the reference
-      mx = __builtin_fmaxf(mx, half_swap(mx)) - m;
+      mx = fmaf(__builtin_fmaxf(mx, half_swap(mx)), scale2, -m);
       const bool need = m_set ? mx > kSlack : mx != -__builtin_inff();
       if (__any(need)) {
         // set or move the reference of the rows that need it; every other

@@ -90,6 +90,8 @@ def test_verify_attention_host_checks(lib):
     assert _verify(lib, N=2048, S=4096) == tg.ERR_UNSUPPORTED
     assert _verify(lib, dt=7) == tg.ERR_INVALID_ARG
     assert _verify(lib, scale=float("nan")) == tg.ERR_INVALID_ARG
+    assert _verify(lib, scale=-0.125) == tg.ERR_INVALID_ARG
+    assert _verify(lib, scale=float("inf")) == tg.ERR_INVALID_ARG
     # a shape that needs a split workspace, called without one
     need = lib.tg_verify_attention_workspace(1, 64, 32, 8, 128, 2112, tg.BF16)
     assert need > 0
