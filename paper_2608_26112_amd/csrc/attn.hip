@@ -89,6 +89,11 @@ __device__ __forceinline__ bf16x4 lds_read_tr4(const __bf16 *p) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
+// byte address of a pointer into LDS (the low 32 bits of the generic address)
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
@@ -432,16 +437,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
 // For long prefixes: 8 waves (two per SIMD) share each K/V tile; a
 // workgroup owns 256 query rows (32 per wave, the same MFMA layout as
 // attn_mfma_kernel).  Each wave alternates an MFMA phase M(t) = {PV of tile
-// t-1, QK^T of tile t} and a vector phase S(t) = {mask, row max, rescale,
-// exponentials of tile t}.  Waves 4-7 run one phase behind waves 0-3, so on
-// every SIMD one wave feeds the matrix core while the other runs its
-// softmax; a workgroup barrier ends every phase.
-//   phase 2j  : loads of K(j+1) and V(j) are issued; group A runs M(j),
+// t-1, QK^T of tile t} and a vector phase S(t) = {mask, reference, rescale,
+// exponentials of tile t}.  On every SIMD one wave (group A) runs one phase
+// ahead of the other (group B), so one wave feeds the matrix core while the
+// other runs its softmax; a workgroup barrier ends every phase.
+//   phase 2j  : K(j+2) and V(j+1) are requested; group A runs M(j),
 //               group B runs S(j-1)
-//   phase 2j+1: group A runs S(j), group B runs M(j); the loads have landed
-//               by the barrier that ends the phase
-// K(j) is read in phases 2j and 2j+1, V(j) in 2j+2 and 2j+3, so two stages
-// of each suffice.
+//   phase 2j+1: group A runs S(j), group B runs M(j)
+// K and V have three LDS stages each, so the requests of phase pair j land
+// during pair j+1 and are waited for only at the barrier that ends it.
+// At D = 128 the MFMA phase is inline assembly (mfma_phase_d128.inc) that
+// keeps its fragment reads four MFMAs ahead; the compiler, at 256 VGPRs for
+// two waves per SIMD, would wait for every read.
+#include "mfma_phase_d128.inc"
+
 template <int D>
 __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
@@ -638,12 +647,71 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   for (int s = 0; s < KS; ++s) koff[s] = Lds::at(r32, 16 * s + 8 * h);
 
   // MFMA phase: PV of the previous tile (pb, V in Vp) then QK^T of this one
-  // (fragment reads one MFMA group ahead)
   auto mphase = [&](bool do_pv, const __bf16 *Vp, bool do_qk, const __bf16 *Kt)
                     __attribute__((always_inline)) {
     // the MFMA wave issues first whenever the matrix core is free; the
     // softmax wave on the same SIMD fills the remaining issue slots
     __builtin_amdgcn_s_setprio(1);
+    if constexpr (D == 128) {
+      // operands in registers the statements name: LDS byte addresses
+      // (stage base in an SGPR, per-lane offsets in VGPRs), fragments as
+      // 4-dword vectors
+      using i32x4 = int __attribute__((ext_vector_type(4)));
+      const uint32_t vbase = lds_addr(Vp), kbase = lds_addr(Kt);
+      const i32x4 p00 = __builtin_bit_cast(i32x4, pb[0][0]);
+      const i32x4 p01 = __builtin_bit_cast(i32x4, pb[0][1]);
+      const i32x4 p10 = __builtin_bit_cast(i32x4, pb[1][0]);
+      const i32x4 p11 = __builtin_bit_cast(i32x4, pb[1][1]);
+      i32x4 qq[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) qq[s] = __builtin_bit_cast(i32x4, qf[s]);
+      int va[8], ka[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        va[i] = 2 * voff[i >> 1][i & 1];
+        ka[i] = 2 * koff[i];
+      }
+#define TG_RING_CLOBBERS                                                                   \
+  "v220", "v221", "v222", "v223", "v224", "v225", "v226", "v227", "v228", "v229", "v230", \
+      "v231", "v232", "v233", "v234", "v235", "v236", "v237", "v238", "v239", "v240",     \
+      "v241", "v242", "v243", "v244", "v245", "v246", "v247", "v248", "v249", "v250",     \
+      "v251", "v252", "v253", "v254", "v255"
+      if (do_pv && do_qk) {
+        asm volatile(TG_ASM_PVQK
+                     : [o0] "+v"(o[0]), [o1] "+v"(o[1]), [o2] "+v"(o[2]), [o3] "+v"(o[3]),
+                       [a0] "=&v"(acc[0]), [a1] "=&v"(acc[1])
+                     : [p00] "v"(p00), [p01] "v"(p01), [p10] "v"(p10), [p11] "v"(p11),
+                       [q0] "v"(qq[0]), [q1] "v"(qq[1]), [q2] "v"(qq[2]), [q3] "v"(qq[3]),
+                       [q4] "v"(qq[4]), [q5] "v"(qq[5]), [q6] "v"(qq[6]), [q7] "v"(qq[7]),
+                       [va0] "v"(va[0]), [va1] "v"(va[1]), [va2] "v"(va[2]), [va3] "v"(va[3]),
+                       [va4] "v"(va[4]), [va5] "v"(va[5]), [va6] "v"(va[6]), [va7] "v"(va[7]),
+                       [ka0] "v"(ka[0]), [ka1] "v"(ka[1]), [ka2] "v"(ka[2]), [ka3] "v"(ka[3]),
+                       [ka4] "v"(ka[4]), [ka5] "v"(ka[5]), [ka6] "v"(ka[6]), [ka7] "v"(ka[7]),
+                       [vb] "s"(vbase), [kb] "s"(kbase)
+                     : TG_RING_CLOBBERS);
+      } else if (do_pv) {
+        asm volatile(TG_ASM_PV
+                     : [o0] "+v"(o[0]), [o1] "+v"(o[1]), [o2] "+v"(o[2]), [o3] "+v"(o[3])
+                     : [p00] "v"(p00), [p01] "v"(p01), [p10] "v"(p10), [p11] "v"(p11),
+                       [va0] "v"(va[0]), [va1] "v"(va[1]), [va2] "v"(va[2]), [va3] "v"(va[3]),
+                       [va4] "v"(va[4]), [va5] "v"(va[5]), [va6] "v"(va[6]), [va7] "v"(va[7]),
+                       [vb] "s"(vbase)
+                     : TG_RING_CLOBBERS);
+      } else if (do_qk) {
+        asm volatile(TG_ASM_QK
+                     : [a0] "=&v"(acc[0]), [a1] "=&v"(acc[1])
+                     : [q0] "v"(qq[0]), [q1] "v"(qq[1]), [q2] "v"(qq[2]), [q3] "v"(qq[3]),
+                       [q4] "v"(qq[4]), [q5] "v"(qq[5]), [q6] "v"(qq[6]), [q7] "v"(qq[7]),
+                       [ka0] "v"(ka[0]), [ka1] "v"(ka[1]), [ka2] "v"(ka[2]), [ka3] "v"(ka[3]),
+                       [ka4] "v"(ka[4]), [ka5] "v"(ka[5]), [ka6] "v"(ka[6]), [ka7] "v"(ka[7]),
+                       [kb] "s"(kbase)
+                     : TG_RING_CLOBBERS);
+      }
+#undef TG_RING_CLOBBERS
+      __builtin_amdgcn_s_setprio(0);
+      return;
+    }
+    // D = 64: fragment reads one MFMA group ahead
     if (do_pv) {
       auto vfrag = [&](int blk, int u, int db) {
         const __bf16 *vb0 = Vp + (blk * 32 + 16 * u) * D;
@@ -795,7 +863,10 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   // the odd ones wait for this wave's loads of the next phase pair's tiles
   // and for its LDS reads; `younger` loads (issued after those) may stay in
   // flight.  s_waitcnt immediate: vmcnt in bits [3:0], expcnt [6:4] left at
-  // its maximum (no wait), lgkmcnt [11:8] = 0.
+  // its maximum (no wait), lgkmcnt [11:8] = 0.  The barrier is not
+  // __syncthreads: its workgroup release fence would wait for every load
+  // in flight (vmcnt(0)), the younger ones included.  The "memory" clobber
+  // keeps the compiler from moving memory operations across it.
   auto bar_odd = [&](int younger) __attribute__((always_inline)) {
     if (younger >= 2 * LOADS)
       __builtin_amdgcn_s_waitcnt((2 * LOADS) | (7 << 4));
@@ -803,7 +874,9 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
       __builtin_amdgcn_s_waitcnt(LOADS | (7 << 4));
     else
       __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   bar_odd(0);

@@ -221,7 +221,6 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
 
   if (tid < K) run[tid] = 0;
   bool bad = false;
-  int rpar = 0;
 
   for (int gr = g_beg; gr < g_end; ++gr) {
     const int e0 = gr * kGrain;
