@@ -647,7 +647,9 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   for (int s = 0; s < KS; ++s) koff[s] = Lds::at(r32, 16 * s + 8 * h);
 
   // MFMA phase: PV of the previous tile (pb, V in Vp) then QK^T of this one
-  auto mphase = [&](bool do_pv, const __bf16 *Vp, bool do_qk, const __bf16 *Kt)
+  // With `bar` (D = 128 only) the phase takes the workgroup barrier that
+  // precedes it inside its statement, after issuing its first fragment reads.
+  auto mphase = [&](bool do_pv, const __bf16 *Vp, bool do_qk, const __bf16 *Kt, bool bar)
                     __attribute__((always_inline)) {
     // the MFMA wave issues first whenever the matrix core is free; the
     // softmax wave on the same SIMD fills the remaining issue slots
@@ -671,42 +673,46 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
         va[i] = 2 * voff[i >> 1][i & 1];
         ka[i] = 2 * koff[i];
       }
+#define TG_O_OUT [o0] "+v"(o[0]), [o1] "+v"(o[1]), [o2] "+v"(o[2]), [o3] "+v"(o[3])
+#define TG_ACC_OUT [a0] "=&v"(acc[0]), [a1] "=&v"(acc[1])
+#define TG_PV_IN                                                                           \
+  [p00] "v"(p00), [p01] "v"(p01), [p10] "v"(p10), [p11] "v"(p11), [va0] "v"(va[0]),        \
+      [va1] "v"(va[1]), [va2] "v"(va[2]), [va3] "v"(va[3]), [va4] "v"(va[4]),               \
+      [va5] "v"(va[5]), [va6] "v"(va[6]), [va7] "v"(va[7]), [vb] "s"(vbase)
+#define TG_QK_IN                                                                           \
+  [q0] "v"(qq[0]), [q1] "v"(qq[1]), [q2] "v"(qq[2]), [q3] "v"(qq[3]), [q4] "v"(qq[4]),     \
+      [q5] "v"(qq[5]), [q6] "v"(qq[6]), [q7] "v"(qq[7]), [ka0] "v"(ka[0]), [ka1] "v"(ka[1]), \
+      [ka2] "v"(ka[2]), [ka3] "v"(ka[3]), [ka4] "v"(ka[4]), [ka5] "v"(ka[5]),               \
+      [ka6] "v"(ka[6]), [ka7] "v"(ka[7]), [kb] "s"(kbase)
 #define TG_RING_CLOBBERS                                                                   \
   "v220", "v221", "v222", "v223", "v224", "v225", "v226", "v227", "v228", "v229", "v230", \
       "v231", "v232", "v233", "v234", "v235", "v236", "v237", "v238", "v239", "v240",     \
       "v241", "v242", "v243", "v244", "v245", "v246", "v247", "v248", "v249", "v250",     \
       "v251", "v252", "v253", "v254", "v255"
+      // the barrier statements also order memory ("memory" clobber), as the
+      // barriers outside them do
       if (do_pv && do_qk) {
-        asm volatile(TG_ASM_PVQK
-                     : [o0] "+v"(o[0]), [o1] "+v"(o[1]), [o2] "+v"(o[2]), [o3] "+v"(o[3]),
-                       [a0] "=&v"(acc[0]), [a1] "=&v"(acc[1])
-                     : [p00] "v"(p00), [p01] "v"(p01), [p10] "v"(p10), [p11] "v"(p11),
-                       [q0] "v"(qq[0]), [q1] "v"(qq[1]), [q2] "v"(qq[2]), [q3] "v"(qq[3]),
-                       [q4] "v"(qq[4]), [q5] "v"(qq[5]), [q6] "v"(qq[6]), [q7] "v"(qq[7]),
-                       [va0] "v"(va[0]), [va1] "v"(va[1]), [va2] "v"(va[2]), [va3] "v"(va[3]),
-                       [va4] "v"(va[4]), [va5] "v"(va[5]), [va6] "v"(va[6]), [va7] "v"(va[7]),
-                       [ka0] "v"(ka[0]), [ka1] "v"(ka[1]), [ka2] "v"(ka[2]), [ka3] "v"(ka[3]),
-                       [ka4] "v"(ka[4]), [ka5] "v"(ka[5]), [ka6] "v"(ka[6]), [ka7] "v"(ka[7]),
-                       [vb] "s"(vbase), [kb] "s"(kbase)
-                     : TG_RING_CLOBBERS);
+        if (bar)
+          asm volatile(TG_ASM_PVQK_BAR : TG_O_OUT, TG_ACC_OUT : TG_PV_IN, TG_QK_IN
+                       : "memory", TG_RING_CLOBBERS);
+        else
+          asm volatile(TG_ASM_PVQK : TG_O_OUT, TG_ACC_OUT : TG_PV_IN, TG_QK_IN
+                       : TG_RING_CLOBBERS);
       } else if (do_pv) {
-        asm volatile(TG_ASM_PV
-                     : [o0] "+v"(o[0]), [o1] "+v"(o[1]), [o2] "+v"(o[2]), [o3] "+v"(o[3])
-                     : [p00] "v"(p00), [p01] "v"(p01), [p10] "v"(p10), [p11] "v"(p11),
-                       [va0] "v"(va[0]), [va1] "v"(va[1]), [va2] "v"(va[2]), [va3] "v"(va[3]),
-                       [va4] "v"(va[4]), [va5] "v"(va[5]), [va6] "v"(va[6]), [va7] "v"(va[7]),
-                       [vb] "s"(vbase)
-                     : TG_RING_CLOBBERS);
+        if (bar)
+          asm volatile(TG_ASM_PV_BAR : TG_O_OUT : TG_PV_IN : "memory", TG_RING_CLOBBERS);
+        else
+          asm volatile(TG_ASM_PV : TG_O_OUT : TG_PV_IN : TG_RING_CLOBBERS);
       } else if (do_qk) {
-        asm volatile(TG_ASM_QK
-                     : [a0] "=&v"(acc[0]), [a1] "=&v"(acc[1])
-                     : [q0] "v"(qq[0]), [q1] "v"(qq[1]), [q2] "v"(qq[2]), [q3] "v"(qq[3]),
-                       [q4] "v"(qq[4]), [q5] "v"(qq[5]), [q6] "v"(qq[6]), [q7] "v"(qq[7]),
-                       [ka0] "v"(ka[0]), [ka1] "v"(ka[1]), [ka2] "v"(ka[2]), [ka3] "v"(ka[3]),
-                       [ka4] "v"(ka[4]), [ka5] "v"(ka[5]), [ka6] "v"(ka[6]), [ka7] "v"(ka[7]),
-                       [kb] "s"(kbase)
-                     : TG_RING_CLOBBERS);
+        if (bar)
+          asm volatile(TG_ASM_QK_BAR : TG_ACC_OUT : TG_QK_IN : "memory", TG_RING_CLOBBERS);
+        else
+          asm volatile(TG_ASM_QK : TG_ACC_OUT : TG_QK_IN : TG_RING_CLOBBERS);
       }
+#undef TG_O_OUT
+#undef TG_ACC_OUT
+#undef TG_PV_IN
+#undef TG_QK_IN
 #undef TG_RING_CLOBBERS
       __builtin_amdgcn_s_setprio(0);
       return;
@@ -891,31 +897,34 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     if (ld_v) issue(vb, j + 1, vis);
     return LOADS * ((int)ld_k + (int)ld_v);
   };
+  // Group B's MFMA phase follows its own softmax phase and reads tiles every
+  // wave could see since the last odd barrier, so at D = 128 it issues its
+  // first fragment reads before the even barrier, inside its statement.
   // pairs 1 .. n-1 run both products
   auto pair = [&](int j, __bf16 *kq, __bf16 *kis, __bf16 *vis, __bf16 *vp)
                   __attribute__((always_inline)) {
     const int younger = requests(j, kis, vis);
     if (lead)
-      mphase(true, vp, true, kq);
+      mphase(true, vp, true, kq, false);
     else
       sphase(j - 1);
-    bar_even();
+    if (lead || D != 128) bar_even();
     if (lead)
       sphase(j);
     else
-      mphase(true, vp, true, kq);
+      mphase(true, vp, true, kq, D == 128);
     bar_odd(younger);
   };
   if (n > 0) {
     // pair 0: QK^T of tile 0 only
     {
       const int younger = requests(0, kst2, vst1);
-      if (lead) mphase(false, vst2, true, kst0);
-      bar_even();
+      if (lead) mphase(false, vst2, true, kst0, false);
+      if (lead || D != 128) bar_even();
       if (lead)
         sphase(0);
       else
-        mphase(false, vst2, true, kst0);
+        mphase(false, vst2, true, kst0, D == 128);
       bar_odd(younger);
     }
     int j = 1;
@@ -930,11 +939,11 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     const int r = (n - 1) % 3;
     __bf16 *vlast = r == 0 ? vst0 : (r == 1 ? vst1 : vst2);
     if (lead)
-      mphase(true, vlast, false, kst0);
+      mphase(true, vlast, false, kst0, false);
     else
       sphase(n - 1);
-    bar_even();
-    if (!lead) mphase(true, vlast, false, kst0);
+    if (lead || D != 128) bar_even();
+    if (!lead) mphase(true, vlast, false, kst0, D == 128);
     bar_odd(0);
   }
 
