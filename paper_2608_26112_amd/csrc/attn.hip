@@ -655,6 +655,11 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     // softmax wave on the same SIMD fills the remaining issue slots
     __builtin_amdgcn_s_setprio(1);
     if constexpr (D == 128) {
+      // the generated statements assume this tile geometry: 64-key tiles of
+      // 256-byte rows, the second 32-key block 8 KB into a K stage, 16-key
+      // halves 4 KB apart in a V stage
+      static_assert(BN == 64 && Lds::TILE == BN * 128 && KS == 8 && DB == 4,
+                    "mfma_phase_d128.inc is generated for 64-key tiles at D = 128");
       // operands in registers the statements name: LDS byte addresses
       // (stage base in an SGPR, per-lane offsets in VGPRs), fragments as
       // 4-dword vectors
