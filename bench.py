@@ -33,6 +33,10 @@ reports each under `extra` with its own roofline and CPU baseline:
                       drafter, scheduler signals, GlobalPrune to 64 nodes,
                       Llama-3-8B verify layer, accept, KV update), replayed as
                       one HIP graph
+  turn-standard       the standard-construction turn (Alg. 1): six expansion
+                      steps over dense logits (root, then 10-node frontiers,
+                      K=8, N=10), GlobalPrune to 64 nodes, the same verify
+                      layer, accept and KV update, replayed as one HIP graph
 `--workload NAME` times only that workload as the headline; `--only` skips
 the extras.  All inputs are seeded synthetic data with the workloads' shapes
 and distributions (no model weights or datasets).  The CPU baselines time the
@@ -62,7 +66,7 @@ PEAK_BF16 = 2.5e15       # flop/s, dense bf16 MFMA
 PEAK_FP32 = 157.3e12     # flop/s, fp32 vector
 ATTN_MAIN = ("attn_pingpong", "attn_mfma", "attn_f32")   # tree-verify attention kernels
 WORKLOADS = ["attn-llama70b", "tiny", "attn-llama8b", "attn-llama8b-x32", "attn-longctx",
-             "expand-twodrafter", "rescore-twodrafter", "turn"]
+             "expand-twodrafter", "rescore-twodrafter", "turn", "turn-standard"]
 
 
 def parse():
@@ -1032,6 +1036,243 @@ def turn_bench(tg, torch, dev, steps, warmup, copies, cpu_s):
     return out
 
 
+# ------------------------------------------ the standard (Alg. 1) turn
+# The Llama-3-8B-shaped decoding turn with the standard construction: six
+# small-drafter expansion steps over dense logits rows (the root, then the
+# best-N frontier; K = 8 children per node, N = 10), GlobalPrune of the
+# 392-node tree to 64 nodes, one bf16 verify-attention layer, acceptance and
+# the KV update.
+STD_STEPS, STD_K, STD_N = 6, 8, 10
+STD_NODES = 8 + 64 + 4 * 80
+
+
+def std_inputs(c, dev):
+    """Input copy c (seed 1003 + c): one logits tensor per step ([1, 1, V]
+    for the root step, [1, N, V] after it; N(0, 3) rows) and the verify
+    layer's Q/K/V."""
+    import torch
+    import workloads as W
+    g = W.rng([1003, c])
+    logits = []
+    for k in range(STD_STEPS):
+        F = 1 if k == 0 else STD_N
+        t = torch.empty((B, F, V), dtype=torch.float32, device=dev)
+        for f in range(F):
+            t[0, f] = torch.from_numpy(W.normal(W.rng([1003, c, k, f]), (V,), 3.0)).to(dev)
+        logits.append(t)
+    s = np.float32(1.0 / np.sqrt(128.0))
+    S = L + N_VER
+    q = torch.from_numpy(W.normal(g, (B, N_VER, HQ, D)) * s).to(dev).bfloat16()
+    k = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
+    v = torch.from_numpy(W.normal(g, (B, HKV, S, D)) * s).to(dev).bfloat16()
+    return dict(logits=logits, q=q, k=k, v=v)
+
+
+class StdStep:
+    """All buffers of one standard turn on one input copy (capturable)."""
+
+    def __init__(self, tg, inp, dev):
+        import torch
+        self.tg, self.inp = tg, inp
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.tree = tg.TreeState(B, CAP, dev)
+        self.ws_e = torch.empty(max(1, tg.expand_topk_workspace(B, STD_N, V, STD_K, STD_N)),
+                                dtype=torch.uint8, device=dev)
+        self.root_fr = torch.full((B, 1), -1, **i32)
+        self.lse = [torch.empty((B, 1 if k == 0 else STD_N), dtype=torch.float32, device=dev)
+                    for k in range(STD_STEPS)]
+        self.fr = [torch.empty((B, STD_N), **i32) for _ in range(STD_STEPS)]
+        self.nn = [torch.empty((B,), **i32) for _ in range(STD_STEPS)]
+        M = N_VER + 1
+        self.pr = dict(kept=torch.empty((B, N_VER), **i32), vparent=torch.empty((B, N_VER), **i32),
+                       vtoken=torch.empty((B, N_VER), **i32),
+                       position_ids=torch.empty((B, M), **i32),
+                       mask=torch.empty((B, M, (M + 31) // 32), **i32),
+                       retrieval=torch.empty((B, M, MAX_DEPTH + 1), **i32),
+                       n_keep=torch.empty((B,), **i32), n_leaves=torch.empty((B,), **i32))
+        nv = tg.verify_attention_workspace(B, N_VER, HQ, HKV, D, L + N_VER, tg.BF16)
+        self.ws_v = torch.empty(max(nv, 1), dtype=torch.uint8, device=dev)
+        self.plen = torch.full((B,), L, **i32)
+        self.new_plen = torch.empty((B,), **i32)
+        self.greedy = torch.zeros((B, N_VER + 1), **i32)
+        self.out = torch.empty_like(inp["q"])
+        self.A = torch.empty((B,), **i32)
+        self.path = torch.empty((B, MAX_DEPTH), **i32)
+        self.bonus = torch.empty((B,), **i32)
+
+    def run(self):
+        tg, x, t = self.tg, self.inp, self.tree
+        tg.tree_reset(t)
+        for k in range(STD_STEPS):
+            fr_k, nf_k = (self.root_fr, None) if k == 0 else (self.fr[k - 1], self.nn[k - 1])
+            tg.expand_topk(t, x["logits"][k], fr_k, nf_k, STD_K, STD_N, row_lse=self.lse[k],
+                           next_frontier=self.fr[k], n_next=self.nn[k], workspace=self.ws_e)
+        p = tg.global_prune(t, N_VER, MAX_DEPTH + 1, out=self.pr)
+        tg.verify_attention(x["q"], x["k"], x["v"], p["vparent"], self.plen, D ** -0.5,
+                            out=self.out, workspace=self.ws_v)
+        tg.accept(p["vparent"], p["vtoken"], p["n_keep"], self.greedy, MAX_DEPTH,
+                  accept_len=self.A, accept_path=self.path, bonus=self.bonus)
+        tg.kv_compact(x["k"], x["v"], self.plen, self.path, self.A,
+                      new_prefix_len=self.new_plen)
+
+
+def std_rows_per_step():
+    """Logits rows one standard turn reads: 1 (root), 8, then 10 per step."""
+    return 1 + 8 + 10 * (STD_STEPS - 2)
+
+
+def std_oracle_turn(host_logits, q, k, v, greedy, lse_gpu=None):
+    """The oracle's standard turn on host copies (lse_gpu: the GPU's row_lse
+    per step, for the split check).  Returns the tree, prune result, the
+    attention output and the acceptance."""
+    from oracle import attention as OA
+    from oracle import tree as OT
+    t = OT.Tree.empty(B, CAP)
+    fr, nn = np.full((B, 1), -1, np.int32), None
+    for step in range(STD_STEPS):
+        t, _, fr, nn, _ = OT.expand(t, host_logits[step], fr, nn, STD_K, STD_N,
+                                    lse_override=None if lse_gpu is None else lse_gpu[step])
+    n = int(t.n_nodes[0])
+    pr = OT.global_prune(t.parent[0, :n], t.cum[0, :n], n, N_VER)
+    par = pr["parent"][None]
+    tok = t.token[0, pr["kept"]][None]
+    out = OA.tree_verify_attention_fast(q, k, v, par, [L], D ** -0.5)
+    A, path, bonus, _ = OT.accept(par, tok, np.array([len(pr["kept"])]), greedy, MAX_DEPTH)
+    return t, pr, par, tok, out, (A, path, bonus)
+
+
+def std_turn_bench(tg, torch, dev, steps, warmup, copies, cpu_s):
+    """One standard turn per step, replayed as one captured HIP graph per
+    input copy (inputs rotate over `copies` resident copies)."""
+    inputs = [std_inputs(c, dev) for c in range(copies)]
+    steps_ = [StdStep(tg, inputs[c], dev) for c in range(copies)]
+    torch.cuda.synchronize()
+    pruned = []
+    for st in steps_:
+        st.run()
+        torch.cuda.synchronize()
+        assert int(st.tree.n_nodes[0].item()) == STD_NODES
+        assert int(st.pr["n_keep"][0].item()) == N_VER
+        par = st.pr["vparent"][0].cpu().numpy()
+        tok = st.pr["vtoken"][0].cpu().numpy()
+        st.greedy.copy_(torch.from_numpy(greedy_for((par, tok))[None]))
+        pruned.append((par, tok))
+    torch.cuda.synchronize()
+    # parity on input copy 0 (untimed): the oracle's turn with the GPU's
+    # exported log-sum-exps must give the same tree, pruned tree and
+    # acceptance bit for bit; attention within the bf16 bar
+    st0 = steps_[0]
+    # the K/V the attention of this run reads (earlier runs' KV updates
+    # included; this run's update comes after its attention)
+    qh, kh, vh = (inputs[0][n].float().cpu().numpy() for n in ("q", "k", "v"))
+    st0.run()
+    torch.cuda.synchronize()
+    host_logits = [x.cpu().numpy() for x in inputs[0]["logits"]]
+    lse_gpu = [x.cpu().numpy() for x in st0.lse]
+    greedy0 = st0.greedy.cpu().numpy()
+    t_o, pr_o, par_o, tok_o, out_o, acc_o = std_oracle_turn(host_logits, qh, kh, vh, greedy0,
+                                                            lse_gpu)
+    n = STD_NODES
+    tree_eq = all(np.array_equal(getattr(t_o, f)[0, :n], getattr(st0.tree, f)[0, :n].cpu().numpy())
+                  for f in ("parent", "token", "depth")) and \
+        np.array_equal(t_o.cum[0, :n].view(np.uint32),
+                       st0.tree.cum[0, :n].cpu().numpy().view(np.uint32))
+    prune_eq = np.array_equal(par_o[0], st0.pr["vparent"][0].cpu().numpy()) and \
+        np.array_equal(tok_o[0], st0.pr["vtoken"][0].cpu().numpy())
+    acc_eq = int(acc_o[0][0]) == int(st0.A[0].item()) and \
+        np.array_equal(acc_o[1][0], st0.path[0].cpu().numpy()) and \
+        int(acc_o[2][0]) == int(st0.bonus[0].item())
+    attn_err = float(np.abs(st0.out.float().cpu().numpy() - out_o).max())
+    graphs, timing = [], "eager launches"
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for st in steps_:
+            st.run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    try:
+        for st in steps_:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                st.run()
+            graphs.append(g)
+        torch.cuda.synchronize()
+        timing = "one captured HIP graph per step"
+    except Exception as exc:  # report and time eager launches instead
+        print(f"bench.py: graph capture failed ({exc}); timing eager launches", file=sys.stderr)
+        graphs = []
+    if graphs:        # replaying a graph must reproduce the eager turn
+        graphs[0].replay()
+        torch.cuda.synchronize()
+        assert int(steps_[0].tree.n_nodes[0].item()) == STD_NODES
+
+    def run(i):
+        if graphs:
+            graphs[i % len(graphs)].replay()
+        else:
+            steps_[i % len(steps_)].run()
+
+    ms_step = time_calls(torch, run, steps, warmup)
+    eager = lambda i: steps_[i % len(steps_)].run()
+    ms_eager = time_calls(torch, eager, steps, warmup)
+    kern, recs = kernel_times(tg, torch, eager, steps)
+    kernels = kernels_json(kern, steps)
+    per_step = len(recs) // steps
+    timeline = [[name, round(1e3 * ms, 2)] for name, ms in recs[-per_step:]]
+    row_bytes = V * 4
+    works = [verify_work(par) for par, _ in pruned]
+    v_bytes = sum(w[0] for w in works) / len(works)
+    v_flops = sum(w[1] for w in works) / len(works)
+    dom_bytes = std_rows_per_step() * row_bytes
+    step_bytes = dom_bytes + v_bytes
+    dom = "row_partial"
+    launches = kern[dom][0]
+    achieved = dom_bytes * steps / (kern[dom][1] * 1e-3)
+    roof = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+            "unit": "GB/s", "frac": achieved / PEAK_HBM, "traffic": None,
+            "bytes_per_launch": dom_bytes * steps / launches,
+            "avg_launch_us": 1e3 * kern[dom][1] / launches,
+            "launch_time_from": "trace pass (event pair around each kernel)",
+            "note": "latency bound: 1-10 live rows per launch"}
+    slowest = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    attn_us = sum(kernels[k]["us_per_step"] for k in ATTN_MAIN + ("attn_combine",) if k in kernels)
+    out = line(step_bytes / (ms_step * 1e-3) / 1e12, "TB/s", steps, warmup, ms_step,
+               {"workload": "standard-construction turn (Alg. 1: 6 expansion steps over dense "
+                            "logits, K = 8, N = 10) + GlobalPrune to 64 nodes + Llama-3-8B-shaped "
+                            "verify layer + acceptance + KV update", "batch": B, "vocab": V,
+                "children_K": STD_K, "frontier_N": STD_N, "steps": STD_STEPS,
+                "q_heads": HQ, "kv_heads": HKV, "head_dim": D, "prefix": L,
+                "verify_nodes": N_VER, "input_copies": copies, "timing": timing},
+               roof, "fp32+bf16",
+               **{"largest_kernel": {"name": slowest,
+                                     "us_per_step": kernels[slowest]["us_per_step"]},
+                  "draft_nodes_per_s": STD_NODES / (ms_step * 1e-3),
+                  "verify_attention": {"us": attn_us, "TB/s": v_bytes / (attn_us * 1e-6) / 1e12,
+                                       "TFLOP/s": v_flops / (attn_us * 1e-6) / 1e12,
+                                       "frac_hbm": v_bytes / (attn_us * 1e-6) / PEAK_HBM},
+                  "step_bytes": step_bytes, "eager_ms_per_step": ms_eager,
+                  "kernels": kernels, "step_timeline_us": timeline,
+                  "parity": {"tree_equal_with_gpu_lse": bool(tree_eq),
+                             "prune_equal": bool(prune_eq), "accept_equal": bool(acc_eq),
+                             "attention_max_abs_err": attn_err, "attention_bar": 2e-2}})
+    if cpu_s > 0:
+        turns, t0 = 0, time.perf_counter()
+        while True:
+            std_oracle_turn(host_logits, qh, kh, vh, greedy0)
+            turns += 1
+            el = time.perf_counter() - t0
+            if el >= cpu_s:
+                break
+        out["cpu_baseline"] = {"value": step_bytes * turns / el / 1e12, "unit": "TB/s",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"{turns} full standard turns on input copy 0 in "
+                                         f"{el:.1f} s (tree steps single-threaded NumPy, their "
+                                         f"own log-sum-exps; attention matmuls on the BLAS "
+                                         f"threads)"}
+    return out
+
+
 # ------------------------------------------------------------------ main
 
 def run_workload(name, args, tg, torch, dev, steps, warmup, cpu_s, shared):
@@ -1047,6 +1288,8 @@ def run_workload(name, args, tg, torch, dev, steps, warmup, cpu_s, shared):
         return tree_bench(tg, torch, dev, name, steps, warmup, cpu_s,
                           flags=args.rescore_flags if name.startswith("rescore") else 0,
                           shared=shared["td"])
+    if name == "turn-standard":
+        return std_turn_bench(tg, torch, dev, steps, warmup, args.copies, cpu_s)
     return turn_bench(tg, torch, dev, steps, warmup, args.copies, cpu_s)
 
 
