@@ -890,7 +890,9 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  bar_odd(0);
+  // The bitsets are complete; of the prologue's loads (K(0), K(1), V(0) in
+  // that order) only K(0) is needed by pair 0, the rest land behind it.
+  bar_odd(n > 1 ? 2 * LOADS : LOADS);
   // One pair of phases per j (tile j's QK^T, tile j-1's PV).  Tile j's K sits
   // in stage j % 3 and its V in stage j % 3; phase 2j requests K(j+2) and
   // V(j+1), whose stages held K(j-1) and V(j-2), last read in phase 2j-1.
