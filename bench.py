@@ -18,10 +18,12 @@ reports each under `extra` with its own roofline and CPU baseline:
                       prefix 128, 16 nodes), one expansion (V=1000, F=8, K=4,
                       N=8) and acceptance, as one step (microseconds)
   attn-llama8b        the Llama-3-8B-shaped verify layer (B1, 32/8 heads,
-                      prefix 2048, 64 nodes) - one call (split-prefix mode)
+                      prefix 2048, 64 nodes) - one call (split-prefix mode),
+                      timed as a replayed HIP graph of calls (the eager loop
+                      would time Python's per-call marshalling)
   attn-llama8b-x32    32 independent layers of that shape back to back
-                      (310 MB): the steady-state bandwidth the single call's
-                      launch latency hides
+                      (310 MB), one HIP graph per step: the steady-state
+                      bandwidth the single call's latency hides
   attn-longctx        long-context verify (B4, 32/8 heads, prefix 8192, 128
                       nodes of 10 levels)
   expand-twodrafter   two-drafter expansion: B8 trees of 256 nodes (a 5-step
@@ -148,6 +150,31 @@ def time_calls(torch, fn, steps, warmup):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / steps
+
+
+def time_graph(torch, fn, n_calls, reps, warmup):
+    """Milliseconds per replay of one HIP graph holding fn(0) .. fn(n_calls-1),
+    captured after one eager pass and replayed `warmup` times untimed, then
+    `reps` times between HIP events: the device time of calls whose Python
+    marshalling takes longer than the kernels, as a serving loop that
+    replays graphs sees it."""
+    for i in range(n_calls):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(n_calls):
+            fn(i)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps, g
 
 
 def kernel_times(tg, torch, fn, steps, start=0):
@@ -316,6 +343,22 @@ def attention_bench(tg, torch, dev, name, steps, warmup, cpu_s):
         tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
 
     ms = time_calls(torch, call, steps, warmup)
+    timing = {"timing": "eager calls"}
+    if name == "attn-llama8b":
+        # a call's Python marshalling outlasts its ~15 us of kernels: the
+        # eager loop measures the host, so the step is timed as one graph of
+        # the copies' calls, replayed; the replay must give the eager output
+        call(0)
+        torch.cuda.synchronize()
+        want = bufs[0][3].clone()
+        ms_eager = ms
+        ms_rep, graph = time_graph(torch, call, copies, max(1, steps), warmup)
+        ms = ms_rep / copies
+        if not torch.equal(bufs[0][3], want):
+            raise RuntimeError("graph replay of the verify call differs from the eager call")
+        del graph
+        timing = {"timing": f"one HIP graph of the {copies} input copies' calls, replayed "
+                            f"{max(1, steps)} times", "eager_ms_per_call": ms_eager}
     kern, _ = kernel_times(tg, torch, call, steps, start=0)
     call(0)                       # copy 0's output for the parity margin
     torch.cuda.synchronize()
@@ -352,7 +395,7 @@ def attention_bench(tg, torch, dev, name, steps, warmup, cpu_s):
                 "input_copies": copies},
                roof, dt, **{"TB/s": nbytes / call_s / 1e12, "TFLOP/s": flops / call_s / 1e12,
                             "bytes": nbytes, "flops": flops,
-                            "kernels": kernels_json(kern, steps)})
+                            "kernels": kernels_json(kern, steps)}, **timing)
     if cpu_s > 0:
         f_cpu, b_cpu, t_cpu, done, parity = attn_cpu_baseline(name, par, bufs[0], cpu_s)
         out["cpu_baseline"] = {
@@ -382,7 +425,17 @@ def attention_layers_bench(tg, torch, dev, steps, warmup, cpu_s, layers=32):
         for q, k, v, o in bufs:
             tg.verify_attention(q, k, v, parent, plen, Dh ** -0.5, out=o, workspace=ws)
 
-    ms = time_calls(torch, step, steps, warmup)
+    # the step as one HIP graph of its 32 calls, replayed (the eager loop is
+    # bound by the calls' Python marshalling); a replay must give the eager
+    # outputs
+    ms_eager = time_calls(torch, step, steps, warmup)
+    want = [b[3].clone() for b in bufs]
+    ms, graph = time_graph(torch, lambda i: tg.verify_attention(
+        bufs[i][0], bufs[i][1], bufs[i][2], parent, plen, Dh ** -0.5, out=bufs[i][3],
+        workspace=ws), layers, steps, warmup)
+    if not all(torch.equal(b[3], w) for b, w in zip(bufs, want)):
+        raise RuntimeError("graph replay of the 32 verify calls differs from the eager calls")
+    del graph
     kern, _ = kernel_times(tg, torch, step, max(2, steps // 4))
     nb1, fl1 = attn_work(name, par)
     nbytes, flops = layers * nb1, layers * fl1
@@ -396,7 +449,9 @@ def attention_layers_bench(tg, torch, dev, steps, warmup, cpu_s, layers=32):
                             f"heads, D{Dh}, prefix {Lp}, {Nn} tree nodes, bf16)",
                 "layers": layers}, roof, "bf16",
                **{"TFLOP/s": flops / (ms * 1e-3) / 1e12, "bytes": nbytes, "flops": flops,
-                  "kernels": kernels_json(kern, max(2, steps // 4))})
+                  "kernels": kernels_json(kern, max(2, steps // 4)),
+                  "timing": f"one HIP graph of the {layers} calls, replayed {steps} times",
+                  "eager_ms_per_step": ms_eager})
     if cpu_s > 0:
         f_cpu, b_cpu, t_cpu, done, parity = attn_cpu_baseline(name, par, bufs[0], cpu_s)
         out["cpu_baseline"] = {"value": b_cpu / t_cpu / 1e12, "unit": "TB/s",

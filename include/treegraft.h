@@ -141,7 +141,8 @@ tg_status tg_tree_reset(const tg_tree *tree, int B, void *stream);
  * prefix_len [B] int32 (device), L_b >= 0 and L_b + N <= S_max
  * out        [B, N, Hq, D]       dtype (fp32 accumulation inside)
  * D in {64, 128}; Hq % Hkv == 0; 1 <= N <= TG_MAX_VERIFY_NODES;
- * sm_scale finite and >= 0 (else TG_ERR_INVALID_ARG).
+ * sm_scale finite and >= 0; q, k_cache, v_cache and out 16-byte aligned
+ * (else TG_ERR_INVALID_ARG).
  * dtype TG_BF16 runs the MFMA kernel; TG_F32 runs an fp32 VALU kernel.
  * Device errors: BAD_PARENT (that parent read as -1), BAD_PREFIX (zeros).
  */

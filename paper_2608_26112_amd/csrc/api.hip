@@ -2,6 +2,7 @@
 // Every call is asynchronous on the caller's stream and allocates nothing.
 #include <hip/hip_runtime.h>
 
+#include <initializer_list>
 #include <mutex>
 
 #include "../../include/treegraft.h"
@@ -82,6 +83,9 @@ tg_status verify_attention_args(const void *q, const void *k_cache, const void *
                                 tg_dtype dtype) {
   if (!q || !k_cache || !v_cache || !parent || !prefix_len || !out)
     return TG_ERR_INVALID_ARG;
+  // the kernels move q, the caches and out in 16-byte vectors
+  for (const void *p : {q, k_cache, v_cache, static_cast<const void *>(out)})
+    if (reinterpret_cast<uintptr_t>(p) & 15) return TG_ERR_INVALID_ARG;
   if (B <= 0 || N <= 0 || Hq <= 0 || Hkv <= 0 || S_max < N) return TG_ERR_INVALID_ARG;
   if (Hq % Hkv) return TG_ERR_INVALID_ARG;
   // a finite, non-negative softmax scale (the kernels take each row's

@@ -94,6 +94,86 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
 
+// One global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l's bytes land at LDS byte address lds_base + 16 l, lds_base wave-
+// uniform.  Written as assembly so the compiler does not track it: a kernel
+// that uses it orders its LDS reads after these copies with explicit waits
+// (vmcnt) and barriers.  M0 is saved and restored around the copy.
+__device__ __forceinline__ void dma16(const void *gaddr, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gaddr), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory");
+}
+
+// Workgroup barrier for LDS data: waits for this wave's LDS accesses
+// (lgkmcnt 0; vmcnt and expcnt at their maxima, i.e. no wait), not for its
+// global loads in flight, which __syncthreads() would also wait for through
+// its release fence.  The "memory" clobber keeps the compiler from moving
+// memory operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Write-out of one wave's 32 query rows (lane (h, r) holds O^T of row r in
+// the 32x32 MFMA output layout: d = 32 db + 8 j + 4 h + i in o[db][4 j + i]).
+// The rows, scaled by `inv` and rounded to bf16, pass through `stage` (32 x D
+// bf16 of LDS that only this wave uses) so that every global store writes
+// whole 16-byte chunks, D / 8 lanes per row, instead of 8-byte pieces of 32
+// different rows.  8-byte slots are XOR-swizzled by row so that both the
+// writes (32 rows, one slot) and the reads (whole rows) are conflict-free.
+// Row r of the wave is query row row_first + r, i.e. node (row_first + r) / G
+// and head g G + (row_first + r) % G; it goes to
+// dst + ((row_off + node) Hq + head) D, and only if row_first + r < rows_total.
+template <int D>
+__device__ __forceinline__ void store_rows(const f32x16 (&o)[D / 32], float inv, __bf16 *stage,
+                                           __bf16 *__restrict__ dst, size_t row_off,
+                                           int row_first, int rows_total, int G, int g, int Hq) {
+  constexpr int DB = D / 32;
+  constexpr int CPR = D / 8;       // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;    // rows per read instruction
+  const int lane = threadIdx.x & (kWave - 1);
+  const int h = lane >> 5, r32 = lane & 31;
+  auto swz = [](int r) { return D == 128 ? (r & 31) : ((r >> 1) & 15); };
+  const int f = swz(r32);
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int slot = (db * 8 + 2 * j + h) ^ f;  // 8-byte slot (4 bf16)
+      *reinterpret_cast<bf16x4 *>(stage + r32 * D + 4 * slot) =
+          bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
+                 (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
+    }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int c = lane % CPR;
+#pragma unroll
+  for (int it = 0; it < 32 / RPI; ++it) {
+    const int r = it * RPI + lane / CPR;
+    const int fr = swz(r);
+    // logical slots 2c, 2c+1 sit in physical chunk c ^ (fr >> 1), swapped
+    // when fr is odd
+    bf16x8 v = *reinterpret_cast<const bf16x8 *>(stage + r * D + 8 * (c ^ (fr >> 1)));
+    if (fr & 1) v = __builtin_shufflevector(v, v, 4, 5, 6, 7, 0, 1, 2, 3);
+    const int qrow = row_first + r;
+    if (qrow < rows_total) {
+      const int node = qrow / G, head = g * G + (qrow - node * G);
+      *reinterpret_cast<bf16x8 *>(dst + ((row_off + node) * Hq + head) * D + 8 * c) = v;
+    }
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ kc,
@@ -110,12 +190,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   // flight into one stage do not alias reads of the other
   __shared__ __attribute__((aligned(16))) __bf16 stage0[Lds::STAGE];
   __shared__ __attribute__((aligned(16))) __bf16 stage1[Lds::STAGE];
+  // dynamic: the bitsets of the tile's nodes, then the parent array
   extern __shared__ __attribute__((aligned(16))) uint32_t anc_s[];
-  int *par_s = reinterpret_cast<int *>(stage1);  // prologue only
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int h = lane >> 5, r32 = lane & 31;
   const int G = Hq / Hkv;
+  const int NW = (N + 31) >> 5;
+  int *par_s = reinterpret_cast<int *>(anc_s + min(N, (BM + G - 1) / G + 1) * NW);
 
   // ---- block -> (b, g, split, tile); tiles of one K/V stream share an XCD
   const int total = gridDim.x;
@@ -130,7 +212,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
 
   // Every global read of the prologue is issued before the first one is
   // waited for: the prefix length, this thread's parents (at most
-  // TG_MAX_VERIFY_NODES / kThreads of them) and its Q fragment.
+  // TG_MAX_VERIFY_NODES / kThreads of them) and its Q fragment.  All of them
+  // are consumed before the first tile is requested, so no later wait for a
+  // register operand can cover the tile loads.
   const int L = prefix_len[b];
   const int rows_total = N * G;
   const int row0 = tile * BM;
@@ -151,7 +235,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+      qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
   if (bad_prefix(L, N, S_max)) {
     if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
@@ -203,20 +287,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     grow[i] = row;
     goff[i] = row * D + chunk * 8;
   }
+  // The copies are assembly (dma16), invisible to the compiler's waits: the
+  // compiler, tracking them, made tile t's fragment reads wait for tile
+  // t + 1's copies.  Every read of a stage follows an explicit wait for its
+  // copies and a barrier.
   auto issue = [&](int t, __bf16 *dst) {
     const int k0 = tile_k0(t), lim = tile_lim(t);
     const __bf16 *kt = kb + (size_t)k0 * D;  // wave-uniform tile base
     const __bf16 *vt = vb + (size_t)k0 * D;
-    __bf16 *dk = dst;
-    __bf16 *dv = dst + Lds::TILE;
+    const uint32_t dk = lds_addr(dst), dv = lds_addr(dst + Lds::TILE);
     auto one = [&](int i, int off) {
-      const int blk_off = (w * LOADS + i) * 512;   // 1 KB block, in bf16 elements
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void *)(kt + off),
-          (__attribute__((address_space(3))) void *)(dk + blk_off), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void *)(vt + off),
-          (__attribute__((address_space(3))) void *)(dv + blk_off), 16, 0, 0);
+      const uint32_t blk = (w * LOADS + i) * 1024;   // 1 KB block
+      dma16(kt + off, dk + blk);
+      dma16(vt + off, dv + blk);
     };
     if (k0 + BN <= lim) {
 #pragma unroll
@@ -229,13 +312,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     }
   };
 
-  // tile 0 streams in while the prologue runs
-  if (n_tiles_all > 0) issue(0, stage0);
-
-  // ---- parents and ancestor-or-self bitsets of this tile's nodes (a1)
-  const int node_hi = min(N, (row0 + BM - 1) / G + 1);
-  const int nloc = node_hi - node_lo;
-  const int NW = (N + 31) >> 5;
+  // ---- parents into LDS; then nothing read into registers is in flight
   bool badp = false;
 #pragma unroll
   for (int k = 0; k < kParPerThread; ++k) {
@@ -250,24 +327,41 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     }
   }
   if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): Q, parents (expcnt, lgkmcnt: no wait)
+
+  // tiles 0 and 1 stream in while the bitsets are built
+  if (n_tiles_all > 0) issue(0, stage0);
+  if (n_tiles_all > 1) issue(1, stage1);
+
+  // ---- ancestor-or-self bitsets of this tile's nodes (a1)
+  const int node_hi = min(N, (row0 + BM - 1) / G + 1);
+  const int nloc = node_hi - node_lo;
   for (int i = tid; i < nloc * NW; i += kThreads) anc_s[i] = 0;
-  __syncthreads();
+  lds_barrier();
   if (tid < nloc) {
     uint32_t *row = anc_s + tid * NW;
     for (int u = node_lo + tid; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
   }
-  __syncthreads();  // bitsets ready; par_s (stage 1) free again
 
-  // ---- this lane's query row (its Q fragment is already in flight)
+  // ---- this lane's query row: its ancestor-or-self bitset
   const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
 
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  // the bitsets are complete and tile 0 has landed (this wave's part of it:
+  // tile 1's 2 LOADS younger loads may stay in flight), in every wave
+  if (n_tiles_all > 1)
+    __builtin_amdgcn_s_waitcnt((2 * LOADS) | (7 << 4));
+  else
+    __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 
   auto step = [&](int t, const __bf16 *cur, __bf16 *nxt) {
     const __bf16 *Kt = cur;
     const __bf16 *Vt = cur + Lds::TILE;
-    if (t + 1 < n_tiles_all) issue(t + 1, nxt);  // lands in LDS while tile t computes
+    // tile t + 1 lands in LDS while tile t computes (tile 1 was requested
+    // by the prologue)
+    if (t >= 1 && t + 1 < n_tiles_all) issue(t + 1, nxt);
     const bool tree_tile = tree_tile_at(t);
     const int k0 = tile_k0(t);
     const int k_lim = tile_lim(t);
@@ -394,43 +488,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   };
-  // unrolled by two so each half reads and fills fixed stages
-  for (int t = 0; t < n_tiles_all; t += 2) {
-    step(t, stage0, stage1);
-    if (t + 1 < n_tiles_all) step(t + 1, stage1, stage0);
+  // Tile 0 peeled (tile 1's loads, from the prologue, are in flight while it
+  // computes); then unrolled by two so each half reads and fills fixed stages.
+  if (n_tiles_all > 0) step(0, stage0, stage1);
+  for (int t = 1; t < n_tiles_all; t += 2) {
+    step(t, stage1, stage0);
+    if (t + 1 < n_tiles_all) step(t + 1, stage0, stage1);
   }
 
-  // ---- finalize
+  // ---- finalize: every wave is past its last read of the stages (the
+  // last step ends with a barrier), so wave w stages its rows in stage 0
   const float lt = l + __shfl_xor(l, 32, 64);
-  if (!qvalid) return;
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-  if (n_splits == 1) {
-    __bf16 *op = out + (((size_t)b * N + qnode) * Hq + qhead) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = db * 32 + 8 * j + 4 * h;
-        bf16x4 v4 = bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
-                           (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
-        *reinterpret_cast<bf16x4 *>(op + d) = v4;
-      }
-    }
-  } else {
-    const size_t prow = (((size_t)split * B + b) * N + qnode) * Hq + qhead;
-    __bf16 *op = part_o + prow * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = db * 32 + 8 * j + 4 * h;
-        *reinterpret_cast<bf16x4 *>(op + d) =
-            bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
-                   (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
-      }
-    }
-    if (h == 0) part_lse[prow] = lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
-  }
+  const bool split_mode = n_splits > 1;
+  store_rows<D>(o, inv, stage0 + w * 32 * D, split_mode ? part_o : out,
+                split_mode ? ((size_t)split * B + b) * N : (size_t)b * N, row0 + w * 32,
+                rows_total, G, g, Hq);
+  if (split_mode && qvalid && h == 0)
+    part_lse[(((size_t)split * B + b) * N + qnode) * Hq + qhead] =
+        lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
 }
 
 // --------------------------------------------- bf16, ping-pong schedule
@@ -523,7 +599,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     const __bf16 *qp = q + (((size_t)b * N + qnode) * Hq + qhead) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      qf[s] = qvalid ? *reinterpret_cast<const bf16x8 *>(qp + 16 * s) : bf16x8{};
+      qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
   if (bad_prefix(L, N, S_max)) {
     if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
@@ -580,15 +656,8 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
   };
 
-  // the first tiles stream in while the prologue runs
-  if (n > 0) issue(kb, 0, kst0);
-  if (n > 1) issue(kb, 1, kst1);
-  if (n > 0) issue(vb, 0, vst0);
-
-  // ---- ancestor-or-self bitsets of this tile's nodes (a1)
-  const int node_hi = min(N, (row0 + BMP - 1) / G + 1);
-  const int nloc = node_hi - node_lo;
-  const int NW = (N + 31) >> 5;
+  // ---- parents into LDS; then nothing read into registers is in flight,
+  // so no later wait for a register operand can cover the tile loads
   bool badp = false;
 #pragma unroll
   for (int k = 0; k < kParPerThread; ++k) {
@@ -603,17 +672,27 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     }
   }
   if (badp && split == 0 && g == 0 && tile == 0) report(d_err, TG_DERR_BAD_PARENT);
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): Q, parents (expcnt, lgkmcnt: no wait)
+
+  // the first tiles stream in while the bitsets are built
+  if (n > 0) issue(kb, 0, kst0);
+  if (n > 1) issue(kb, 1, kst1);
+  if (n > 0) issue(vb, 0, vst0);
+
+  // ---- ancestor-or-self bitsets of this tile's nodes (a1)
+  const int node_hi = min(N, (row0 + BMP - 1) / G + 1);
+  const int nloc = node_hi - node_lo;
+  const int NW = (N + 31) >> 5;
   for (int i = tid; i < nloc * NW; i += NT) anc_s[i] = 0;
-  __syncthreads();
+  lds_barrier();  // the prologue's tile loads stay in flight
   for (int i = tid; i < nloc; i += NT) {
     uint32_t *row = anc_s + i * NW;
     for (int u = node_lo + i; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
   }
   bool lead = true;
   for (int i = 0; i < w; ++i) lead = lead && simd_s[i] != my_simd;
-  __syncthreads();
 
-  // ---- this lane's query row (its Q fragment is already in flight)
+  // ---- this lane's query row: its ancestor-or-self bitset
   const uint32_t *my_anc = anc_s + (qnode - node_lo) * NW;
 
   // Running row reference m (log2 units): the max of the row's first tile
@@ -890,8 +969,9 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // The bitsets are complete; of the prologue's loads (K(0), K(1), V(0) in
-  // that order) only K(0) is needed by pair 0, the rest land behind it.
+  // The bitsets are complete (this barrier also waits for the LDS accesses
+  // that built them); of the prologue's loads (K(0), K(1), V(0) in that
+  // order) only K(0) is needed by pair 0, the rest land behind it.
   bar_odd(n > 1 ? 2 * LOADS : LOADS);
   // One pair of phases per j (tile j's QK^T, tile j-1's PV).  Tile j's K sits
   // in stage j % 3 and its V in stage j % 3; phase 2j requests K(j+2) and
@@ -954,37 +1034,19 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     bar_odd(0);
   }
 
-  // ---- finalize
+  // ---- finalize: every wave is past its last read of the stages (the last
+  // pair ends with a barrier); waves 2i and 2i+1 stage their rows in the
+  // i-th of K stages 0-2 and V stage 0
   const float lt = l + half_swap(l);
-  if (!qvalid) return;
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-  if (n_splits == 1) {
-    __bf16 *op = out + (((size_t)b * N + qnode) * Hq + qhead) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = db * 32 + 8 * j + 4 * h;
-        bf16x4 v4 = bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
-                           (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
-        *reinterpret_cast<bf16x4 *>(op + d) = v4;
-      }
-    }
-  } else {
-    const size_t prow = (((size_t)split * B + b) * N + qnode) * Hq + qhead;
-    __bf16 *op = part_o + prow * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = db * 32 + 8 * j + 4 * h;
-        *reinterpret_cast<bf16x4 *>(op + d) =
-            bf16x4{(__bf16)(o[db][4 * j] * inv), (__bf16)(o[db][4 * j + 1] * inv),
-                   (__bf16)(o[db][4 * j + 2] * inv), (__bf16)(o[db][4 * j + 3] * inv)};
-      }
-    }
-    if (h == 0) part_lse[prow] = lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
-  }
+  const bool split_mode = n_splits > 1;
+  __bf16 *ost = (w >> 1) == 0 ? kst0 : (w >> 1) == 1 ? kst1 : (w >> 1) == 2 ? kst2 : vst0;
+  store_rows<D>(o, inv, ost + (w & 1) * 32 * D, split_mode ? part_o : out,
+                split_mode ? ((size_t)split * B + b) * N : (size_t)b * N, row0 + w * 32,
+                rows_total, G, g, Hq);
+  if (split_mode && qvalid && h == 0)
+    part_lse[(((size_t)split * B + b) * N + qnode) * Hq + qhead] =
+        lt > 0.0f ? m + __log2f(lt) : -__builtin_inff();
 }
 
 // Merge split partials: out = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M).
@@ -1248,7 +1310,9 @@ hipError_t launch_attn_bf16(const AttnShape &s, const void *q, const void *k,
   // bitset words of the nodes one row tile can hold
   const int bm = plan.pingpong ? 256 : BM;
   const int nodes_per_tile = std::min(s.N, (bm + G - 1) / G + 1);
-  const size_t lds = (size_t)nodes_per_tile * ((s.N + 31) / 32) * 4;
+  // (the 4-wave kernel keeps the parent array after them)
+  const size_t lds = (size_t)nodes_per_tile * ((s.N + 31) / 32) * 4 +
+                     (plan.pingpong ? 0 : (size_t)s.N * 4);
   auto go = [&](auto kernel, const char *name, int threads) {
     hipError_t r = hipFuncSetAttribute((const void *)kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

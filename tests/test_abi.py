@@ -92,6 +92,9 @@ def test_verify_attention_host_checks(lib):
     assert _verify(lib, scale=float("nan")) == tg.ERR_INVALID_ARG
     assert _verify(lib, scale=-0.125) == tg.ERR_INVALID_ARG
     assert _verify(lib, scale=float("inf")) == tg.ERR_INVALID_ARG
+    # q, the caches and out are read / written in 16-byte vectors
+    for arg in ("q", "k", "v", "out"):
+        assert _verify(lib, **{arg: ctypes.c_void_p(256 + 8)}) == tg.ERR_INVALID_ARG
     # a shape that needs a split workspace, called without one
     need = lib.tg_verify_attention_workspace(1, 64, 32, 8, 128, 2112, tg.BF16)
     assert need > 0
