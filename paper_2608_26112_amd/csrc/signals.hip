@@ -9,8 +9,9 @@
 // closure D_C as bitsets over depth, the candidate set R (root included) as
 // node keys ranked by counting (a sort past 1024 keys) for the preview
 // Top_W(R, s), and one block reduction of all sums.  Wave 0 then evaluates
-// the 3,265-parameter MLP alone (no block barriers): a lane per hidden unit,
-// fp32, fixed summation order.
+// the 3,265-parameter MLP alone (no block barriers), with its weights in
+// registers (loaded with the first batch): a lane per hidden unit, fp32,
+// fixed summation order.
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -27,18 +28,10 @@ constexpr int kH1 = 64, kH2 = 32;
 constexpr int kOffB1 = kH1 * kIn, kOffW2 = kOffB1 + kH1, kOffB2 = kOffW2 + kH2 * kH1;
 constexpr int kOffW3 = kOffB2 + kH2, kOffB3 = kOffW3 + kH2;
 constexpr int kParams = kOffB3 + 1;  // 3265
-constexpr int kParPer = (kParams + kThreads - 1) / kThreads;
 constexpr int kNodePer = 4;          // node fields a thread loads per batch
 constexpr int kMaxKeys = 2 * TG_MAX_CAP;  // pow2 >= cap + 1 (root)
 constexpr int kSums = 9;             // block sums
 
-// LDS position of parameter i: W2 is stored transposed ([64 inputs][32
-// units]) so the lanes of a layer-2 step read consecutive words.
-__device__ __forceinline__ int par_slot(int i) {
-  if (i < kOffW2 || i >= kOffB2) return i;
-  const int u = (i - kOffW2) / kH1, in = (i - kOffW2) - u * kH1;
-  return kOffW2 + in * kH2 + u;
-}
 
 __global__ __launch_bounds__(kThreads) void signals_kernel(
     tg_tree tree, const int32_t *__restrict__ frontier, const int32_t *__restrict__ n_frontier,
@@ -50,8 +43,8 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   __shared__ uint8_t inF[TG_MAX_CAP + 1];
   __shared__ uint32_t dF[(TG_MAX_CAP + 1 + 31) / 32], dC[(TG_MAX_CAP + 1 + 31) / 32];
   __shared__ float red[kSums + 2][kWaves];  // sums | frontier max | preview count
-  __shared__ float x_s[kIn], h1_s[kH1];
-  __shared__ float par_s[kParams];   // the predictor's weights (W2 transposed)
+  __shared__ __attribute__((aligned(16))) float x_s[kIn + 3];
+  __shared__ __attribute__((aligned(16))) float h1_s[kH1];
   __shared__ int dep_s[TG_MAX_CAP];
   __shared__ float cum_s[TG_MAX_CAP];
   __shared__ int bad_s;
@@ -69,14 +62,22 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   if (bad_n) n = 0;
   const int32_t *fr = frontier + (size_t)b * F;
 
-  // ---- one batch of global reads
-  float pv[kParPer];
-  if (params) {
+  // ---- one batch of global reads.  Wave 0's lanes hold the predictor's
+  // weights: lane u the 17 layer-1 weights and the bias of hidden unit u;
+  // lane u (half h = u / 32) the layer-2 weights of unit u % 32 on inputs
+  // 32 h .. 32 h + 31, that unit's bias and its layer-3 weight.
+  float w1[kIn], w2[kH1 / 2];
+  float b1 = 0.0f, b2 = 0.0f, w3 = 0.0f, b3 = 0.0f;
+  if (params && w == 0) {
 #pragma unroll
-    for (int j = 0; j < kParPer; ++j) {
-      const int i = tid + j * kThreads;
-      pv[j] = i < kParams ? params[i] : 0.0f;
-    }
+    for (int i = 0; i < kIn; ++i) w1[i] = params[lane * kIn + i];
+    b1 = params[kOffB1 + lane];
+    const int u = lane & (kH2 - 1), half = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < kH1 / 2; ++i) w2[i] = params[kOffW2 + u * kH1 + half * (kH1 / 2) + i];
+    b2 = params[kOffB2 + u];
+    w3 = params[kOffW3 + u];
+    b3 = params[kOffB3];
   }
   float ctx = 0.0f;
   if (params && tid < kCtx) ctx = context[(size_t)b * kCtx + tid];
@@ -97,14 +98,7 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
     inF[i] = 0;
   }
   for (int i = tid; i < DW; i += kThreads) dF[i] = dC[i] = 0;
-  if (params) {
-#pragma unroll
-    for (int j = 0; j < kParPer; ++j) {
-      const int i = tid + j * kThreads;
-      if (i < kParams) par_s[par_slot(i)] = pv[j];
-    }
-    if (tid < kCtx) x_s[tid] = ctx;
-  }
+  if (params && tid < kCtx) x_s[tid] = ctx;
 #pragma unroll
   for (int j = 0; j < kNodePer; ++j) {
     const int v = tid + j * kThreads;
@@ -262,8 +256,8 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   {
     float a = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kIn; ++i) a = fmaf(par_s[lane * kIn + i], x_s[i], a);
-    h1_s[lane] = fmaxf(a + par_s[kOffB1 + lane], 0.0f);
+    for (int i = 0; i < kIn; ++i) a = fmaf(w1[i], x_s[i], a);
+    h1_s[lane] = fmaxf(a + b1, 0.0f);
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -272,15 +266,12 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   // 32..63, added in that order
   const int u = lane & (kH2 - 1), half = lane >> 5;
   float a = 0.0f;
-#pragma unroll 8
-  for (int i = 0; i < kH1 / 2; ++i) {
-    const int in = half * (kH1 / 2) + i;
-    a = fmaf(par_s[kOffW2 + in * kH2 + u], h1_s[in], a);
-  }
+#pragma unroll
+  for (int i = 0; i < kH1 / 2; ++i) a = fmaf(w2[i], h1_s[half * (kH1 / 2) + i], a);
   const float hi_half = __shfl_down(a, 32, kWave);
-  const float h2 = fmaxf((a + hi_half) + par_s[kOffB2 + u], 0.0f);
+  const float h2 = fmaxf((a + hi_half) + b2, 0.0f);
   // layer 3
-  const float y = wave_sum_f32(lane < kH2 ? par_s[kOffW3 + u] * h2 : 0.0f) + par_s[kOffB3];
+  const float y = wave_sum_f32(lane < kH2 ? w3 * h2 : 0.0f) + b3;
   if (lane == 0) {
     margin[b] = y;
     action[b] = y > 0.0f ? 1 : 0;
