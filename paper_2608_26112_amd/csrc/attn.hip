@@ -211,11 +211,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   const int b = rest / Hkv;
 
   // Every global read of the prologue is issued before the first one is
-  // waited for: the prefix length, this thread's parents (at most
-  // TG_MAX_VERIFY_NODES / kThreads of them) and its Q fragment.  All of them
-  // are consumed before the first tile is requested, so no later wait for a
-  // register operand can cover the tile loads.
-  const int L = prefix_len[b];
+  // waited for: this thread's parents (at most TG_MAX_VERIFY_NODES / kThreads
+  // of them), its Q fragment and the prefix length.  All of them are consumed
+  // before the first tile is requested, so no later wait for a register
+  // operand can cover the tile loads.
   const int rows_total = N * G;
   const int row0 = tile * BM;
   constexpr int kParPerThread = (TG_MAX_VERIFY_NODES + kThreads - 1) / kThreads;
@@ -237,20 +236,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
     for (int s = 0; s < KS; ++s)
       qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
-  if (bad_prefix(L, N, S_max)) {
-    if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
-    if (n_splits == 1) {
-      for (int rr = w; rr < BM; rr += 4) {
-        int row = row0 + rr;
-        if (row >= rows_total) break;
-        int node = row / G, hq = g * G + row % G;
-        __bf16 *o = out + (((size_t)b * N + node) * Hq + hq) * D;
-        for (int d = lane; d < D; d += 64) o[d] = (__bf16)0.0f;
-      }
-    }
-    // split mode: attn_combine_kernel writes the zeros
-    return;
-  }
+  const int L_in = prefix_len[b];
+  // A prefix length out of range (BAD_PREFIX) runs no key tile: its rows
+  // leave as zeros (o = 0, l = 0), or in split mode as empty partials, which
+  // the combine turns into zeros.  No early return: the compiler would move
+  // the Q loads behind the prefix length's arrival.
+  const bool bad_len = bad_prefix(L_in, N, S_max);
+  if (bad_len && tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
+  const int L = bad_len ? 0 : L_in;
 
   // ---- key tiles: the prefix's 64-key tiles, then the tree's, dealt out to
   // the splits as equal runs (the tree's tiles weigh like any other)
@@ -258,7 +251,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   const int n_vt = n_pt + (N + BN - 1) / BN;
   const int per_split = (n_vt + n_splits - 1) / n_splits;
   const int vt0 = min(n_vt, split * per_split);
-  const int n_tiles_all = min(n_vt, vt0 + per_split) - vt0;
+  const int n_tiles_all = bad_len ? 0 : min(n_vt, vt0 + per_split) - vt0;
 
   const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
   const __bf16 *kb = kc + kv_base;
@@ -575,8 +568,7 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   const int b = rest / Hkv;
 
   // Every global read of the prologue is issued before the first one is
-  // waited for: the prefix length, this thread's parents and its Q fragment.
-  const int L = prefix_len[b];
+  // waited for: this thread's parents, its Q fragment and the prefix length.
   const int rows_total = N * G;
   const int row0 = tile * BMP;
   constexpr int kParPerThread = (TG_MAX_VERIFY_NODES + NT - 1) / NT;
@@ -601,26 +593,20 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
     for (int s = 0; s < KS; ++s)
       qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
-  if (bad_prefix(L, N, S_max)) {
-    if (tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
-    if (n_splits == 1) {
-      for (int rr = w; rr < BMP; rr += NT / 64) {
-        int row = row0 + rr;
-        if (row >= rows_total) break;
-        int node = row / G, hq = g * G + row % G;
-        __bf16 *o = out + (((size_t)b * N + node) * Hq + hq) * D;
-        for (int d = lane; d < D; d += 64) o[d] = (__bf16)0.0f;
-      }
-    }
-    return;
-  }
+  const int L_in = prefix_len[b];
+  // A prefix length out of range (BAD_PREFIX) runs no key tile: its rows
+  // leave as zeros, or in split mode as empty partials (no early return, as
+  // in attn_mfma_kernel)
+  const bool bad_len = bad_prefix(L_in, N, S_max);
+  if (bad_len && tid == 0 && split == 0 && tile == 0 && g == 0) report(d_err, TG_DERR_BAD_PREFIX);
+  const int L = bad_len ? 0 : L_in;
 
   // key tiles: the prefix's, then the tree's, dealt out as equal runs
   const int n_pt = (L + BN - 1) / BN;
   const int n_vt = n_pt + (N + BN - 1) / BN;
   const int per_split = (n_vt + n_splits - 1) / n_splits;
   const int vt0 = min(n_vt, split * per_split);
-  const int n = min(n_vt, vt0 + per_split) - vt0;
+  const int n = bad_len ? 0 : min(n_vt, vt0 + per_split) - vt0;
 
   const size_t kv_base = ((size_t)b * Hkv + g) * (size_t)S_max * D;
   const __bf16 *kb = kc + kv_base;
