@@ -329,11 +329,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(
   // ---- ancestor-or-self bitsets of this tile's nodes (a1)
   const int node_hi = min(N, (row0 + BM - 1) / G + 1);
   const int nloc = node_hi - node_lo;
-  for (int i = tid; i < nloc * NW; i += kThreads) anc_s[i] = 0;
-  lds_barrier();
-  if (tid < nloc) {
-    uint32_t *row = anc_s + tid * NW;
-    for (int u = node_lo + tid; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
+  lds_barrier();  // the parents are in LDS
+  // word j of node i's ancestor-or-self bitset, by one thread: it walks the
+  // chain (ids fall along it) down to the word's first id
+  for (int it = tid; it < nloc * NW; it += kThreads) {
+    const int i = it / NW, j = it - i * NW;
+    uint32_t word = 0;
+    for (int u = node_lo + i; u >= 32 * j; u = par_s[u])
+      if (u < 32 * (j + 1)) word |= 1u << (u & 31);
+    anc_s[it] = word;
   }
 
   // ---- this lane's query row: its ancestor-or-self bitset
@@ -669,11 +673,15 @@ __global__ __launch_bounds__(512, 1) void attn_pingpong_kernel(
   const int node_hi = min(N, (row0 + BMP - 1) / G + 1);
   const int nloc = node_hi - node_lo;
   const int NW = (N + 31) >> 5;
-  for (int i = tid; i < nloc * NW; i += NT) anc_s[i] = 0;
-  lds_barrier();  // the prologue's tile loads stay in flight
-  for (int i = tid; i < nloc; i += NT) {
-    uint32_t *row = anc_s + i * NW;
-    for (int u = node_lo + i; u >= 0; u = par_s[u]) row[u >> 5] |= 1u << (u & 31);
+  lds_barrier();  // the parents are in LDS; the prologue's tile loads stay in flight
+  // word j of node i's ancestor-or-self bitset, by one thread (as in
+  // attn_mfma_kernel)
+  for (int it = tid; it < nloc * NW; it += NT) {
+    const int i = it / NW, j = it - i * NW;
+    uint32_t word = 0;
+    for (int u = node_lo + i; u >= 32 * j; u = par_s[u])
+      if (u < 32 * (j + 1)) word |= 1u << (u & 31);
+    anc_s[it] = word;
   }
   bool lead = true;
   for (int i = 0; i < w; ++i) lead = lead && simd_s[i] != my_simd;
