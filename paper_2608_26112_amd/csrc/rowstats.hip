@@ -70,8 +70,10 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
 
 // The K-th and the kq-th largest (kq <= K <= 64) of the wave's values, ties
 // counted: at least K (kq) lanes hold a value >= tK (tq); -inf when fewer
-// lanes hold finite values.  Small K: rounds of "take the wave maximum,
-// retire the lanes holding it"; larger K: a bitonic sort of the wave.
+// lanes hold finite values.  Larger K: a bitonic sort of the wave gives
+// both.  Small K: only tq, by kq rounds of "take the wave maximum, retire
+// the lanes holding it" (tK stays -inf): the K rounds for tK took longer
+// than the few extra candidates the looser bound lets through.
 __device__ __forceinline__ void wave_order_stats(float v, int K, int kq, int lane, float &tK,
                                                  float &tq) {
   const float ninf = -__builtin_inff();
@@ -84,14 +86,12 @@ __device__ __forceinline__ void wave_order_stats(float v, int K, int kq, int lan
     return;
   }
   int taken = 0;
-  for (int j = 0; j < K && taken < K; ++j) {
+  for (int j = 0; j < kq && taken < kq; ++j) {
     const float mx = wave_max_f32(v);
     if (mx == ninf) return;
     const bool hit = v == mx;
-    const int before = taken;
     taken += __popcll(__ballot(hit));
-    if (before < kq && taken >= kq) tq = mx;
-    if (taken >= K) tK = mx;
+    if (taken >= kq) tq = mx;
     v = hit ? ninf : v;
   }
 }
@@ -175,14 +175,15 @@ __device__ __noinline__ void grain_bisect_topk(const float *__restrict__ row, in
 //  2. one (max, sum-exp) partial per grain, waves by a fixed DPP tree,
 //     then the four waves in order: the same bits whatever the chunking;
 //  3. a lower bound T on the grain's K-th largest logit from the thread
-//     maxima, each wave on its own: the largest over waves of a wave's K-th
-//     largest maximum (K threads hold an element >= it), and the smallest
-//     over waves of a wave's ceil(K/4)-th largest (every wave then holds
-//     ceil(K/4) elements >= it); the larger of the two, raised to the
-//     running chunk list's K-th entry;
-//  4. elements >= T are compacted into LDS (about K of them for continuous
-//     logits); with more than kCandCap (heavy ties) the grain's exact K-th
-//     key is found by bisection over the key bits instead (out of line);
+//     maxima, each wave on its own: the smallest over waves of a wave's
+//     ceil(K/4)-th largest (every wave then holds ceil(K/4) elements >= it),
+//     for K > 16 raised to the largest over waves of a wave's K-th largest
+//     maximum (K threads hold an element >= it), and to the running chunk
+//     list's K-th entry;
+//  4. elements >= T are compacted into LDS (a few times K of them for
+//     continuous logits); with more than kCandCap (heavy ties) the grain's
+//     exact K-th key is found by bisection over the key bits instead (out of
+//     line);
 //  5. the running list and the candidates are ranked by (logit desc, token
 //     asc) and the best K kept.
 __global__ __launch_bounds__(kThreads) void row_partial_kernel(
@@ -333,8 +334,12 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     for (int t = r0 + tid; t < total; t += kThreads) {
       const uint64_t key = cand[t];
       if (key == 0) continue;
-      int rank = 0;
-      for (int u = r0; u < total; ++u) rank += cand[u] > key;
+      int rank = 0, u = r0;
+      for (; u + 4 <= total; u += 4) {  // four reads in flight
+        const uint64_t a0 = cand[u], a1 = cand[u + 1], a2 = cand[u + 2], a3 = cand[u + 3];
+        rank += (int)(a0 > key) + (int)(a1 > key) + (int)(a2 > key) + (int)(a3 > key);
+      }
+      for (; u < total; ++u) rank += cand[u] > key;
       if (rank < K) run[rank] = key;
     }
     __syncthreads();
