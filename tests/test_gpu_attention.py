@@ -84,6 +84,32 @@ def test_random_small(tg, N, kind, dtype):
         C.attn_close_f32(got, want)
 
 
+@pytest.mark.parametrize("Hq,Hkv,N,L,D,kernel", [
+    (6, 2, 77, 300, 128, "attn_mfma"),      # 3 query heads per KV head
+    (10, 2, 41, 130, 64, "attn_mfma"),      # 5
+    (6, 2, 90, 4200, 128, "attn_pingpong"),  # 270 rows, prefix >= 4096
+    (15, 3, 60, 4100, 64, "attn_pingpong"),  # 5 per KV head, 300 rows
+])
+def test_group_sizes_not_powers_of_two(tg, Hq, Hkv, N, L, D, kernel):
+    """Query heads per KV head that are not powers of two: a wave's 32 output
+    rows then straddle nodes at any row, and each row leaves to its own
+    (node, head).  Ragged per-sequence prefixes; the route is asserted."""
+    g = W.rng(7000 + Hq * 100 + N)
+    B = 2
+    plen = np.array([L, L - 37], np.int32)
+    parent = np.stack([W.uniform_parents(g, N) for _ in range(B)])
+    q, k, v = _gen(7001 + N, B, N, Hq, Hkv, D, L)
+    torch.cuda.synchronize()
+    tg.trace_begin(16)
+    try:
+        got, q, k, v = _run(tg, q, k, v, parent, plen, D ** -0.5, torch.bfloat16)
+    finally:
+        names = [n for n, _ in tg.trace_end()]
+    assert kernel in names, names
+    want = tree_verify_attention_fast(q, k, v, parent, plen, D ** -0.5)
+    C.attn_close_bf16(got, want)
+
+
 @pytest.mark.parametrize("kind", ["random", "chain"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_largest_tree_1024_nodes(tg, kind, dtype):
