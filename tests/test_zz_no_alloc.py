@@ -26,7 +26,7 @@ def _inputs(seed, B, N, Hq, Hkv, D, L, dtype):
 
 
 @pytest.mark.parametrize("shapes", [
-    # Llama-3-8B-shaped layer (17 splits), then a smaller split-mode call
+    # Llama-3-8B-shaped layer (11 splits), then a smaller split-mode call
     [(1, 64, 32, 8, 128, 2048), (2, 17, 8, 2, 64, 1000)],
     # long-context-shaped (ping-pong kernel, 4 splits), then the 8B shape
     [(4, 128, 32, 8, 128, 8192), (1, 64, 32, 8, 128, 2048)],
