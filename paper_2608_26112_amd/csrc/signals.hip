@@ -8,10 +8,11 @@
 // front; then child counts, the frontier's depth set D_F and its lookback
 // closure D_C as bitsets over depth, the candidate set R (root included) as
 // node keys ranked by counting (a sort past 1024 keys) for the preview
-// Top_W(R, s), and one block reduction of all sums.  Wave 0 then evaluates
-// the 3,265-parameter MLP alone (no block barriers), with its weights in
-// registers (loaded with the first batch): a lane per hidden unit, fp32,
-// fixed summation order.
+// Top_W(R, s), and the sums: by wave 0 alone when the frontier and the
+// preview fit in a wave (the other waves hand over their candidate counts),
+// else one block reduction.  Wave 0 then evaluates the 3,265-parameter MLP
+// alone (no block barriers), with its weights in registers (loaded with the
+// first batch): a lane per hidden unit, fp32, fixed summation order.
 #include "tg_device.h"
 #include "tg_kernels.h"
 
@@ -43,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   __shared__ uint8_t inF[TG_MAX_CAP + 1];
   __shared__ uint32_t dF[(TG_MAX_CAP + 1 + 31) / 32], dC[(TG_MAX_CAP + 1 + 31) / 32];
   __shared__ float red[kSums + 2][kWaves];  // sums | frontier max | preview count
-  __shared__ __attribute__((aligned(16))) float x_s[kIn + 3];
+  __shared__ __attribute__((aligned(16))) float x_s[kCtx + 1];
   __shared__ __attribute__((aligned(16))) float h1_s[kH1];
   __shared__ int dep_s[TG_MAX_CAP];
   __shared__ float cum_s[TG_MAX_CAP];
@@ -173,8 +174,18 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
     sums[3] += cum_of(v) > ninf ? 1.0f : 0.0f;
     mx = fmaxf(mx, d);
   }
+  // With at most a wave's width of frontier and preview slots (the usual
+  // case) every sum but the candidate count comes from wave 0 alone, which
+  // then finishes the call: the other waves hand over their counts and leave
+  // after the ranking.
+  const bool one_wave = F <= kWave && W <= kWave;
+  if (one_wave) {
+    const float c0 = wave_sum_f32(sums[0]);
+    if (lane == 0) red[0][w] = c0;
+  }
   __syncthreads();
   block_top_keys<kThreads>(key, n + 1, P2, W);
+  if (one_wave && w != 0) return;
 
   // ---- preview frontier: the present keys among the first W
   float nh_f = 0.0f;
@@ -193,70 +204,87 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
       sums[8] += c;
     }
   }
-  // ---- one block reduction (waves by a DPP tree, then the waves in order)
+  // ---- totals, the same in every lane of wave 0: waves by a DPP tree, then
+  // the waves in order
+  float t[kSums], fmx;
+  int nh;
+  if (one_wave) {
+    t[0] = red[0][0];
+    for (int j = 1; j < kWaves; ++j) t[0] += red[0][j];
 #pragma unroll
-  for (int i = 0; i < kSums; ++i) {
-    const float t = wave_sum_f32(sums[i]);
-    if (lane == 0) red[i][w] = t;
-  }
-  {
-    const float t = wave_max_f32(mx);
-    if (lane == 0) red[kSums][w] = t;
-  }
-  {
-    const float t = wave_sum_f32(nh_f);
-    if (lane == 0) red[kSums + 1][w] = t;
-  }
-  __syncthreads();
-  if (w != 0) return;
-  if (tid == 0) {
-    float t[kSums];
+    for (int i = 1; i < kSums; ++i) t[i] = wave_sum_f32(sums[i]);
+    fmx = wave_max_f32(mx);
+    nh = (int)wave_sum_f32(nh_f);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSums; ++i) {
+      const float r = wave_sum_f32(sums[i]);
+      if (lane == 0) red[i][w] = r;
+    }
+    {
+      const float r = wave_max_f32(mx);
+      if (lane == 0) red[kSums][w] = r;
+    }
+    {
+      const float r = wave_sum_f32(nh_f);
+      if (lane == 0) red[kSums + 1][w] = r;
+    }
+    __syncthreads();
+    if (w != 0) return;
     for (int i = 0; i < kSums; ++i) {
       t[i] = red[i][0];
       for (int j = 1; j < kWaves; ++j) t[i] += red[i][j];
     }
-    float fmx = red[kSums][0];
+    fmx = red[kSums][0];
     for (int j = 1; j < kWaves; ++j) fmx = fmaxf(fmx, red[kSums][j]);
-    int nh = 0;
+    nh = 0;
     for (int j = 0; j < kWaves; ++j) nh += (int)red[kSums + 1][j];
-    const float nan = __builtin_nanf("");
-    const float nf = (float)Fb;
-    const float mean_f = Fb > 0 ? t[1] / nf : nan;
-    const float mean_h = nh > 0 ? t[4] / (float)nh : nan;
-    const float delta = mean_h - mean_f;
-    float s[kSigs];
-    s[0] = mean_f;                                  // depth_before
-    s[1] = Fb > 0 ? t[2] / nf : nan;                // leaf_ratio_before
-    s[2] = delta;                                   // pre_reselect_depth_delta
-    s[3] = t[0];                                    // pre_reselect_cands
-    s[4] = Fb > 0 ? fmx : nan;                      // max_depth_before
-    s[5] = delta == delta ? fmaxf(0.0f, -delta) : nan;  // collapse_debt
-    s[6] = nh > 0 ? t[5] / (float)nh : nan;         // pre_reselect_past_ratio
-    s[7] = nh > 0 ? t[6] / (float)nh : nan;         // pre_reselect_overlap
-    s[8] = t[7] > 0.0f ? t[8] / t[7] : nan;         // pre_reselect_score
-    s[9] = Fb > 0 ? t[3] / nf : nan;                // finite_score_ratio_before
-    if (bad) {
-      for (int i = 0; i < kSigs; ++i) s[i] = nan;
-      report(d_err, TG_DERR_BAD_NODE);
-    }
-    for (int i = 0; i < kSigs; ++i) signals[(size_t)b * kSigs + i] = s[i];
-    x_s[11] = s[0];  // depth_before
-    x_s[12] = s[1];  // leaf_ratio_before
-    x_s[13] = s[5];  // collapse_debt
-    x_s[14] = s[6];  // pre_reselect_past_ratio
-    x_s[15] = s[7];  // pre_reselect_overlap
-    x_s[16] = s[8];  // pre_reselect_score
+  }
+  const float nan = __builtin_nanf("");
+  const float nf = (float)Fb;
+  const float mean_f = Fb > 0 ? t[1] / nf : nan;
+  const float mean_h = nh > 0 ? t[4] / (float)nh : nan;
+  const float delta = mean_h - mean_f;
+  float sg[kSigs];
+  sg[0] = mean_f;                                  // depth_before
+  sg[1] = Fb > 0 ? t[2] / nf : nan;                // leaf_ratio_before
+  sg[2] = delta;                                   // pre_reselect_depth_delta
+  sg[3] = t[0];                                    // pre_reselect_cands
+  sg[4] = Fb > 0 ? fmx : nan;                      // max_depth_before
+  sg[5] = delta == delta ? fmaxf(0.0f, -delta) : nan;  // collapse_debt
+  sg[6] = nh > 0 ? t[5] / (float)nh : nan;         // pre_reselect_past_ratio
+  sg[7] = nh > 0 ? t[6] / (float)nh : nan;         // pre_reselect_overlap
+  sg[8] = t[7] > 0.0f ? t[8] / t[7] : nan;         // pre_reselect_score
+  sg[9] = Fb > 0 ? t[3] / nf : nan;                // finite_score_ratio_before
+  if (bad) {
+#pragma unroll
+    for (int i = 0; i < kSigs; ++i) sg[i] = nan;
+    if (lane == 0) report(d_err, TG_DERR_BAD_NODE);
+  }
+  {
+    float mine = sg[0];
+#pragma unroll
+    for (int i = 1; i < kSigs; ++i) mine = lane == i ? sg[i] : mine;
+    if (lane < kSigs) signals[(size_t)b * kSigs + lane] = mine;
   }
   if (!params) return;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  // ---- margin predictor: W1[64,17] b1[64] W2[32,64] b2[32] W3[1,32] b3[1]
+  // ---- margin predictor: W1[64,17] b1[64] W2[32,64] b2[32] W3[1,32] b3[1];
+  // inputs: the context, then depth_before, leaf_ratio_before, collapse_debt,
+  // pre_reselect_past_ratio, pre_reselect_overlap, pre_reselect_score
+  float xin[kIn];
+#pragma unroll
+  for (int i = 0; i < kCtx; ++i) xin[i] = x_s[i];
+  xin[11] = sg[0];
+  xin[12] = sg[1];
+  xin[13] = sg[5];
+  xin[14] = sg[6];
+  xin[15] = sg[7];
+  xin[16] = sg[8];
   // layer 1: lane u is unit u
   {
     float a = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kIn; ++i) a = fmaf(w1[i], x_s[i], a);
+    for (int i = 0; i < kIn; ++i) a = fmaf(w1[i], xin[i], a);
     h1_s[lane] = fmaxf(a + b1, 0.0f);
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -295,60 +295,75 @@ __device__ __forceinline__ void wave_key_order_stats(uint64_t v, int k, int kq, 
 }
 
 // block_top_keys for a small k against a larger set (n <= kRankPerThread *
-// kBlock): a lower bound T on the k-th largest key from the thread maxima,
-// each wave on its own (the largest over waves of a wave's k-th largest
-// maximum; the smallest over waves of a wave's ceil(k / waves)-th largest),
-// then only the present keys >= T are compacted to the front and ranked by
-// counting.  Same contract as block_top_keys.  Kept out of line: the common
-// small sets take the inlined counting paths.
+// kBlock): the keys are dealt round-robin over the waves, so each wave holds
+// about n / waves of them, and each wave's ceil(k / waves)-th largest thread
+// maximum is found (that many rounds of wave maxima); the smallest of those,
+// T, has at least k present keys at or above it (every wave holds that many
+// distinct thread maxima >= T), so only the keys >= T are compacted to the
+// front and ranked by counting, by wave 0 alone when at most a wave's width
+// of them remain.  A wave with too few keys gives T = 0 (every key ranked).
+// Same contract as block_top_keys.  Kept out of line: the common small sets
+// take the inlined counting paths.
 template <int kBlock>
 __device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
   constexpr int kW = kBlock / kWave;
-  __shared__ uint64_t bnd_s[2][kW];
+  __shared__ uint64_t bnd_s[kW];
   __shared__ int cnt_s;
   const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
   uint64_t mk[kRankPerThread];
   uint64_t tmax = 0;
 #pragma unroll
   for (int j = 0; j < kRankPerThread; ++j) {
-    const int i = threadIdx.x + j * kBlock;
+    const int i = j * kBlock + lane * kW + w;
     mk[j] = i < n ? key[i] : 0;
     tmax = mk[j] > tmax ? mk[j] : tmax;
   }
-  uint64_t tk, tq;
-  wave_key_order_stats(tmax, k, (k + kW - 1) / kW, tk, tq);
-  if (lane == 0) {
-    bnd_s[0][w] = tk;
-    bnd_s[1][w] = tq;
-  }
+  const int kq = (k + kW - 1) / kW;
+  uint64_t tq, unused;
+  wave_key_order_stats(tmax, kq, kq, tq, unused);
+  if (lane == 0) bnd_s[w] = tq;
   if (threadIdx.x == 0) cnt_s = 0;
   __syncthreads();
-  uint64_t T = 0, Tq = ~0ull;
+  uint64_t T = ~0ull;
 #pragma unroll
-  for (int i = 0; i < kW; ++i) {
-    T = bnd_s[0][i] > T ? bnd_s[0][i] : T;
-    Tq = bnd_s[1][i] < Tq ? bnd_s[1][i] : Tq;
-  }
-  T = Tq > T ? Tq : T;
+  for (int i = 0; i < kW; ++i) T = bnd_s[i] < T ? bnd_s[i] : T;
 #pragma unroll
   for (int j = 0; j < kRankPerThread; ++j)
     if (mk[j] != 0 && mk[j] >= T) key[atomicAdd(&cnt_s, 1)] = mk[j];
   __syncthreads();
   const int c = cnt_s;
   for (int j = c + threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
-  if (c > 2 * kBlock)
+  if (c <= kWave) {
+    // wave 0: lane l ranks candidate l against the others through lane reads
+    if (w == 0) {
+      const uint64_t mine = lane < c ? key[lane] : 0;
+      const uint32_t mlo = (uint32_t)mine, mhi = (uint32_t)(mine >> 32);
+      int r = 0;
+      for (int j = 0; j < c; ++j) {
+        const uint64_t o =
+            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)mhi, j) << 32) |
+            (uint32_t)__builtin_amdgcn_readlane((int)mlo, j);
+        r += o > mine ? 1 : 0;
+      }
+      if (lane < c && r < k) key[r] = mine;
+    }
+    __syncthreads();
+  } else if (c > 2 * kBlock) {
     block_top_keys_r<kBlock, 4>(key, c, k);
-  else if (c > kBlock)
+  } else if (c > kBlock) {
     block_top_keys_r<kBlock, 2>(key, c, k);
-  else
+  } else {
     block_top_keys_r<kBlock, 1>(key, c, k);
+  }
 }
 
+// sets of more keys than this take block_select_top for k <= 16
+constexpr int kSelectFrom = 128;
 template <int kBlock>
 __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
   if (n > kRankPerThread * kBlock) {
     block_bitonic_desc(key, P2);
-  } else if ((k <= 16 && n > kBlock) || (k <= kWave && n > 2 * kBlock)) {
+  } else if ((k <= 16 && n > kSelectFrom) || (k <= kWave && n > 2 * kBlock)) {
     block_select_top<kBlock>(key, n, k);
   } else if (n > 2 * kBlock) {
     block_top_keys_r<kBlock, 4>(key, n, k);
