@@ -160,9 +160,10 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
     td[i] = v < nt ? tree.depth[base + v] : 0;
     tc[i] = v < nt ? tree.cum[base + v] : 0.0f;
   }
+  const int fv = tid < F ? fr[tid] : 0;  // before the frontier's live size arrives
   bool bad = nb < 0 || nb > cap;
   for (int f = tid; f < Fb; f += kThreads) {
-    const int v = fr[f];
+    const int v = f == tid ? fv : fr[f];
     fr_s[f] = v;
     bad |= v < -1 || v >= nb;
   }
@@ -222,23 +223,41 @@ __global__ __launch_bounds__(kThreads) void ngram_expand_kernel(
 
   // ---- latest longest match of every node.  The first token decides almost
   // every position: a thread compares its prompt tokens (registers) for every
-  // node and extends only the hits.  Key (length, position), larger is better.
+  // node, then extends all of its hits together, one suffix token per round
+  // (one LDS round trip for every hit of the thread), until no hit of the
+  // wave extends.  Key (length, position), larger is better.
   if (in_lds) {
     for (int f = 0; f < Fb; ++f) {
       const int32_t *sf = suf + f * n_max;
       const int pl = plen[f];
       const int32_t s0 = sf[0];
-      uint32_t mine = 0;  // length << 27 | position (positions < kCtxLds)
+      int len[kCtxPer];  // matched length at position tid + i * kThreads, 0 = no hit
+      bool hit = false;
 #pragma unroll
       for (int i = 0; i < kCtxPer; ++i) {
         const int j = tid + i * kThreads;
-        if (j < Lb && cr[i] == s0) {
-          int l = 1;
-          const int lim = min(pl, j + 1);
-          while (l < lim && ctx_s[j - l] == sf[l]) ++l;
-          const uint32_t key = ((uint32_t)l << 27) | (uint32_t)j;
-          mine = key > mine ? key : mine;
+        len[i] = j < Lb && cr[i] == s0 ? 1 : 0;
+        hit |= len[i] != 0;
+      }
+      if (!__any(hit)) continue;
+      for (int l = 1; l < pl; ++l) {
+        const int32_t want = sf[l];
+        bool ext = false;
+#pragma unroll
+        for (int i = 0; i < kCtxPer; ++i) {
+          const int j = tid + i * kThreads;
+          if (len[i] == l && j >= l && ctx_s[j - l] == want) {
+            len[i] = l + 1;
+            ext = true;
+          }
         }
+        if (!__any(ext)) break;
+      }
+      uint32_t mine = 0;  // length << 27 | position (positions < kCtxLds)
+#pragma unroll
+      for (int i = 0; i < kCtxPer; ++i) {
+        const uint32_t key = ((uint32_t)len[i] << 27) | (uint32_t)(tid + i * kThreads);
+        mine = len[i] != 0 && key > mine ? key : mine;
       }
       mine = wave_max_u32(mine);
       if (lane == 0 && mine)
