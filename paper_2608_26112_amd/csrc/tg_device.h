@@ -357,12 +357,64 @@ __device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
   }
 }
 
+// block_top_keys for 1 <= k <= 16 and at most one key per thread: the keys
+// are dealt round-robin over the waves; each wave ranks its own keys against
+// its own (LDS broadcasts of a quarter of the set, no barrier) and keeps
+// those of local rank < k (a key of the k largest has fewer than k larger
+// keys in its wave), then wave 0 ranks the at most waves * k survivors the
+// same way and writes the result.  Two barriers.  Same contract as
+// block_top_keys.
+template <int kBlock>
+__device__ void block_small_top(uint64_t *key, int n, int k) {
+  constexpr int kW = kBlock / kWave;
+  static_assert(kW * 16 <= kWave, "survivors fit one wave");
+  __shared__ uint64_t cand_s[kW * 16];
+  __shared__ int ncand_s[kW];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const int i = lane * kW + w;
+  const uint64_t mine = i < n ? key[i] : 0;
+  const int nw = n > w ? (n - w + kW - 1) / kW : 0;  // keys of this wave: key[j * kW + w]
+  int r = 0;
+  int j = 0;
+#pragma unroll 4
+  for (; j + 1 < nw; j += 2) {
+    const uint64_t a = key[j * kW + w], c = key[(j + 1) * kW + w];
+    r += (int)(a > mine) + (int)(c > mine);
+  }
+  if (j < nw) r += (int)(key[j * kW + w] > mine);
+  const int present = __builtin_popcountll(__ballot(mine != 0));
+  const int nc = present < k ? present : k;
+  if (mine != 0 && r < k) cand_s[w * k + r] = mine;
+  if (lane >= nc && lane < k) cand_s[w * k + lane] = 0;
+  if (lane == 0) ncand_s[w] = nc;
+  __syncthreads();
+  if (w == 0) {
+    const int m = kW * k;
+    const uint64_t c = lane < m ? cand_s[lane] : 0;
+    int tot = 0;
+#pragma unroll
+    for (int u = 0; u < kW; ++u) tot += ncand_s[u];
+    int rr = 0;
+    int u = 0;
+#pragma unroll 4
+    for (; u + 1 < m; u += 2) rr += (int)(cand_s[u] > c) + (int)(cand_s[u + 1] > c);
+    if (u < m) rr += (int)(cand_s[u] > c);
+    if (c != 0 && rr < k) key[rr] = c;
+    if (lane >= tot && lane < k && lane < n) key[lane] = 0;
+  }
+  __syncthreads();
+}
+
 // sets of more keys than this take block_select_top for k <= 16
 constexpr int kSelectFrom = 128;
+// ... and sets of more keys than this, up to one per thread, block_small_top
+constexpr int kSmallFrom = 32;
 template <int kBlock>
 __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
   if (n > kRankPerThread * kBlock) {
     block_bitonic_desc(key, P2);
+  } else if (k >= 1 && k <= 16 && n > kSmallFrom && n <= kBlock) {
+    block_small_top<kBlock>(key, n, k);
   } else if ((k <= 16 && n > kSelectFrom) || (k <= kWave && n > 2 * kBlock)) {
     block_select_top<kBlock>(key, n, k);
   } else if (n > 2 * kBlock) {
