@@ -405,9 +405,8 @@ __device__ void block_small_top(uint64_t *key, int n, int k) {
   __syncthreads();
 }
 
-// sets of more keys than this take block_select_top for k <= 16
-constexpr int kSelectFrom = 128;
-// ... and sets of more keys than this, up to one per thread, block_small_top
+// sets of more keys than this, up to one per thread, take block_small_top
+// for k <= 16 (larger ones block_select_top)
 constexpr int kSmallFrom = 32;
 template <int kBlock>
 __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
@@ -415,7 +414,7 @@ __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
     block_bitonic_desc(key, P2);
   } else if (k >= 1 && k <= 16 && n > kSmallFrom && n <= kBlock) {
     block_small_top<kBlock>(key, n, k);
-  } else if ((k <= 16 && n > kSelectFrom) || (k <= kWave && n > 2 * kBlock)) {
+  } else if ((k <= 16 && n > kBlock) || (k <= kWave && n > 2 * kBlock)) {
     block_select_top<kBlock>(key, n, k);
   } else if (n > 2 * kBlock) {
     block_top_keys_r<kBlock, 4>(key, n, k);

@@ -458,26 +458,59 @@ __global__ __launch_bounds__(kThreads) void rescore_tree_kernel(
   if (badtok) report(d_err, TG_DERR_BAD_NODE);
   if (nonfin) report(d_err, TG_DERR_NONFINITE);
 
-  // ---- cum recompute, parents before children: rounds of "every pool node
-  // whose parent is final takes cum[parent] + logp" (one round per level)
-  for (;;) {
-    // phase 1: decide who is ready from the previous round's state
-    uint32_t ready = 0;  // bit i <-> node tid + i * kThreads
-    int pending = 0;
-    for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
-      if (!inC[v] || done[v]) continue;
-      const int p = par_s[v];
-      if (p < 0 || done[p]) ready |= 1u << i;
-      else pending = 1;
+  // ---- cum recompute, parents before children.  Each pool node walks up to
+  // its nearest ancestor outside the pool (or the root), up to kChain steps,
+  // and folds the logps of the path down from there: the same additions in
+  // the same order as level by level, with no barrier.  Nodes further below
+  // the pool's edge are finished by rounds of "every pool node whose parent
+  // is final takes cum[parent] + logp" (one round per level).
+  constexpr int kChain = 16;
+  bool deep = false;
+  for (int v = tid; v < nb; v += kThreads) {
+    if (!inC[v]) continue;
+    int ch[kChain];
+    int len = 0, u = v;
+    bool up = true;
+#pragma unroll
+    for (int t = 0; t < kChain; ++t) {
+      if (up) {
+        ch[t] = u;
+        len = t + 1;
+        u = par_s[u];
+        up = u >= 0 && inC[u];
+      }
     }
-    __syncthreads();
-    for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
-      if (!(ready >> i & 1u)) continue;
-      const int p = par_s[v];
-      cum_s[v] = __fadd_rn(p < 0 ? 0.0f : cum_s[p], lp_s[v]);
-      done[v] = 1;
+    if (up) {  // the pool continues above kChain levels
+      deep = true;
+      continue;
     }
-    if (!__syncthreads_or(pending)) break;
+    float c = u < 0 ? 0.0f : cum_s[u];
+#pragma unroll
+    for (int t = kChain - 1; t >= 0; --t)
+      if (t < len) c = __fadd_rn(c, lp_s[ch[t]]);
+    cum_s[v] = c;
+    done[v] = 1;
+  }
+  if (__syncthreads_or(deep)) {
+    for (;;) {
+      // phase 1: decide who is ready from the previous round's state
+      uint32_t ready = 0;  // bit i <-> node tid + i * kThreads
+      int pending = 0;
+      for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
+        if (!inC[v] || done[v]) continue;
+        const int p = par_s[v];
+        if (p < 0 || done[p]) ready |= 1u << i;
+        else pending = 1;
+      }
+      __syncthreads();
+      for (int i = 0, v = tid; v < nb; ++i, v += kThreads) {
+        if (!(ready >> i & 1u)) continue;
+        const int p = par_s[v];
+        cum_s[v] = __fadd_rn(p < 0 ? 0.0f : cum_s[p], lp_s[v]);
+        done[v] = 1;
+      }
+      if (!__syncthreads_or(pending)) break;
+    }
   }
 
   // ---- reselection: Top_W(C) by (cum desc, depth asc, id asc)

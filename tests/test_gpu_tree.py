@@ -429,6 +429,34 @@ def test_rescore_identical_drafter_and_all_visited(tg):
     assert np.all(np.isnan(lse.cpu().numpy()))
 
 
+def test_rescore_deep_pool_chains(tg):
+    """Pool paths deeper than the rescore kernel's per-thread walk (16 pool
+    levels above a node): a 45-node chain and a 20-node branch hanging from
+    its sixth node, the first three chain nodes visited (the rest and the
+    branch form the pool), plus a second tree whose pool is shallow."""
+    g = W.rng(91)
+    V, cap = 400, 256
+    t = OT.Tree.empty(2, cap)
+    par = [[-1] + list(range(0, 44)) + [5] + list(range(45, 64)),
+           [-1, -1, 0, 0, 1, 2, 3, 3, 5, 6]]
+    for b, pb in enumerate(par):
+        n = len(pb)
+        t.parent[b, :n] = pb
+        for v, p in enumerate(pb):
+            t.depth[b, v] = 1 if p < 0 else t.depth[b, p] + 1
+            t.token[b, v] = int(g.integers(0, V))
+            t.logp[b, v] = np.float32(-g.random() * 4.0)
+            t.cum[b, v] = t.logp[b, v] if p < 0 else np.float32(t.cum[b, p] + t.logp[b, v])
+        t.n_nodes[b] = n
+        t.root_visited[b] = 1
+    t.visited[0, :3] = 1
+    t.visited[1, :2] = 1
+    R = int(t.n_nodes.max()) + 1
+    strong = W.normal(g, (2, R, V), 3.0)
+    got, _, _, ng, err = run_rescore(tg, t, strong, 5, 3)
+    assert err == 0 and list(ng) == [5, 5]
+
+
 def test_rescore_capacity_and_rows_errors(tg):
     tree, _ = C.scored_tree(8, 2, 50, steps=2, width=3, K=3, cap=20)  # 3 + 9 = 12 nodes
     strong = W.normal(W.rng(2), (2, 13, 50), 2.0)
