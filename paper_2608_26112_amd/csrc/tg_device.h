@@ -319,8 +319,28 @@ __device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
     tmax = mk[j] > tmax ? mk[j] : tmax;
   }
   const int kq = (k + kW - 1) / kW;
-  uint64_t tq, unused;
-  wave_key_order_stats(tmax, kq, kq, tq, unused);
+  uint64_t tq = 0;
+  if (kq <= 4) {
+    uint64_t unused;
+    wave_key_order_stats(tmax, kq, kq, tq, unused);
+  } else {
+    // the kq-th largest thread maximum of the wave by counting the larger
+    // ones among the wave's 64 (LDS broadcasts within the wave)
+    __shared__ uint64_t tm_s[kW][kWave];
+    tm_s[w][lane] = tmax;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    int r = 0;
+#pragma unroll 8
+    for (int j = 0; j < kWave; ++j) r += (int)(tm_s[w][j] > tmax);
+    const uint64_t hit = __ballot(tmax != 0 && r == kq - 1);
+    if (hit) {
+      const int src = __builtin_ctzll(hit);
+      tq = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(tmax >> 32), src) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)tmax, src);
+    }
+  }
   if (lane == 0) bnd_s[w] = tq;
   if (threadIdx.x == 0) cnt_s = 0;
   __syncthreads();
