@@ -287,11 +287,6 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
     }
     __syncthreads();
     if (tid < K) run[tid] = 0;
-    if (tid == 0) {
-      float M = gm[0], S = gs[0];
-      for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[i], gs[i]);
-      part_ms[(size_t)slot * n_grains + gr] = make_float2(M, S);
-    }
     float T = key_threshold(cand[K - 1]), Tq = lmaxq[0];
 #pragma unroll
     for (int i = 0; i < kWavesPerBlock; ++i) {
@@ -329,6 +324,14 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
 
     // ---- 5. rank the running list (empty on a chunk's first grain) and
     // the candidates; keys are distinct (distinct tokens)
+    // the grain's (max, sum-exp) from the wave partials, by the last thread
+    // (its wave has no candidate to rank unless the candidates nearly fill
+    // the block)
+    if (tid == kThreads - 1) {
+      float M = gm[0], S = gs[0];
+      for (int i = 1; i < kWavesPerBlock; ++i) merge_ms(M, S, gm[i], gs[i]);
+      part_ms[(size_t)slot * n_grains + gr] = make_float2(M, S);
+    }
     const int r0 = gr == g_beg ? K : 0;
     const int total = K + n;
     for (int t = r0 + tid; t < total; t += kThreads) {
