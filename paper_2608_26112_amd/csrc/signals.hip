@@ -211,10 +211,22 @@ __global__ __launch_bounds__(kThreads) void signals_kernel(
   if (one_wave) {
     t[0] = red[0][0];
     for (int j = 1; j < kWaves; ++j) t[0] += red[0][j];
-#pragma unroll
-    for (int i = 1; i < kSums; ++i) t[i] = wave_sum_f32(sums[i]);
+    // a lane holds at most one frontier and one preview slot, so the six
+    // counts are 0 or 1 per lane and at most 64 in total: a byte each in two
+    // integer sums (the same totals as float sums of the counts)
+    const int ca = (int)sums[2] | ((int)sums[3] << 8) | ((int)sums[5] << 16) | ((int)sums[6] << 24);
+    const int cb = (int)sums[7] | ((int)nh_f << 8);
+    const int ta = wave_sum_i32(ca), tb = wave_sum_i32(cb);
+    t[1] = wave_sum_f32(sums[1]);
+    t[4] = wave_sum_f32(sums[4]);
+    t[8] = wave_sum_f32(sums[8]);
+    t[2] = (float)(ta & 255);
+    t[3] = (float)((ta >> 8) & 255);
+    t[5] = (float)((ta >> 16) & 255);
+    t[6] = (float)((ta >> 24) & 255);
+    t[7] = (float)(tb & 255);
+    nh = (tb >> 8) & 255;
     fmx = wave_max_f32(mx);
-    nh = (int)wave_sum_f32(nh_f);
   } else {
 #pragma unroll
     for (int i = 0; i < kSums; ++i) {
