@@ -37,9 +37,9 @@ __global__ __launch_bounds__(kThreads) void ngram_cache_kernel(
   const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
   const long long r = (long long)blockIdx.x * kWaves + w;
   if (r >= rows) return;  // wave-uniform
-  float lse = 0.0f;
-  if (lane == 0) lse = finish_lse(part_ms + r * n_ms, n_ms);
-  lse = __shfl(lse, 0, kWave);
+  const float2 *ms = part_ms + r * n_ms;
+  const float lse = wave_fold_lse(
+      ms, n_ms, lane < n_ms ? ms[lane] : make_float2(-__builtin_inff(), 0.0f));
   const uint64_t key =
       wave_finish_topk(part_keys + r * chunks * m, chunks, m, wsmem + (size_t)w * chunks * m);
   if (lane < m) {

@@ -352,9 +352,9 @@ __global__ __launch_bounds__(kThreads) void row_partial_kernel(
 }
 
 // One wave per row slot, live by the row pass's rule: the row's
-// log-sum-exp from its grain partials, folded in grain order (the lanes load
-// them, the fold reads them lane by lane: the same bits as a serial pass),
-// and its top-K from the chunk lists (staged in LDS, K-round merge).  The
+// log-sum-exp from its grain partials (wave_fold_lse: a fixed pairwise tree
+// over the grains, the same bits whatever the chunking), and its top-K from
+// the chunk lists (staged in LDS, K-round merge).  The
 // partials and up to 256 list keys are loaded before the row's liveness is
 // known (the workspace holds every row), so one round trip covers both.
 // Writes lse[s] and out_keys[s * K + j], best first.
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(kThreads) void row_finish_kernel(
   const float2 *ms = part_ms + s * n_ms;
   const uint64_t *lists = part_keys + s * chunks * K;
   const int nk = chunks * K;
-  float2 p = lane < n_ms ? ms[lane] : make_float2(-__builtin_inff(), 0.0f);
+  const float2 p = lane < n_ms ? ms[lane] : make_float2(-__builtin_inff(), 0.0f);
   uint64_t t[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
@@ -398,16 +398,9 @@ __global__ __launch_bounds__(kThreads) void row_finish_kernel(
   } else {
     key = wave_finish_topk(lists, chunks, K, ws);
   }
-  float m = -__builtin_inff(), sum = 0.0f;
-  for (int i0 = 0; i0 < n_ms; i0 += kWave) {
-    if (i0 > 0) p = i0 + lane < n_ms ? ms[i0 + lane] : make_float2(-__builtin_inff(), 0.0f);
-    const int cnt = min(kWave, n_ms - i0);
-    for (int i = 0; i < cnt; ++i)
-      merge_ms(m, sum, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p.x), i)),
-               __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p.y), i)));
-  }
+  const float l = wave_fold_lse(ms, n_ms, p);
   if (lane < K) out_keys[s * K + lane] = key;
-  if (lane == 0) lse[s] = m == -__builtin_inff() ? -__builtin_inff() : m + logf(sum);
+  if (lane == 0) lse[s] = l;
 }
 
 }  // namespace

@@ -106,11 +106,15 @@ __device__ __forceinline__ T wave_reduce(T v, T id, Op op) {
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   return wave_reduce(v, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
 }
-// 64-bit keys: the high words first, then the low words of the lanes that
-// hold the high maximum.
+// 64-bit keys: the high words first, then (unless one lane holds the high
+// maximum) the low words of the lanes that hold it.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   const uint32_t hi = (uint32_t)(v >> 32);
   const uint32_t mh = wave_max_u32(hi);
+  const uint64_t at = __ballot(hi == mh);
+  if (__builtin_popcountll(at) == 1)  // one lane holds the high maximum: its key
+    return ((uint64_t)mh << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, __builtin_ctzll(at));
   const uint32_t ml = wave_max_u32(hi == mh ? (uint32_t)v : 0u);
   return ((uint64_t)mh << 32) | ml;
 }
@@ -446,14 +450,27 @@ __device__ void block_top_keys(uint64_t *key, int n, int P2, int k) {
 }
 
 // ------------------------------------------------------- finishing rows
-// log-sum-exp of one row from its per-grain (max, sum-exp) partials, folded
-// in grain order (the same bits whatever the call's chunking).
-__device__ inline float finish_lse(const float2 *__restrict__ ms, int n) {
+// log-sum-exp of one row from its per-grain (max, sum-exp) partials, by one
+// wave (every lane calls it; the result is the same in all): the grains 64
+// at a time, each batch folded as a fixed pairwise tree over the lanes (lane
+// l takes lane l + d for d = 1, 2, 4, ... while l is a multiple of 2d), the
+// batches in order.  The partials are per grain, so this is the same bits
+// whatever the call's chunking.  `first` is the lane's partial of the first
+// batch (ms[lane] for lane < n, already loaded by the caller).
+__device__ inline float wave_fold_lse(const float2 *__restrict__ ms, int n, float2 first) {
+  const int lane = threadIdx.x & (kWave - 1);
   float m = -__builtin_inff(), s = 0.0f;
-#pragma unroll 8
-  for (int i = 0; i < n; ++i) {
-    const float2 p = ms[i];
-    merge_ms(m, s, p.x, p.y);
+  for (int i0 = 0; i0 < n; i0 += kWave) {
+    const int cnt = n - i0 < kWave ? n - i0 : kWave;
+    float2 p = first;
+    if (i0 > 0) p = lane < cnt ? ms[i0 + lane] : make_float2(-__builtin_inff(), 0.0f);
+    float bm = p.x, bs = p.y;
+    for (int d = 1; d < cnt; d <<= 1) {
+      const float om = __shfl_down(bm, d, kWave), os = __shfl_down(bs, d, kWave);
+      if ((lane & (2 * d - 1)) == 0 && lane + d < cnt) merge_ms(bm, bs, om, os);
+    }
+    merge_ms(m, s, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bm), 0)),
+             __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bs), 0)));
   }
   return m == -__builtin_inff() ? -__builtin_inff() : m + logf(s);
 }

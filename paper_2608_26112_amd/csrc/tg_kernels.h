@@ -49,7 +49,7 @@ hipError_t launch_row_partials(const float *logits, int B, int rows_per_batch,
                                float2 *part_ms, uint64_t *part_keys,
                                uint32_t *d_err, hipStream_t stream);
 
-// Finishes the same live rows: lse[s] (grain order) and the row's top-K keys
+// Finishes the same live rows: lse[s] (a fixed fold of the grain partials) and the row's top-K keys
 // out_keys[s * K + j], best first (one wave per row over the whole chip).
 hipError_t launch_row_finish(int B, int rows_per_batch, int K, RowPlan plan,
                              const int32_t *n_live, const uint8_t *needed,
