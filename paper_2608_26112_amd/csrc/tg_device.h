@@ -358,17 +358,15 @@ __device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
   const int c = cnt_s;
   for (int j = c + threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
   if (c <= kWave) {
-    // wave 0: lane l ranks candidate l against the others through lane reads
+    // wave 0: lane l ranks candidate l against the others (LDS broadcasts;
+    // the wave's reads are done before its writes, in issue order)
     if (w == 0) {
       const uint64_t mine = lane < c ? key[lane] : 0;
-      const uint32_t mlo = (uint32_t)mine, mhi = (uint32_t)(mine >> 32);
       int r = 0;
-      for (int j = 0; j < c; ++j) {
-        const uint64_t o =
-            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)mhi, j) << 32) |
-            (uint32_t)__builtin_amdgcn_readlane((int)mlo, j);
-        r += o > mine ? 1 : 0;
-      }
+      int u = 0;
+#pragma unroll 4
+      for (; u + 1 < c; u += 2) r += (int)(key[u] > mine) + (int)(key[u + 1] > mine);
+      if (u < c) r += (int)(key[u] > mine);
       if (lane < c && r < k) key[r] = mine;
     }
     __syncthreads();
