@@ -192,8 +192,8 @@ constexpr int kRankPerThread = 4;  // keys a thread ranks (sets up to 4 * block)
 
 // r[j] = how many of key[0..n) are larger than mk[j] = key[threadIdx.x +
 // j * kBlock] (~0, ranking nothing, past n).  n <= R * kBlock.
-template <int kBlock, int R>
-__device__ __forceinline__ void count_larger(const uint64_t *key, int n, uint64_t (&mk)[R],
+template <int kBlock, int R, typename P>
+__device__ __forceinline__ void count_larger(P key, int n, uint64_t (&mk)[R],
                                              int (&r)[R]) {
 #pragma unroll
   for (int j = 0; j < R; ++j) {
@@ -244,11 +244,11 @@ __device__ __forceinline__ void rank_each(const uint64_t *key, int n, Fn f) {
 // ranked by counting (each thread compares as many keys as the set needs),
 // larger ones sorted whole: then key[n..P2) must hold 0, P2 a power of two
 // >= n.  Callers synchronise before; ends synchronised.
-template <int kBlock, int R>
-__device__ void block_top_keys_r(uint64_t *key, int n, int k) {
+template <int kBlock, int R, typename P>
+__device__ void block_top_keys_r(P key, int n, int k) {
   uint64_t mk[R];
   int r[R];
-  count_larger<kBlock, R>(key, n, mk, r);
+  count_larger<kBlock, R, P>(key, n, mk, r);
   __syncthreads();
   for (int j = threadIdx.x; j < k && j < n; j += kBlock) key[j] = 0;
   __syncthreads();
@@ -309,7 +309,11 @@ __device__ __forceinline__ void wave_key_order_stats(uint64_t v, int k, int kq, 
 // Same contract as block_top_keys.  Kept out of line: the common small sets
 // take the inlined counting paths.
 template <int kBlock>
-__device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
+__device__ __noinline__ void block_select_top(uint64_t *key_generic, int n, int k) {
+  // out of line, so a generic pointer would cost an address conversion (with
+  // a null check) per access; the keys live in LDS
+  using lds_u64 = __attribute__((address_space(3))) uint64_t;
+  lds_u64 *key = (lds_u64 *)key_generic;
   constexpr int kW = kBlock / kWave;
   __shared__ uint64_t bnd_s[kW];
   __shared__ int cnt_s;
@@ -371,11 +375,11 @@ __device__ __noinline__ void block_select_top(uint64_t *key, int n, int k) {
     }
     __syncthreads();
   } else if (c > 2 * kBlock) {
-    block_top_keys_r<kBlock, 4>(key, c, k);
+    block_top_keys_r<kBlock, 4, lds_u64 *>(key, c, k);
   } else if (c > kBlock) {
-    block_top_keys_r<kBlock, 2>(key, c, k);
+    block_top_keys_r<kBlock, 2, lds_u64 *>(key, c, k);
   } else {
-    block_top_keys_r<kBlock, 1>(key, c, k);
+    block_top_keys_r<kBlock, 1, lds_u64 *>(key, c, k);
   }
 }
 
