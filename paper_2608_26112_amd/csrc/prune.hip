@@ -128,7 +128,8 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   for (int v = tid; v < nn; v += kThreads) flag[v] = 0;
   __syncthreads();
 
-  // ---- keep
+  // ---- keep (`sel`: the kept set is key[0, B_ver), selected below)
+  bool sel = false;
   if (nn <= B_ver) {
     for (int v = tid; v < nn; v += kThreads) flag[v] = 1;
   } else {
@@ -145,7 +146,9 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
         block_select_top<kThreads>(key, nn, B_ver);
       else
         block_top_keys<kThreads>(key, nn, P2, B_ver);
-      for (int i = tid; i < B_ver; i += kThreads) flag[node_key_id(key[i])] = 1;
+      sel = B_ver <= kWave;
+      if (!sel)
+        for (int i = tid; i < B_ver; i += kThreads) flag[node_key_id(key[i])] = 1;
     } else {
       // exact ranks (counting for up to kRankCountMax nodes, else a bitonic
       // sort), then the literal loop: add each ranked node's missing
@@ -172,35 +175,57 @@ __global__ __launch_bounds__(kThreads) void prune_kernel(
   }
   __syncthreads();
 
-  // ---- re-index the kept nodes by (depth, id): compact them (id order),
-  // then rank the compacted keys
-  const int per_c = (nn + kThreads - 1) / kThreads;
-  const int c_lo = min(nn, tid * per_c), c_hi = min(nn, c_lo + per_c);
-  int mine_k = 0;
-  for (int v = c_lo; v < c_hi; ++v) mine_k += flag[v];
-  int nk_total = 0;
-  int pos = block_exclusive_scan<kThreads>(mine_k, cnt, nk_total);
-  for (int v = c_lo; v < c_hi; ++v)
-    if (flag[v]) key[pos++] = ~(((uint64_t)depth[v] << 32) | (uint64_t)v);
+  // ---- re-index the kept nodes by (depth, id)
   for (int v = tid; v < nn; v += kThreads) newid[v] = 0;
-  if (tid == 0) nk_s = nk_total;
-  __syncthreads();
-  const int nk = nk_s;
-  if (nk <= kRankCountMax) {
-    rank_each<kThreads>(key, nk, [&](int, uint64_t k, int r) {
-      const int v = (int)(uint32_t)~k;
-      order[r] = (int16_t)v;
-      newid[v] = (int16_t)(r + 1);
-    });
+  int nk;
+  if (sel) {
+    // the selected set (at most a wave's width): wave 0 ranks (depth, id)
+    // packed in 32 bits (both below 2^16) against the set
+    nk = B_ver;
+    __syncthreads();  // newid cleared before the kept nodes' entries land
+    if (tid < kWave) {
+      const int v = tid < nk ? node_key_id(key[tid]) : 0;
+      const uint32_t dk = tid < nk ? ((uint32_t)depth[v] << 16) | (uint32_t)v : ~0u;
+      cnt[tid] = (int)dk;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      int r = 0;
+      for (int j = 0; j < nk; ++j) r += (uint32_t)cnt[j] < dk ? 1 : 0;
+      if (tid < nk) {
+        order[r] = (int16_t)v;
+        newid[v] = (int16_t)(r + 1);
+      }
+    }
   } else {
-    const int P2k = pow2_at_least(nk);
-    for (int i = nk + tid; i < P2k; i += kThreads) key[i] = 0;
+    // compact them (id order), then rank the compacted keys
+    const int per_c = (nn + kThreads - 1) / kThreads;
+    const int c_lo = min(nn, tid * per_c), c_hi = min(nn, c_lo + per_c);
+    int mine_k = 0;
+    for (int v = c_lo; v < c_hi; ++v) mine_k += flag[v];
+    int nk_total = 0;
+    int pos = block_exclusive_scan<kThreads>(mine_k, cnt, nk_total);
+    for (int v = c_lo; v < c_hi; ++v)
+      if (flag[v]) key[pos++] = ~(((uint64_t)depth[v] << 32) | (uint64_t)v);
+    if (tid == 0) nk_s = nk_total;
     __syncthreads();
-    block_bitonic_desc(key, P2k);
-    for (int j = tid; j < nk; j += kThreads) {
-      const int v = (int)(uint32_t)~key[j];
-      order[j] = (int16_t)v;
-      newid[v] = (int16_t)(j + 1);
+    nk = nk_s;
+    if (nk <= kRankCountMax) {
+      rank_each<kThreads>(key, nk, [&](int, uint64_t k, int r) {
+        const int v = (int)(uint32_t)~k;
+        order[r] = (int16_t)v;
+        newid[v] = (int16_t)(r + 1);
+      });
+    } else {
+      const int P2k = pow2_at_least(nk);
+      for (int i = nk + tid; i < P2k; i += kThreads) key[i] = 0;
+      __syncthreads();
+      block_bitonic_desc(key, P2k);
+      for (int j = tid; j < nk; j += kThreads) {
+        const int v = (int)(uint32_t)~key[j];
+        order[j] = (int16_t)v;
+        newid[v] = (int16_t)(j + 1);
+      }
     }
   }
   __syncthreads();
