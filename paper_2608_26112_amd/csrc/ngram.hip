@@ -16,8 +16,8 @@
 //   for each node the block scans the prompt: end position j scores the
 //   length l(j) of the longest common suffix of x[..j] and the node's prefix
 //   (capped at n_max), and the maximum of (l, j) with l >= 1 is the latest
-//   longest match, which is what "longest n-gram first, shorter on a miss,
-//   latest occurrence" selects.  Children take ids n_b + f*K + k, then
+//   longest match: the longest n-gram that occurs, shorter ones only when no
+//   longer one does, at its latest occurrence.  Children take ids n_b + f*K + k, then
 //   Top_N of them by (cum desc, depth asc, id asc).
 #include "tg_device.h"
 #include "tg_kernels.h"
