@@ -16,7 +16,8 @@ Besides the headline, the default run measures every other workload once and
 reports each under `extra` with its own roofline and CPU baseline:
   tiny                the tiny fp32 workload: attention (B1, 4/4 heads, D64,
                       prefix 128, 16 nodes), one expansion (V=1000, F=8, K=4,
-                      N=8) and acceptance, as one step (microseconds)
+                      N=8) and acceptance, as one step (microseconds), timed
+                      as a replayed HIP graph of steps (the eager time beside)
   attn-llama8b        the Llama-3-8B-shaped verify layer (B1, 32/8 heads,
                       prefix 2048, 64 nodes) - one call (split-prefix mode),
                       timed as a replayed HIP graph of calls (the eager loop
@@ -519,13 +520,39 @@ def tiny_bench(tg, torch, dev, steps, warmup, cpu_s):
     path = torch.empty((1, Nn), dtype=torch.int32, device=dev)
     bonus = torch.empty((1,), dtype=torch.int32, device=dev)
 
-    def step(i):
+    def step_on(t):
         tg.verify_attention(q, k, v, dpar, plen, Dh ** -0.5, out=out)
-        tg.expand_topk(trees[i], logits, fr, None, 4, 8, row_lse=lse, next_frontier=nx,
+        tg.expand_topk(t, logits, fr, None, 4, 8, row_lse=lse, next_frontier=nx,
                        n_next=nn, workspace=ws)
         tg.accept(dpar, dtok, nnodes, dgreedy, Nn, accept_len=A, accept_path=path, bonus=bonus)
 
-    ms = time_calls(torch, step, steps, warmup)
+    def step(i):
+        step_on(trees[i])
+
+    ms_eager = time_calls(torch, step, steps, warmup)
+    # the three calls' Python marshalling (~20 us each) outlasts their
+    # kernels, so the eager loop measures the host: the step is timed as one
+    # graph of 8 steps on trees of their own, replayed; each captured step
+    # first puts its tree back to the 16 nodes (a 4-byte device copy), so every
+    # replay expands the same tree, and the replay must give the eager result
+    n_g = 8
+    gtrees = [tg.TreeState(1, 64, dev) for _ in range(n_g)]
+    for t in gtrees:
+        for f in tg.TreeState.FIELDS:
+            getattr(t, f).copy_(getattr(base, f))
+
+    def step_g(i):
+        gtrees[i].n_nodes.copy_(base.n_nodes)
+        step_on(gtrees[i])
+    step_g(0)
+    torch.cuda.synchronize()
+    want = (out.clone(), nx.clone(), gtrees[0].cum.clone(), A.clone())
+    ms_rep, graph = time_graph(torch, step_g, n_g, max(1, steps), warmup)
+    ms = ms_rep / n_g
+    got = (out, nx, gtrees[0].cum, A)
+    if not all(torch.equal(a, b) for a, b in zip(got, want)):
+        raise RuntimeError("graph replay of the tiny step differs from the eager step")
+    del graph
     kern, _ = kernel_times(tg, torch, step, steps, start=warmup + steps)
     nbytes, flops = attn_work("tiny", parent)
     a_us = 1e3 * kern["attn_f32"][1] / kern["attn_f32"][0]
@@ -537,7 +564,9 @@ def tiny_bench(tg, torch, dev, steps, warmup, cpu_s):
     res = line(1e3 * ms, "us", steps, warmup, ms,
                {"workload": "tiny fp32 workload: attention (B1, 4/4 heads, D64, prefix 128, "
                             "16 nodes) + expansion (V=1000, F=8, K=4, N=8) + acceptance"},
-               roof, "f32", higher=False, kernels=kernels_json(kern, steps))
+               roof, "f32", higher=False, kernels=kernels_json(kern, steps),
+               timing=f"one HIP graph of {n_g} steps, replayed {max(1, steps)} times",
+               eager_ms_per_step=ms_eager)
     if cpu_s > 0:
         from oracle import attention as OA
         from oracle import tree as OT
